@@ -32,11 +32,17 @@ READINGS (where the paper is silent; each is also listed in the design notes):
   2^(sigma_i+tau_j-8) G'_ij <= 2^(c-8) <= M/4 and sum_l |A~||B~| <= M/4 +
   slack with slack <= k 2^max(sigma,tau) + k/4 < M/4, so Eq. (M-bound) holds
   per entry (asserted below).
+* The code product is evaluated in k-slabs of 65536 (FP32-exact: a slab sum
+  is at most 256 * 65536 = 2^24) and R_i is the SUM over slabs of the
+  slab-wise row maxima (an upper bound of max_j G'_ij; equal to it for
+  k <= 65536).  Likewise K_j.
 * Fixed mode (no max pass, alpha = 3r): R_i = K_j = 256 k, the literal
   mu = k max|A~| max|B~| of Alg. 1 line "mu <- ...".
 * Quantiser RN is round-half-to-even.
 * Fallback trigger: T1 (non-finite entry) or T2 (a nonzero entry quantises to
-  zero: the row's exponent span exceeds what the scaling certifies).
+  zero: the row's exponent span exceeds what the scaling certifies).  T2 is
+  evaluated only on rows/columns without non-finite entries (T1 rows are not
+  quantised at all).
 """
 from __future__ import annotations
 
@@ -49,6 +55,7 @@ from . import planes as _planes
 from .moduli import moduli as _moduli, modulus_product, width_budget
 
 SIGMA_CAP = 62
+CODE_SLAB = 65536
 
 
 @dataclass
@@ -225,8 +232,12 @@ def dgemm(A, B, r=12, *, rows=None, cols=None, mode="bound", quant="rn",
         # exact: integer terms <= 256 summed over k < 2^44
         R = np.zeros(m, dtype=np.int64)
         K = np.zeros(n, dtype=np.int64)
-        R[rows] = (cAm[rows] @ cBm).max(axis=1).astype(np.int64) if n else 0
-        K[cols] = (cAm @ cBm[:, cols]).max(axis=0).astype(np.int64) if m else 0
+        for l0 in range(0, max(k, 1), CODE_SLAB):
+            sl = slice(l0, min(k, l0 + CODE_SLAB))
+            if n:
+                R[rows] += (cAm[rows, sl] @ cBm[sl]).max(axis=1).astype(np.int64)
+            if m:
+                K[cols] += (cAm[:, sl] @ cBm[sl, cols]).max(axis=0).astype(np.int64)
         sig = widths(R, cA)
         tau = widths(K, cB)
     elif mode == "fixed":
@@ -242,8 +253,9 @@ def dgemm(A, B, r=12, *, rows=None, cols=None, mode="bound", quant="rn",
     # Phase 1: quantisation (only rows/cols needed for the requested block)
     Aq = quantise(np.where(t1A[rows][:, None], 0.0, A[rows]), sA[rows], quant)
     Bq = quantise(np.where(t1B[cols][:, None], 0.0, B[:, cols].T), tB[cols], quant).T
-    t2A = np.any((A[rows] != 0) & np.isfinite(A[rows]) & (Aq == 0), axis=1)
-    t2B = np.any((B[:, cols] != 0) & np.isfinite(B[:, cols]) & (Bq == 0), axis=0)
+    # T2 is evaluated only on rows/columns that are quantised (not T1)
+    t2A = ~t1A[rows] & np.any((A[rows] != 0) & (Aq == 0), axis=1)
+    t2B = ~t1B[cols] & np.any((B[:, cols] != 0) & (Bq == 0), axis=0)
 
     # Eq. (M-bound) for every computed entry: sum_l |A~_il||B~_lj| < M/2.
     # Checked exactly in Python integers for small blocks.
