@@ -1,0 +1,149 @@
+/*
+ * ozaki2.h -- FP64 matrix multiply emulated on CDNA4 (gfx950) FP8 matrix
+ * cores through the CRT-based Ozaki Scheme II.
+ *
+ * Method: Matsuoka, "FP8 is All You Need (Part 1)", arXiv 2606.06510,
+ * Algorithm 1 (Ozaki II dense GEMM at phase level):
+ *   Phase 1  power-of-two row/column scaling to integers, Eq. (scale), with the
+ *            max-magnitude estimation pass (the "+1" of alpha = 3r+1);
+ *   Phase 2  r modular GEMMs, Eq. (modgemm), each as three FP8 plane products
+ *            (Eq. (sq-shortcut) for square moduli, Eq. (kar) for nonsquare
+ *            ones) accumulated exactly in FP32, Eq. (accum-exact);
+ *   Phase 3  CRT reconstruction of the exact integer, Eq. (garner) / (M-bound),
+ *            one rounded conversion back to FP64, and the native-FP64
+ *            fallback for rows the scaling cannot certify.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Layout: column-major (BLAS), no transposes: C (m x n) = A (m x k) * B (k x n).
+ * A, B, C and the workspace are DEVICE pointers owned by the caller; the
+ * library keeps no reference to them after a call returns, except that a plan
+ * borrows A and B from ozaki2_deconstruct until its ozaki2_reconstruct (the
+ * fallback recomputes flagged rows from them).
+ * `stream` is a hipStream_t passed as void* (NULL = the default stream).  Work
+ * is enqueued asynchronously; nothing synchronises except ozaki2_plan_query
+ * and ozaki2_finalize.
+ * Validation happens before any launch: on an error nothing is written.
+ * Asynchronous device faults surface at the caller's next synchronisation.
+ * num_moduli (r) must be in [8, 16]; the moduli are the paper's r = 12 set
+ * (1089, 1024, 961, 841, 625, 529, 511, 509, 503, 499, 491, 487) extended by
+ * the nonsquare 481, 479, 467, 463 and truncated to the r largest.
+ * Limits: m, n, k >= 0 and m*k, k*n, m*n each below 2^40.
+ * Accuracy contract: entries of rows/columns that are not flagged are the
+ * IEEE round-to-nearest-even value of the exact rational D^-1 (A~ B~) E^-1,
+ * where A~ = RN(D A), B~ = RN(B E) are the quantised integer matrices; an
+ * exactly zero result is +0.0.  Flagged rows of A (columns of B) -- any
+ * NaN/Inf (T1), or a nonzero entry that quantises to zero (T2) -- are
+ * recomputed in native FP64 (one fused multiply-add per k, ascending k).
+ */
+#ifndef OZAKI2_H
+#define OZAKI2_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+enum {
+  OZ2_OK = 0,
+  OZ2_E_INVALID = -1,      /* bad size, leading dimension, pointer, r or flags */
+  OZ2_E_NOMEM = -2,        /* internal workspace allocation failed */
+  OZ2_E_DEVICE = -3,       /* a HIP runtime call or a kernel launch failed */
+  OZ2_E_UNSUPPORTED = -4,  /* not a gfx950 device */
+  OZ2_E_WORKSPACE = -5     /* caller workspace NULL or smaller than required */
+};
+
+/* flags (bitwise or) */
+enum {
+  OZ2_ACCUMULATE = 1u,     /* C <- C + A*B: one extra IEEE RN addition per entry */
+  OZ2_SCALE_FIXED = 2u,    /* no max-magnitude pass: mu = k max|A~| max|B~| (alpha = 3r) */
+  OZ2_QUANT_TZ = 4u,       /* quantise by truncation toward zero instead of RN-even */
+  OZ2_NO_FALLBACK = 8u,    /* never recompute flagged rows natively */
+  OZ2_FORCE_FALLBACK = 16u /* recompute every row natively (testing aid) */
+};
+
+/* C = A*B with the default flags (accumulation: ozaki2_dgemm_ex).
+ * Uses a library-internal, grow-only workspace per device (hipMalloc'd on
+ * first use and when a call needs more; released by ozaki2_finalize).  Calls
+ * on one device share it, so concurrent calls on different streams must use
+ * ozaki2_dgemm_ex with workspaces of their own.
+ * Returns OZ2_OK or an error code; on error nothing is enqueued. */
+int ozaki2_dgemm(int m, int n, int k, const double* A, int lda, const double* B,
+                 int ldb, double* C, int ldc, int num_moduli, void* stream);
+
+/* C = A*B, or C = C + A*B with OZ2_ACCUMULATE, using the caller's workspace
+ * (device memory of at least ozaki2_workspace_bytes(m, n, k, r, flags) bytes,
+ * 256-byte aligned; contents on entry are ignored and on exit undefined). */
+int ozaki2_dgemm_ex(int m, int n, int k, const double* A, int lda,
+                    const double* B, int ldb, double* C, int ldc,
+                    int num_moduli, unsigned flags, void* workspace,
+                    size_t ws_bytes, void* stream);
+
+/* batch independent products C_b = A_b * B_b, A_b = A + b*strideA (elements),
+ * likewise B_b, C_b; each with the layout rules above.  Strides must keep the
+ * output matrices disjoint. Internal workspace as for ozaki2_dgemm. */
+int ozaki2_dgemm_strided_batched(int m, int n, int k, const double* A, int lda,
+                                 long long strideA, const double* B, int ldb,
+                                 long long strideB, double* C, int ldc,
+                                 long long strideC, int batch, int num_moduli,
+                                 void* stream);
+
+/* Workspace bytes ozaki2_dgemm_ex / ozaki2_plan_create need (0 on invalid
+ * arguments). */
+size_t ozaki2_workspace_bytes(int m, int n, int k, int num_moduli, unsigned flags);
+
+/* The r moduli in ascending (reconstruction) order into host_out[0..r-1]. */
+int ozaki2_moduli(int num_moduli, int* host_out);
+
+/* ---------------------------------------------------------------- staged API
+ * The three phases of Alg. 1 as separately callable stages over one plan.
+ * A plan borrows a caller workspace (ozaki2_workspace_bytes) and is not
+ * re-entrant; different plans may run on different streams. */
+typedef struct ozaki2_plan_s* ozaki2_plan_t;
+
+int ozaki2_plan_create(ozaki2_plan_t* out, int m, int n, int k, int num_moduli,
+                       unsigned flags, void* workspace, size_t ws_bytes);
+int ozaki2_plan_destroy(ozaki2_plan_t plan);
+
+/* Phase 1: scan (exponents, T1 flags), max-magnitude pass (codes, the code
+ * GEMM on FP8 MFMA, row/column maxima), scales, quantisation, centred
+ * residues and their E4M3 digit planes (T2 flags).  Borrows A and B. */
+int ozaki2_deconstruct(ozaki2_plan_t plan, const double* A, int lda,
+                       const double* B, int ldb, void* stream);
+
+/* Phase 2: the 3r FP8 plane products and their exact modular accumulation;
+ * writes the r centred residues of every output entry into the workspace. */
+int ozaki2_residue_gemm(ozaki2_plan_t plan, void* stream);
+
+/* Phase 3: CRT reconstruction, inverse scaling with one rounding, then the
+ * native-FP64 fallback of flagged rows/columns (reads the A, B given to
+ * ozaki2_deconstruct).  With OZ2_ACCUMULATE in the plan's flags, C += .. */
+int ozaki2_reconstruct(ozaki2_plan_t plan, double* C, int ldc, void* stream);
+
+/* Diagnostics for tests: synchronises the device, then copies a plan
+ * quantity to host memory.  ozaki2_plan_query_bytes gives the size. */
+enum {
+  OZ2_Q_EXPONENTS = 1,     /* int32 E^A[m] then E^B[n] (frexp exponent of row/col max) */
+  OZ2_Q_MAXIMA = 2,        /* uint64 R[m] then K[n] (code-product row/col maxima) */
+  OZ2_Q_SCALES = 3,        /* int32 s[m] then t[n] (power-of-two scales) */
+  OZ2_Q_FLAGS = 4,         /* uint32 flagsA[m] then flagsB[n]: bit0 T1, bit1 T2 */
+  OZ2_Q_CODES = 5,         /* uint8 codes of A [m][k] then of B [n][k] (E4M3 bytes) */
+  OZ2_Q_PLANES = 6,        /* uint8 planes of A [p_store][m][k] then of B [p_store][n][k] */
+  OZ2_Q_RESIDUES = 7,      /* int16 [r][n][m] centred residues (after residue_gemm) */
+  OZ2_Q_INTEGERS = 8,      /* uint32 [n][m][5]: exact integer, two's complement, 160 bits LE */
+  OZ2_Q_FALLBACK_COUNT = 9 /* int32 [2]: flagged rows of A, flagged columns of B */
+};
+size_t ozaki2_plan_query_bytes(ozaki2_plan_t plan, int what);
+int ozaki2_plan_query(ozaki2_plan_t plan, int what, void* host_out, size_t bytes);
+
+const char* ozaki2_status_string(int status);
+
+/* Releases the internal workspaces of ozaki2_dgemm (synchronises). */
+void ozaki2_finalize(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* OZAKI2_H */

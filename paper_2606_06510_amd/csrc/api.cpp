@@ -1,0 +1,602 @@
+// Host orchestration of the Ozaki-II FP8 emulated DGEMM (the C ABI of
+// include/ozaki2.h): argument validation, the per-plan constant table,
+// workspace layout, stage sequencing and test queries.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <vector>
+
+#include "../../include/ozaki2.h"
+#include "oz2_internal.h"
+
+namespace {
+
+// The paper's r = 12 set S (section "The frozen plane kernel") plus the
+// nonsquare extension 481, 479, 467, 463, in descending order; r moduli are
+// the r largest, used in ascending order.
+const int kPool[OZ2_MAXR] = {1089, 1024, 961, 841, 625, 529, 511, 509,
+                             503,  499,  491, 487, 481, 479, 467, 463};
+
+// ------------------------------------------------------------ tiny bigint
+struct Big {
+  std::vector<uint32_t> w;  // little endian, non-negative
+  explicit Big(uint64_t v = 0) {
+    w.push_back((uint32_t)v);
+    w.push_back((uint32_t)(v >> 32));
+    trim();
+  }
+  void trim() {
+    while (w.size() > 1 && w.back() == 0) w.pop_back();
+  }
+  void mul_small(uint32_t f) {
+    uint64_t carry = 0;
+    for (auto& x : w) {
+      uint64_t t = (uint64_t)x * f + carry;
+      x = (uint32_t)t;
+      carry = t >> 32;
+    }
+    if (carry) w.push_back((uint32_t)carry);
+    trim();
+  }
+  uint32_t mod_small(uint32_t m) const {
+    uint64_t r = 0;
+    for (size_t i = w.size(); i-- > 0;) r = ((r << 32) | w[i]) % m;
+    return (uint32_t)r;
+  }
+  void shr1() {
+    for (size_t i = 0; i < w.size(); ++i) {
+      w[i] >>= 1;
+      if (i + 1 < w.size()) w[i] |= (w[i + 1] & 1u) << 31;
+    }
+    trim();
+  }
+  int bitlen() const {
+    int top = (int)w.size() - 1;
+    while (top > 0 && w[top] == 0) --top;
+    if (w[top] == 0) return 0;
+    return 32 * top + (32 - __builtin_clz(w[top]));
+  }
+  uint32_t word(int i) const { return i < (int)w.size() ? w[i] : 0u; }
+};
+
+int64_t inv_mod(int64_t a, int64_t m) {  // a^-1 mod m, gcd(a, m) = 1
+  int64_t t = 0, nt = 1, r = m, nr = ((a % m) + m) % m;
+  while (nr) {
+    int64_t q = r / nr;
+    int64_t x = t - q * nt; t = nt; nt = x;
+    x = r - q * nr; r = nr; nr = x;
+  }
+  return t < 0 ? t + m : t;
+}
+
+bool make_const(int r, Oz2Const& c) {
+  if (r < 8 || r > OZ2_MAXR) return false;
+  std::memset(&c, 0, sizeof(c));
+  std::vector<int> ms(kPool, kPool + r);
+  std::sort(ms.begin(), ms.end());
+  c.r = r;
+  int pb = 0;
+  Big M(1);
+  for (int i = 0; i < r; ++i) M.mul_small((uint32_t)ms[i]);
+  for (int i = 0; i < r; ++i) {
+    const int m = ms[i];
+    int s = (int)std::lround(std::sqrt((double)m));
+    if (s * s != m) s = 0;
+    c.m[i] = m;
+    c.sq[i] = s;
+    c.pbase[i] = pb;
+    pb += s ? 2 : 3;
+    c.c32[i] = (int)((1ull << 32) % (uint64_t)m);
+    if (s) {
+      c.rho0[i] = s;            // chain (d1e0 + d0e1) carries coefficient s, then d0e0 carries 1
+      c.rho1[i] = 0;
+      c.fin[i] = 1;
+    } else {                    // coefficients 240 (d1e1), -15 (d0e0), 16 (sum planes)
+      c.rho0[i] = m - 16;                                         // 240 / -15 = -16
+      c.rho1[i] = (int)(((int64_t)(m - 15) * inv_mod(16, m)) % m);  // -15 / 16
+      c.fin[i] = 16;
+    }
+    c.finv[i] = 1.0f / (float)m;
+    c.finv_s[i] = s ? 1.0f / (float)s : 0.0f;
+    c.dinv[i] = 1.0 / (double)m;
+    // W_i = (M/m_i) * ((M/m_i)^-1 mod m_i)
+    Big Mi(1);
+    for (int j = 0; j < r; ++j)
+      if (j != i) Mi.mul_small((uint32_t)ms[j]);
+    const int64_t inv = inv_mod(Mi.mod_small((uint32_t)m), m);
+    Big Wi = Mi;
+    Wi.mul_small((uint32_t)inv);
+    for (int j = 0; j < OZ2_NLIMB; ++j) c.W[i][j] = (double)Wi.word(j);
+    c.wfrac[i] = (double)inv / (double)m;   // W_i / M exactly = inv_i / m_i
+  }
+  c.P = pb;
+  Big Mh = M;
+  Mh.shr1();
+  for (int j = 0; j < OZ2_NLIMB; ++j) {
+    c.Ml[j] = (double)M.word(j);
+    c.Mhalf[j] = (double)Mh.word(j);
+  }
+  const int cc = (M.bitlen() - 1) + 6;     // floor(log2 M) + 6
+  c.cA = cc / 2;
+  c.cB = cc - c.cA;
+  return true;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+int round_up(int x, int q) { return ((x + q - 1) / q) * q; }
+
+bool make_dims(int m, int n, int k, unsigned flags, Oz2Dims& d) {
+  if (m < 0 || n < 0 || k < 0) return false;
+  d.m = m;
+  d.n = n;
+  d.k = k;
+  d.mp = round_up(std::max(m, 1), OZ2_TILE);
+  d.np = round_up(std::max(n, 1), OZ2_TILE);
+  d.kp = round_up(std::max(k, 1), OZ2_KSTEP);
+  d.cslabs = (d.kp + OZ2_CSLAB - 1) / OZ2_CSLAB;
+  d.flags = flags;
+  const double lim = 1099511627776.0;      // 2^40
+  if ((double)d.mp * d.kp >= lim || (double)d.np * d.kp >= lim || (double)d.mp * d.np >= lim)
+    return false;
+  return true;
+}
+
+Oz2Layout make_layout(const Oz2Dims& d, const Oz2Const& c) {
+  Oz2Layout L;
+  size_t o = 0;
+  auto take = [&o](size_t bytes) { size_t at = o; o = align256(o + bytes); return at; };
+  L.rowbits = take((size_t)d.mp * 8);
+  L.colbits = take((size_t)d.np * 8);
+  L.flagsA = take((size_t)d.mp * 4);
+  L.flagsB = take((size_t)d.np * 4);
+  L.Rmax = take((size_t)d.cslabs * d.mp * 4);
+  L.Kmax = take((size_t)d.cslabs * d.np * 4);
+  L.sA = take((size_t)d.mp * 4);
+  L.tB = take((size_t)d.np * 4);
+  L.counters = take(64);
+  L.listA = take((size_t)d.mp * 4);
+  L.listB = take((size_t)d.np * 4);
+  L.codesA = take((size_t)d.mp * d.kp);
+  L.codesB = take((size_t)d.np * d.kp);
+  L.planesA = take((size_t)c.P * d.mp * d.kp);
+  L.planesB = take((size_t)c.P * d.np * d.kp);
+  L.res = take((size_t)c.r * d.mp * d.np * 2);
+  L.total = o;
+  return L;
+}
+
+const unsigned kKnownFlags = OZ2_ACCUMULATE | OZ2_SCALE_FIXED | OZ2_QUANT_TZ | OZ2_NO_FALLBACK |
+                             OZ2_FORCE_FALLBACK;
+
+// gfx950 check, cached per device
+int device_ok() {
+  static std::mutex mu;
+  static int cache[64];
+  static bool init = false;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return OZ2_E_DEVICE;
+  std::lock_guard<std::mutex> g(mu);
+  if (!init) { for (int& x : cache) x = 0; init = true; }
+  if (dev < 0 || dev >= 64) return OZ2_E_DEVICE;
+  if (cache[dev] == 0) {
+    hipDeviceProp_t p;
+    if (hipGetDeviceProperties(&p, dev) != hipSuccess) return OZ2_E_DEVICE;
+    cache[dev] = (std::strncmp(p.gcnArchName, "gfx950", 6) == 0) ? 1 : 2;
+  }
+  return cache[dev] == 1 ? OZ2_OK : OZ2_E_UNSUPPORTED;
+}
+
+bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
+  uintptr_t a0 = (uintptr_t)a, a1 = a0 + abytes, b0 = (uintptr_t)b, b1 = b0 + bbytes;
+  return a0 < b1 && b0 < a1;
+}
+
+size_t span_bytes(int rows, int cols, int ld) {
+  if (rows <= 0 || cols <= 0) return 0;
+  return ((size_t)(cols - 1) * ld + rows) * sizeof(double);
+}
+
+int check_mats(int m, int n, int k, const double* A, int lda, const double* B, int ldb,
+               const double* C, int ldc) {
+  if (m < 0 || n < 0 || k < 0) return OZ2_E_INVALID;
+  if (lda < std::max(1, m) || ldb < std::max(1, k) || ldc < std::max(1, m)) return OZ2_E_INVALID;
+  if (m > 0 && n > 0) {
+    if (!C) return OZ2_E_INVALID;
+    if (k > 0 && (!A || !B)) return OZ2_E_INVALID;
+    size_t cb = span_bytes(m, n, ldc);
+    if (k > 0 && (overlaps(C, cb, A, span_bytes(m, k, lda)) ||
+                  overlaps(C, cb, B, span_bytes(k, n, ldb))))
+      return OZ2_E_INVALID;
+  }
+  return OZ2_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? OZ2_OK : OZ2_E_DEVICE; }
+
+}  // namespace
+
+// ------------------------------------------------------------------ plans
+struct ozaki2_plan_s {
+  Oz2Dims d;
+  Oz2Const c;
+  Oz2Layout L;
+  uint8_t* ws = nullptr;
+  const double* A = nullptr;
+  const double* B = nullptr;
+  int lda = 0, ldb = 0;
+  int stage = 0;      // 0 created, 1 deconstructed, 2 residues ready, 3 reconstructed
+};
+
+namespace {
+
+int run_deconstruct(ozaki2_plan_s& p, hipStream_t s) {
+  const Oz2Dims& d = p.d;
+  hipError_t e = oz2_launch_init(d, p.L, p.ws, s);
+  if (e == hipSuccess) e = oz2_launch_scan(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, s);
+  if (!(d.flags & OZ2_SCALE_FIXED)) {
+    if (e == hipSuccess) e = oz2_launch_codes(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, s);
+    if (e == hipSuccess) e = oz2_launch_codegemm(d, p.L, p.ws, s);
+  }
+  if (e == hipSuccess) e = oz2_launch_scales(d, p.L, p.c, p.ws, s);
+  if (e == hipSuccess) e = oz2_launch_split(d, p.L, p.c, p.ws, p.A, p.lda, p.B, p.ldb, s);
+  return hip_status(e);
+}
+
+int run_reconstruct(ozaki2_plan_s& p, double* C, int ldc, hipStream_t s) {
+  hipError_t e = oz2_launch_reconstruct(p.d, p.L, p.c, p.ws, C, ldc, s);
+  if (e == hipSuccess && !(p.d.flags & OZ2_NO_FALLBACK))
+    e = oz2_launch_fallback(p.d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, C, ldc, s);
+  return hip_status(e);
+}
+
+// internal grow-only workspace of ozaki2_dgemm, per device
+struct Pool {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+std::mutex g_pool_mu;
+Pool g_pool[64];
+
+int pool_get(size_t need, void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return OZ2_E_DEVICE;
+  std::lock_guard<std::mutex> g(g_pool_mu);
+  Pool& P = g_pool[dev];
+  if (P.bytes < need) {
+    if (P.ptr) {
+      if (hipDeviceSynchronize() != hipSuccess) return OZ2_E_DEVICE;
+      (void)hipFree(P.ptr);
+      P.ptr = nullptr;
+      P.bytes = 0;
+    }
+    size_t grow = std::max(need, (size_t)1 << 20);
+    if (hipMalloc(&P.ptr, grow) != hipSuccess) {
+      (void)hipGetLastError();
+      P.ptr = nullptr;
+      return OZ2_E_NOMEM;
+    }
+    P.bytes = grow;
+  }
+  *out = P.ptr;
+  return OZ2_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ozaki2_status_string(int status) {
+  switch (status) {
+    case OZ2_OK: return "ok";
+    case OZ2_E_INVALID: return "invalid argument";
+    case OZ2_E_NOMEM: return "out of device memory";
+    case OZ2_E_DEVICE: return "HIP runtime or launch error";
+    case OZ2_E_UNSUPPORTED: return "unsupported device (gfx950 required)";
+    case OZ2_E_WORKSPACE: return "workspace missing or too small";
+    default: return "unknown status";
+  }
+}
+
+int ozaki2_moduli(int num_moduli, int* host_out) {
+  Oz2Const c;
+  if (!host_out || !make_const(num_moduli, c)) return OZ2_E_INVALID;
+  for (int i = 0; i < num_moduli; ++i) host_out[i] = c.m[i];
+  return OZ2_OK;
+}
+
+size_t ozaki2_workspace_bytes(int m, int n, int k, int num_moduli, unsigned flags) {
+  Oz2Const c;
+  Oz2Dims d;
+  if ((flags & ~kKnownFlags) || !make_const(num_moduli, c) || !make_dims(m, n, k, flags, d))
+    return 0;
+  return make_layout(d, c).total;
+}
+
+int ozaki2_plan_create(ozaki2_plan_t* out, int m, int n, int k, int num_moduli, unsigned flags,
+                       void* workspace, size_t ws_bytes) {
+  if (!out) return OZ2_E_INVALID;
+  *out = nullptr;
+  if (flags & ~kKnownFlags) return OZ2_E_INVALID;
+  if (m <= 0 || n <= 0 || k <= 0) return OZ2_E_INVALID;
+  ozaki2_plan_s* p = new (std::nothrow) ozaki2_plan_s();
+  if (!p) return OZ2_E_NOMEM;
+  if (!make_const(num_moduli, p->c) || !make_dims(m, n, k, flags, p->d)) {
+    delete p;
+    return OZ2_E_INVALID;
+  }
+  p->L = make_layout(p->d, p->c);
+  if (!workspace || ws_bytes < p->L.total || ((uintptr_t)workspace & 255)) {
+    delete p;
+    return OZ2_E_WORKSPACE;
+  }
+  int st = device_ok();
+  if (st != OZ2_OK) {
+    delete p;
+    return st;
+  }
+  p->ws = (uint8_t*)workspace;
+  *out = p;
+  return OZ2_OK;
+}
+
+int ozaki2_plan_destroy(ozaki2_plan_t plan) {
+  delete plan;
+  return OZ2_OK;
+}
+
+int ozaki2_deconstruct(ozaki2_plan_t p, const double* A, int lda, const double* B, int ldb,
+                       void* stream) {
+  if (!p || !A || !B) return OZ2_E_INVALID;
+  if (lda < std::max(1, p->d.m) || ldb < std::max(1, p->d.k)) return OZ2_E_INVALID;
+  p->A = A;
+  p->B = B;
+  p->lda = lda;
+  p->ldb = ldb;
+  int st = run_deconstruct(*p, (hipStream_t)stream);
+  p->stage = st == OZ2_OK ? 1 : 0;
+  return st;
+}
+
+int ozaki2_residue_gemm(ozaki2_plan_t p, void* stream) {
+  if (!p || p->stage < 1) return OZ2_E_INVALID;
+  int st = hip_status(oz2_launch_resgemm(p->d, p->L, p->c, p->ws, (hipStream_t)stream));
+  if (st == OZ2_OK) p->stage = 2;
+  return st;
+}
+
+int ozaki2_reconstruct(ozaki2_plan_t p, double* C, int ldc, void* stream) {
+  if (!p || p->stage < 2 || !C || ldc < std::max(1, p->d.m)) return OZ2_E_INVALID;
+  int st = check_mats(p->d.m, p->d.n, p->d.k, p->A, p->lda, p->B, p->ldb, C, ldc);
+  if (st != OZ2_OK) return st;
+  st = run_reconstruct(*p, C, ldc, (hipStream_t)stream);
+  if (st == OZ2_OK) p->stage = 3;
+  return st;
+}
+
+int ozaki2_dgemm_ex(int m, int n, int k, const double* A, int lda, const double* B, int ldb,
+                    double* C, int ldc, int num_moduli, unsigned flags, void* workspace,
+                    size_t ws_bytes, void* stream) {
+  if (flags & ~kKnownFlags) return OZ2_E_INVALID;
+  if (num_moduli < 8 || num_moduli > OZ2_MAXR) return OZ2_E_INVALID;
+  int st = check_mats(m, n, k, A, lda, B, ldb, C, ldc);
+  if (st != OZ2_OK) return st;
+  if (m == 0 || n == 0) return OZ2_OK;
+  st = device_ok();
+  if (st != OZ2_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if (k == 0) {
+    if (flags & OZ2_ACCUMULATE) return OZ2_OK;
+    return hip_status(oz2_launch_fill(C, m, n, ldc, s));
+  }
+  ozaki2_plan_s p;
+  if (!make_const(num_moduli, p.c) || !make_dims(m, n, k, flags, p.d)) return OZ2_E_INVALID;
+  p.L = make_layout(p.d, p.c);
+  if (!workspace || ws_bytes < p.L.total || ((uintptr_t)workspace & 255)) return OZ2_E_WORKSPACE;
+  p.ws = (uint8_t*)workspace;
+  p.A = A;
+  p.B = B;
+  p.lda = lda;
+  p.ldb = ldb;
+  st = run_deconstruct(p, s);
+  if (st != OZ2_OK) return st;
+  st = hip_status(oz2_launch_resgemm(p.d, p.L, p.c, p.ws, s));
+  if (st != OZ2_OK) return st;
+  return run_reconstruct(p, C, ldc, s);
+}
+
+int ozaki2_dgemm(int m, int n, int k, const double* A, int lda, const double* B, int ldb,
+                 double* C, int ldc, int num_moduli, void* stream) {
+  if (num_moduli < 8 || num_moduli > OZ2_MAXR) return OZ2_E_INVALID;
+  int st = check_mats(m, n, k, A, lda, B, ldb, C, ldc);
+  if (st != OZ2_OK) return st;
+  if (m == 0 || n == 0) return OZ2_OK;
+  size_t need = ozaki2_workspace_bytes(m, n, k, num_moduli, 0);
+  if (need == 0) return OZ2_E_INVALID;
+  st = device_ok();
+  if (st != OZ2_OK) return st;
+  void* ws = nullptr;
+  st = pool_get(need, &ws);
+  if (st != OZ2_OK) return st;
+  return ozaki2_dgemm_ex(m, n, k, A, lda, B, ldb, C, ldc, num_moduli, 0, ws, need, stream);
+}
+
+int ozaki2_dgemm_strided_batched(int m, int n, int k, const double* A, int lda, long long strideA,
+                                 const double* B, int ldb, long long strideB, double* C, int ldc,
+                                 long long strideC, int batch, int num_moduli, void* stream) {
+  if (batch < 0 || num_moduli < 8 || num_moduli > OZ2_MAXR) return OZ2_E_INVALID;
+  if (strideA < 0 || strideB < 0 || strideC < 0) return OZ2_E_INVALID;
+  int st = check_mats(m, n, k, A, lda, B, ldb, C, ldc);
+  if (st != OZ2_OK) return st;
+  if (batch == 0 || m == 0 || n == 0) return OZ2_OK;
+  if (batch > 1 && (size_t)strideC * sizeof(double) < span_bytes(m, n, ldc)) return OZ2_E_INVALID;
+  size_t need = ozaki2_workspace_bytes(m, n, k, num_moduli, 0);
+  if (need == 0) return OZ2_E_INVALID;
+  st = device_ok();
+  if (st != OZ2_OK) return st;
+  void* ws = nullptr;
+  st = pool_get(need, &ws);
+  if (st != OZ2_OK) return st;
+  for (int b = 0; b < batch; ++b) {
+    st = ozaki2_dgemm_ex(m, n, k, A + (size_t)b * strideA, lda, B + (size_t)b * strideB, ldb,
+                         C + (size_t)b * strideC, ldc, num_moduli, 0, ws, need, stream);
+    if (st != OZ2_OK) return st;
+  }
+  return OZ2_OK;
+}
+
+void ozaki2_finalize(void) {
+  std::lock_guard<std::mutex> g(g_pool_mu);
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess) return;
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  for (int d = 0; d < ndev && d < 64; ++d) {
+    if (!g_pool[d].ptr) continue;
+    if (hipSetDevice(d) == hipSuccess) {
+      (void)hipDeviceSynchronize();
+      (void)hipFree(g_pool[d].ptr);
+    }
+    g_pool[d].ptr = nullptr;
+    g_pool[d].bytes = 0;
+  }
+  (void)hipSetDevice(cur);
+}
+
+size_t ozaki2_plan_query_bytes(ozaki2_plan_t p, int what) {
+  if (!p) return 0;
+  const size_t m = p->d.m, n = p->d.n, k = p->d.k;
+  switch (what) {
+    case OZ2_Q_EXPONENTS: return (m + n) * 4;
+    case OZ2_Q_MAXIMA: return (m + n) * 8;
+    case OZ2_Q_SCALES: return (m + n) * 4;
+    case OZ2_Q_FLAGS: return (m + n) * 4;
+    case OZ2_Q_CODES: return (m + n) * k;
+    case OZ2_Q_PLANES: return (size_t)p->c.P * (m + n) * k;
+    case OZ2_Q_RESIDUES: return (size_t)p->c.r * m * n * 2;
+    case OZ2_Q_INTEGERS: return m * n * OZ2_NLIMB * 4;
+    case OZ2_Q_FALLBACK_COUNT: return 8;
+    default: return 0;
+  }
+}
+
+int ozaki2_plan_query(ozaki2_plan_t p, int what, void* host_out, size_t bytes) {
+  if (!p || !host_out) return OZ2_E_INVALID;
+  const size_t need = ozaki2_plan_query_bytes(p, what);
+  if (need == 0 || bytes < need) return OZ2_E_INVALID;
+  const int needs_stage = (what == OZ2_Q_RESIDUES || what == OZ2_Q_INTEGERS) ? 2
+                          : (what == OZ2_Q_FALLBACK_COUNT)                    ? 3
+                                                                              : 1;
+  if (p->stage < needs_stage) return OZ2_E_INVALID;
+  if (hipDeviceSynchronize() != hipSuccess) return OZ2_E_DEVICE;
+  const Oz2Dims& d = p->d;
+  const Oz2Layout& L = p->L;
+  uint8_t* ws = p->ws;
+  uint8_t* out = (uint8_t*)host_out;
+  auto cp = [](void* dst, const void* src, size_t b) {
+    return hipMemcpy(dst, src, b, hipMemcpyDeviceToHost) == hipSuccess;
+  };
+  switch (what) {
+    case OZ2_Q_EXPONENTS: {
+      std::vector<uint64_t> rb(d.m), cb(d.n);
+      if (!cp(rb.data(), ws + L.rowbits, d.m * 8) || !cp(cb.data(), ws + L.colbits, d.n * 8))
+        return OZ2_E_DEVICE;
+      int32_t* o = (int32_t*)out;
+      auto ex = [](uint64_t b) -> int32_t {
+        if (b == 0 || b >= 0x7FF0000000000000ull) return 0;
+        double x;
+        std::memcpy(&x, &b, 8);
+        int e;
+        std::frexp(x, &e);
+        return e;
+      };
+      for (int i = 0; i < d.m; ++i) o[i] = ex(rb[i]);
+      for (int j = 0; j < d.n; ++j) o[d.m + j] = ex(cb[j]);
+      return OZ2_OK;
+    }
+    case OZ2_Q_MAXIMA: {
+      std::vector<uint32_t> R((size_t)d.cslabs * d.mp), K((size_t)d.cslabs * d.np);
+      if (!cp(R.data(), ws + L.Rmax, R.size() * 4) || !cp(K.data(), ws + L.Kmax, K.size() * 4))
+        return OZ2_E_DEVICE;
+      uint64_t* o = (uint64_t*)out;
+      for (int i = 0; i < d.m; ++i) {
+        uint64_t s = 0;
+        for (int sl = 0; sl < d.cslabs; ++sl) s += R[(size_t)sl * d.mp + i];
+        o[i] = s;
+      }
+      for (int j = 0; j < d.n; ++j) {
+        uint64_t s = 0;
+        for (int sl = 0; sl < d.cslabs; ++sl) s += K[(size_t)sl * d.np + j];
+        o[d.m + j] = s;
+      }
+      return OZ2_OK;
+    }
+    case OZ2_Q_SCALES:
+      if (!cp(out, ws + L.sA, (size_t)d.m * 4) || !cp(out + (size_t)d.m * 4, ws + L.tB, (size_t)d.n * 4))
+        return OZ2_E_DEVICE;
+      return OZ2_OK;
+    case OZ2_Q_FLAGS:
+      if (!cp(out, ws + L.flagsA, (size_t)d.m * 4) ||
+          !cp(out + (size_t)d.m * 4, ws + L.flagsB, (size_t)d.n * 4))
+        return OZ2_E_DEVICE;
+      return OZ2_OK;
+    case OZ2_Q_CODES:
+    case OZ2_Q_PLANES: {
+      const bool codes = what == OZ2_Q_CODES;
+      const int P = codes ? 1 : p->c.P;
+      size_t o = 0;
+      for (int side = 0; side < 2; ++side) {
+        const int rows = side ? d.n : d.m, rp = side ? d.np : d.mp;
+        const size_t base = codes ? (side ? L.codesB : L.codesA) : (side ? L.planesB : L.planesA);
+        for (int pl = 0; pl < P; ++pl) {
+          if (hipMemcpy2D(out + o, d.k, ws + base + (size_t)pl * rp * d.kp, d.kp, d.k, rows,
+                          hipMemcpyDeviceToHost) != hipSuccess)
+            return OZ2_E_DEVICE;
+          o += (size_t)rows * d.k;
+        }
+      }
+      return OZ2_OK;
+    }
+    case OZ2_Q_RESIDUES: {
+      const size_t plane = (size_t)d.mp * d.np;
+      std::vector<int16_t> raw((size_t)p->c.r * plane);
+      if (!cp(raw.data(), ws + L.res, raw.size() * 2)) return OZ2_E_DEVICE;
+      int16_t* o = (int16_t*)out;
+      const int ntm = d.mp / OZ2_TILE;
+      for (int i = 0; i < p->c.r; ++i)
+        for (size_t gid = 0; gid < plane / 4; ++gid) {
+          const size_t tile = gid >> 14;
+          const int q = (int)(gid & 16383), lane = q & 63, blk = q >> 6;
+          const int y = blk & 7, x = (blk >> 3) & 7, w = blk >> 6;
+          const int tm = (int)(tile % ntm), tn = (int)(tile / ntm);
+          const int row = tm * OZ2_TILE + (w >> 1) * 128 + x * 16 + 4 * (lane >> 4);
+          const int col = tn * OZ2_TILE + (w & 1) * 128 + y * 16 + (lane & 15);
+          if (col >= d.n) continue;
+          for (int j = 0; j < 4; ++j)
+            if (row + j < d.m)
+              o[((size_t)i * d.n + col) * d.m + row + j] =
+                  raw[(size_t)i * plane + tile * (OZ2_TILE * OZ2_TILE) + (size_t)q * 4 + j];
+        }
+      return OZ2_OK;
+    }
+    case OZ2_Q_INTEGERS: {
+      uint32_t* dev = nullptr;
+      if (hipMalloc(&dev, need) != hipSuccess) return OZ2_E_NOMEM;
+      hipError_t e = oz2_launch_integers(d, L, p->c, ws, dev, nullptr);
+      if (e == hipSuccess) e = hipDeviceSynchronize();
+      if (e == hipSuccess) e = hipMemcpy(out, dev, need, hipMemcpyDeviceToHost);
+      (void)hipFree(dev);
+      return hip_status(e);
+    }
+    case OZ2_Q_FALLBACK_COUNT:
+      return cp(out, ws + L.counters, 8) ? OZ2_OK : OZ2_E_DEVICE;
+    default:
+      return OZ2_E_INVALID;
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,106 @@
+// Internal definitions shared by the host orchestration and the gfx950
+// kernels of the Ozaki-II FP8 emulated DGEMM.  Not part of the public ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define OZ2_MAXR 16
+#define OZ2_NLIMB 5          // 36-bit limbs of the CRT sum: 180 bits >= log2(16 * 545 * M_max)
+#define OZ2_TILE 256         // output tile of the FP8 GEMMs (rows and columns)
+#define OZ2_KSTEP 128        // K per LDS stage = K of one v_mfma_f32_16x16x128_f8f6f4
+#define OZ2_KSLAB 32768      // residue GEMM: k per exact FP32 slab, Eq. (accum-exact)
+#define OZ2_CSLAB 65536      // code GEMM: codes <= 16, products <= 256: 65536*256 = 2^24
+
+// Flags per row of A / column of B.
+#define OZ2_T1 1u            // a NaN or +-Inf entry
+#define OZ2_T2 2u            // a nonzero entry that quantises to zero
+
+// Per-plan constants, passed to every kernel by value (kernarg segment).
+struct Oz2Const {
+  int r;
+  int P;                      // p_store: planes per scalar
+  int m[OZ2_MAXR];            // moduli, ascending
+  int sq[OZ2_MAXR];           // s if m = s^2, else 0
+  int pbase[OZ2_MAXR];        // first plane of modulus i
+  int c32[OZ2_MAXR];          // 2^32 mod m
+  int rho0[OZ2_MAXR];         // chain transition multipliers (mod m, in [0, m))
+  int rho1[OZ2_MAXR];
+  int fin[OZ2_MAXR];          // final epilogue coefficient (1 square, 16 nonsquare)
+  float finv[OZ2_MAXR];       // RN(1/m) in fp32
+  float finv_s[OZ2_MAXR];     // RN(1/s) in fp32 (square moduli)
+  double dinv[OZ2_MAXR];      // RN(1/m) in fp64
+  // direct CRT sum: X = sum_i x_i W_i - q M, W_i = (M/m_i) * ((M/m_i)^-1 mod m_i)
+  double W[OZ2_MAXR][OZ2_NLIMB];  // 36-bit limbs of W_i (exact integers)
+  double wfrac[OZ2_MAXR];         // W_i / M rounded to fp64
+  double Ml[OZ2_NLIMB];           // 36-bit limbs of M
+  double Mhalf[OZ2_NLIMB];        // 36-bit limbs of floor(M/2)
+  int cA, cB;                     // width budgets of the scaling rule
+};
+
+struct Oz2Dims {
+  int m, n, k;
+  int mp, np, kp;             // padded: mp, np multiples of OZ2_TILE; kp of OZ2_KSTEP
+  int cslabs;                 // number of code-GEMM slabs
+  unsigned flags;
+};
+
+// Workspace carve-up (byte offsets from the workspace base).
+struct Oz2Layout {
+  size_t rowbits, colbits;    // uint64 [mp] / [np]: max |x| bit patterns
+  size_t flagsA, flagsB;      // uint32 [mp] / [np]
+  size_t Rmax, Kmax;          // uint32 [cslabs][mp] / [cslabs][np]
+  size_t sA, tB;              // int32 [mp] / [np]
+  size_t codesA, codesB;      // uint8 [mp][kp] / [np][kp]
+  size_t planesA, planesB;    // uint8 [P][mp][kp] / [P][np][kp]
+  size_t res;                 // int16 [r][mp*np] (MFMA-native tile order)
+  size_t counters;            // int32 [4]: fallback row / column counts
+  size_t listA, listB;        // int32 [mp] / [np]: flagged row / column indices
+  size_t total;
+};
+
+// ---------------------------------------------------------------- launchers
+// Each returns hipGetLastError() of its launches.
+hipError_t oz2_launch_init(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, hipStream_t s);
+hipError_t oz2_launch_scan(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
+                           const double* A, int lda, const double* B, int ldb, hipStream_t s);
+hipError_t oz2_launch_codes(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
+                            const double* A, int lda, const double* B, int ldb, hipStream_t s);
+hipError_t oz2_launch_codegemm(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, hipStream_t s);
+hipError_t oz2_launch_scales(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
+                             uint8_t* ws, hipStream_t s);
+hipError_t oz2_launch_split(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
+                            const double* A, int lda, const double* B, int ldb, hipStream_t s);
+hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
+                              uint8_t* ws, hipStream_t s);
+hipError_t oz2_launch_reconstruct(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
+                                  uint8_t* ws, double* C, int ldc, hipStream_t s);
+hipError_t oz2_launch_fallback(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
+                               const double* A, int lda, const double* B, int ldb,
+                               double* C, int ldc, hipStream_t s);
+hipError_t oz2_launch_integers(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
+                               uint8_t* ws, uint32_t* out, hipStream_t s);
+hipError_t oz2_launch_fill(double* C, int m, int n, int ldc, hipStream_t s);
+
+// ---------------------------------------------------------------- device helpers
+#ifdef __HIPCC__
+// x mod m in [0, m) for |x| < 2^25 (float reciprocal estimate, one correction
+// each way: the estimate of x/m is within 0.02 of the true quotient).
+__device__ __forceinline__ int oz2_mod(int x, int m, float inv) {
+  int q = (int)floorf((float)x * inv);
+  int r = x - q * m;
+  r += (r < 0) ? m : 0;
+  r -= (r >= m) ? m : 0;
+  return r;
+}
+// x - m * rint(x/m): a representative of x mod m with |result| <= m/2 + 2,
+// for |x| < 2^25.
+__device__ __forceinline__ int oz2_red(int x, int m, float inv) {
+  int q = (int)rintf((float)x * inv);
+  return x - q * m;
+}
+// exact centred residue in [-floor(m/2), ceil(m/2) - 1] for |x| < 2^25
+__device__ __forceinline__ int oz2_centre(int x, int m, float inv) {
+  int r = oz2_mod(x, m, inv);
+  return (r >= ((m + 1) >> 1)) ? r - m : r;
+}
+#endif

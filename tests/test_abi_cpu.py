@@ -1,0 +1,95 @@
+"""The C-ABI library: it loads without a GPU, exports every entry point
+include/ozaki2.h declares, and rejects invalid arguments before touching the
+device (no compute calls here)."""
+import os
+import re
+
+import pytest
+
+import paper_2606_06510_amd as oz
+from paper_2606_06510_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "ozaki2.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ozaki2_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = oz.load()
+    names = _declared()
+    assert len(names) == 14
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(_lib.EXPORTS) == names
+
+
+def test_status_strings():
+    assert oz.ozaki2_status_string(0) == "ok"
+    assert "workspace" in oz.ozaki2_status_string(-5)
+
+
+def test_moduli_table():
+    assert oz.ozaki2_moduli(12) == [487, 491, 499, 503, 509, 511, 529, 625, 841, 961, 1024, 1089]
+    assert oz.ozaki2_moduli(16)[:4] == [463, 467, 479, 481]
+    with pytest.raises(oz.Ozaki2Error):
+        oz.ozaki2_moduli(7)
+    with pytest.raises(oz.Ozaki2Error):
+        oz.ozaki2_moduli(17)
+
+
+def test_workspace_bytes():
+    # planes 30 B per padded element of A and B, residues 24 B per padded output
+    b = oz.ozaki2_workspace_bytes(4096, 4096, 4096, 12)
+    assert b >= 30 * 2 * 4096 * 4096 + 24 * 4096 * 4096
+    assert b < 1.05 * (31 * 2 * 4096 * 4096 + 24 * 4096 * 4096) + (1 << 20)
+    assert oz.ozaki2_workspace_bytes(10, 10, 10, 7) == 0
+    assert oz.ozaki2_workspace_bytes(10, 10, 10, 12, 1 << 10) == 0
+    assert oz.ozaki2_workspace_bytes(-1, 10, 10, 12) == 0
+
+
+FAKE = 1 << 40      # never dereferenced: validation rejects before any launch
+
+
+@pytest.mark.parametrize("args", [
+    dict(m=-1), dict(n=-1), dict(k=-1), dict(lda=3), dict(ldb=4), dict(ldc=3), dict(r=7),
+    dict(r=17), dict(A=0), dict(B=0), dict(C=0), dict(flags=1 << 8),
+])
+def test_invalid_arguments_rejected(args):
+    p = dict(m=4, n=5, k=6, A=FAKE, lda=4, B=FAKE + (1 << 20), ldb=6, C=FAKE + (2 << 20), ldc=4,
+             r=12, flags=0)
+    p.update(args)
+    L = oz.load()
+    st = L.ozaki2_dgemm_ex(p["m"], p["n"], p["k"], p["A"] or None, p["lda"], p["B"] or None,
+                           p["ldb"], p["C"] or None, p["ldc"], p["r"], p["flags"], FAKE + (3 << 20),
+                           1 << 30, None)
+    assert st == _lib.OZ2_E_INVALID
+
+
+def test_overlapping_output_rejected():
+    L = oz.load()
+    st = L.ozaki2_dgemm_ex(4, 5, 6, FAKE, 4, FAKE + (1 << 20), 6, FAKE + 8, 4, 12, 0,
+                           FAKE + (3 << 20), 1 << 30, None)
+    assert st == _lib.OZ2_E_INVALID
+
+
+def test_zero_sized_output_is_a_noop():
+    L = oz.load()
+    assert L.ozaki2_dgemm_ex(0, 5, 6, None, 1, None, 6, None, 1, 12, 0, None, 0, None) == 0
+    assert L.ozaki2_dgemm(4, 0, 6, None, 4, None, 6, None, 4, 12, None) == 0
+
+
+def test_plan_create_validation():
+    L = oz.load()
+    import ctypes
+    h = ctypes.c_void_p()
+    need = oz.ozaki2_workspace_bytes(8, 8, 8, 12)
+    assert L.ozaki2_plan_create(ctypes.byref(h), 8, 8, 8, 12, 0, None, need) == _lib.OZ2_E_WORKSPACE
+    assert L.ozaki2_plan_create(ctypes.byref(h), 8, 8, 8, 12, 0, FAKE, need - 1) == _lib.OZ2_E_WORKSPACE
+    assert L.ozaki2_plan_create(ctypes.byref(h), 8, 8, 8, 12, 0, FAKE + 8, need) == _lib.OZ2_E_WORKSPACE
+    assert L.ozaki2_plan_create(ctypes.byref(h), 8, 8, 8, 5, 0, FAKE, need) == _lib.OZ2_E_INVALID
+    assert L.ozaki2_residue_gemm(None, None) == _lib.OZ2_E_INVALID
+    assert L.ozaki2_reconstruct(None, FAKE, 8, None) == _lib.OZ2_E_INVALID

@@ -1,0 +1,144 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, element
+by element on seeded inputs.  Integer stages (exponents, code-product maxima,
+scales, flags, code and plane bytes, residues, reconstructed integers) must be
+bit-exact; emulated C entries are bit-exact too (both sides round the same
+exact rational once); native-FP64 fallback entries are within the FP64
+dot-product error bound (their summation order is the hardware's)."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_util import compare_all, compare_C, run_staged, bits, device
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 1), (17, 33, 129), (256, 256, 256), (300, 520, 700),
+                                   (513, 129, 257), (64, 700, 5)])
+def test_stage_parity_shapes(shape):
+    m, n, k = shape
+    A, B = synth.lognormal(m, n, k, seed=m + n + k)
+    res = oracle.dgemm(A, B, 12)
+    plan, C = run_staged(A, B, 12)
+    compare_all(plan, C, A, B, 12, res, check_integers=m * n <= 70000)
+
+
+@pytest.mark.parametrize("r", range(8, 17))
+def test_moduli_sweep(r):
+    A, B = synth.lognormal(160, 200, 300, seed=100 + r)
+    res = oracle.dgemm(A, B, r)
+    plan, C = run_staged(A, B, r)
+    compare_all(plan, C, A, B, r, res, check_integers=(r in (8, 12, 16)))
+
+
+def test_gemm256_uniform_full():
+    A, B = synth.make("gemm256_uniform")
+    res = oracle.dgemm(A, B, 12)
+    plan, C = run_staged(A, B, 12)
+    compare_all(plan, C, A, B, 12, res)
+
+
+@pytest.mark.parametrize("flags,mode,quant", [(2, "fixed", "rn"), (4, "bound", "tz"),
+                                              (6, "fixed", "tz")])
+def test_modes(flags, mode, quant):
+    A, B = synth.wide(200, 150, 333, seed=7, spread=1.0, frac=0.0)[:2]
+    res = oracle.dgemm(A, B, 12, mode=mode, quant=quant)
+    plan, C = run_staged(A, B, 12, flags=flags)
+    compare_all(plan, C, A, B, 12, res, check_integers=False)
+
+
+def test_accumulate():
+    A, B, Cin = synth.rankk(300, 260, 256, seed=4)
+    res = oracle.dgemm(A, B, 12, C_in=Cin)
+    plan, C = run_staged(A, B, 12, flags=1, C_in=Cin)
+    compare_C(C, A, B, res)
+
+
+def test_fallback_rows_and_columns():
+    rng = np.random.default_rng(9)
+    A, B = synth.uniform(260, 270, 300, seed=9)
+    A[3, 7] = np.nan
+    A[100, 5] = np.inf
+    B[11, 200] = -np.inf
+    A[50, ::2] *= 1e200                       # T2: intra-row span ~2^664
+    B[::3, 20] *= 1e-250                      # T2 on a column of B
+    res = oracle.dgemm(A, B, 12)
+    assert set(res.fallback_rows) == {3, 50, 100} and set(res.fallback_cols) == {20, 200}
+    plan, C = run_staged(A, B, 12)
+    compare_all(plan, C, A, B, 12, res, check_integers=False)
+    import paper_2606_06510_amd as oz
+    assert plan.query(oz.OZ2_Q_FALLBACK_COUNT) == (3, 2)
+
+
+def test_whole_rows_1e200_absorbed():
+    A, B, rows = synth.wide(300, 200, 256, seed=3)
+    assert len(rows) > 0
+    res = oracle.dgemm(A, B, 15)
+    assert len(res.fallback_rows) == 0
+    plan, C = run_staged(A, B, 15)
+    compare_all(plan, C, A, B, 15, res, check_integers=False)
+
+
+def test_no_fallback_and_force_fallback():
+    A, B = synth.uniform(100, 90, 80, seed=5)
+    A[2, ::2] *= 1e200
+    res = oracle.dgemm(A, B, 12, fallback=False)
+    plan, C = run_staged(A, B, 12, flags=8)
+    assert np.array_equal(bits(C), bits(res.C))
+    res2 = oracle.dgemm(A, B, 12, force_fallback=True)
+    plan2, C2 = run_staged(A, B, 12, flags=16)
+    compare_C(C2, A, B, res2)
+
+
+def test_multi_slab_k():
+    """k above the 32768 residue slab and the 65536 code slab."""
+    A, B = synth.uniform(40, 48, 70000, seed=12)
+    res = oracle.dgemm(A, B, 12)
+    plan, C = run_staged(A, B, 12)
+    compare_all(plan, C, A, B, 12, res, check_integers=True)
+
+
+def test_zero_rows_columns_and_k0():
+    import paper_2606_06510_amd as oz
+    import torch
+    A, B = synth.uniform(70, 60, 50, seed=1)
+    A[5] = 0.0
+    B[:, 9] = 0.0
+    res = oracle.dgemm(A, B, 12)
+    plan, C = run_staged(A, B, 12)
+    compare_all(plan, C, A, B, 12, res)
+    assert not np.any(np.signbit(C[5])) and np.all(C[5] == 0)
+    # k = 0: C = 0; with ACCUMULATE, C unchanged
+    dev = device()
+    Ad = oz.colmajor_empty(4, 0, device=dev)
+    Bd = oz.colmajor_empty(0, 3, device=dev)
+    Cd = oz.to_device_colmajor(np.full((4, 3), 7.0), dev)
+    oz.ozaki2_dgemm(4, 3, 0, Ad, 4, Bd, 1, Cd, 4, 12)
+    torch.cuda.synchronize()
+    assert np.all(oz.from_device_colmajor(Cd) == 0.0)
+
+
+def test_plain_entry_point_and_batched():
+    import paper_2606_06510_amd as oz
+    import torch
+    dev = device()
+    A, B = synth.lognormal(200, 100, 150, seed=21)
+    Ad, Bd = oz.to_device_colmajor(A, dev), oz.to_device_colmajor(B, dev)
+    Cd = oz.colmajor_empty(200, 100, device=dev)
+    oz.ozaki2_dgemm(200, 100, 150, Ad, 200, Bd, 150, Cd, 200, 12)
+    torch.cuda.synchronize()
+    res = oracle.dgemm(A, B, 12)
+    assert np.array_equal(bits(oz.from_device_colmajor(Cd)), bits(res.C))
+    # strided batched: 5 problems of 64^3 with per-matrix scales
+    Ab, Bb = synth.batched(5, 64, 64, 64, seed=5)
+    Ad = torch.from_numpy(np.ascontiguousarray(Ab.transpose(0, 2, 1))).to(dev)
+    Bd = torch.from_numpy(np.ascontiguousarray(Bb.transpose(0, 2, 1))).to(dev)
+    Cd = torch.empty((5, 64, 64), dtype=torch.float64, device=dev)
+    oz.ozaki2_dgemm_strided_batched(64, 64, 64, Ad, 64, 64 * 64, Bd, 64, 64 * 64, Cd, 64, 64 * 64,
+                                    5, 12)
+    torch.cuda.synchronize()
+    Cb = Cd.cpu().numpy().transpose(0, 2, 1)
+    for b in range(5):
+        rb = oracle.dgemm(Ab[b], Bb[b], 12)
+        assert np.array_equal(bits(Cb[b]), bits(rb.C))
