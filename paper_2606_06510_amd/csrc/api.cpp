@@ -137,7 +137,7 @@ bool make_dims(int m, int n, int k, unsigned flags, Oz2Dims& d) {
   d.k = k;
   d.mp = round_up(std::max(m, 1), OZ2_TILE);
   d.np = round_up(std::max(n, 1), OZ2_TILE);
-  d.kp = round_up(std::max(k, 1), OZ2_KSTEP);
+  d.kp = round_up(std::max(k, 1), OZ2_KPAD);
   d.cslabs = (d.kp + OZ2_CSLAB - 1) / OZ2_CSLAB;
   d.flags = flags;
   const double lim = 1099511627776.0;      // 2^40
@@ -546,40 +546,47 @@ int ozaki2_plan_query(ozaki2_plan_t p, int what, void* host_out, size_t bytes) {
       return OZ2_OK;
     case OZ2_Q_CODES:
     case OZ2_Q_PLANES: {
+      // K-blocked [kp/64][rows_pad][64] per plane -> [rows][k]
       const bool codes = what == OZ2_Q_CODES;
       const int P = codes ? 1 : p->c.P;
       size_t o = 0;
       for (int side = 0; side < 2; ++side) {
         const int rows = side ? d.n : d.m, rp = side ? d.np : d.mp;
         const size_t base = codes ? (side ? L.codesB : L.codesA) : (side ? L.planesB : L.planesA);
+        std::vector<uint8_t> raw((size_t)rp * d.kp);
         for (int pl = 0; pl < P; ++pl) {
-          if (hipMemcpy2D(out + o, d.k, ws + base + (size_t)pl * rp * d.kp, d.kp, d.k, rows,
-                          hipMemcpyDeviceToHost) != hipSuccess)
-            return OZ2_E_DEVICE;
+          if (!cp(raw.data(), ws + base + (size_t)pl * rp * d.kp, raw.size())) return OZ2_E_DEVICE;
+          for (int rr = 0; rr < rows; ++rr)
+            for (int l = 0; l < d.k; ++l)
+              out[o + (size_t)rr * d.k + l] =
+                  raw[((size_t)(l / OZ2_KBLK) * rp + rr) * OZ2_KBLK + (l % OZ2_KBLK)];
           o += (size_t)rows * d.k;
         }
       }
       return OZ2_OK;
     }
     case OZ2_Q_RESIDUES: {
+      // [tile][wave 8][x 4][y 2][lane 64][16] per modulus -> [r][n][m]
       const size_t plane = (size_t)d.mp * d.np;
       std::vector<int16_t> raw((size_t)p->c.r * plane);
       if (!cp(raw.data(), ws + L.res, raw.size() * 2)) return OZ2_E_DEVICE;
       int16_t* o = (int16_t*)out;
       const int ntm = d.mp / OZ2_TILE;
       for (int i = 0; i < p->c.r; ++i)
-        for (size_t gid = 0; gid < plane / 4; ++gid) {
-          const size_t tile = gid >> 14;
-          const int q = (int)(gid & 16383), lane = q & 63, blk = q >> 6;
-          const int y = blk & 7, x = (blk >> 3) & 7, w = blk >> 6;
+        for (size_t t = 0; t < plane / 16; ++t) {
+          const size_t tile = t >> 12;
+          const int q = (int)(t & 4095), lane = q & 63, blk = q >> 6;
+          const int y = blk & 1, x = (blk >> 1) & 3, w = blk >> 3;
           const int tm = (int)(tile % ntm), tn = (int)(tile / ntm);
-          const int row = tm * OZ2_TILE + (w >> 1) * 128 + x * 16 + 4 * (lane >> 4);
-          const int col = tn * OZ2_TILE + (w & 1) * 128 + y * 16 + (lane & 15);
+          const int row = tm * OZ2_TILE + (w >> 2) * 128 + 32 * x + 4 * (lane >> 5);
+          const int col = tn * OZ2_TILE + (w & 3) * 64 + 32 * y + (lane & 31);
           if (col >= d.n) continue;
-          for (int j = 0; j < 4; ++j)
-            if (row + j < d.m)
-              o[((size_t)i * d.n + col) * d.m + row + j] =
-                  raw[(size_t)i * plane + tile * (OZ2_TILE * OZ2_TILE) + (size_t)q * 4 + j];
+          for (int e = 0; e < 16; ++e) {
+            const int rr = row + 8 * (e >> 2) + (e & 3);
+            if (rr < d.m)
+              o[((size_t)i * d.n + col) * d.m + rr] =
+                  raw[(size_t)i * plane + tile * (OZ2_TILE * OZ2_TILE) + (size_t)q * 16 + e];
+          }
         }
       return OZ2_OK;
     }

@@ -7,8 +7,8 @@
 //
 // All of it is HBM-bound streaming: A (column-major, rows strided) is read
 // with lanes along the rows so every load instruction is a contiguous 512 B;
-// B's columns are contiguous along k.  Outputs (codes, planes) are K-major
-// byte rows, written 16 bytes per lane.
+// B's columns are contiguous along k.  Outputs (codes, planes) are K-blocked
+// byte planes [k/64][rows][64] (the GEMM's stage order), 16 bytes per lane.
 #include "oz2_internal.h"
 
 namespace {
@@ -84,10 +84,12 @@ __device__ __forceinline__ uint32_t pack4_fp8(float a, float b, float c, float d
   return (uint32_t)w;
 }
 
-// Row segment of 16 consecutive k for one row of A (TRANS) or column of B.
-// A-side: tile 64 rows x 64 k per 256 threads; B-side: 32 columns x 128 k.
-// The grid is one-dimensional: block b covers row block b % nrb and k block
-// b / nrb (nrb = padded rows / rows per block).
+// Row segment of 16 consecutive k for one row of A (TRANS) or column of B;
+// a block of 256 threads covers 64 rows x 64 k.  A-side lanes run along the
+// rows (each load instruction reads 512 contiguous bytes of a column of A);
+// B-side lanes run along k (4 lanes read 512 contiguous bytes of a column
+// of B).  The grid is one-dimensional: block b covers row block b % nrb and
+// k block b / nrb (nrb = padded rows / 64).
 template <bool TRANS>
 __device__ __forceinline__ void seg_coords(int nrb, int& row, int& l0) {
   const int t = threadIdx.x;
@@ -96,9 +98,14 @@ __device__ __forceinline__ void seg_coords(int nrb, int& row, int& l0) {
     row = bx * 64 + (t & 63);
     l0 = by * 64 + (t >> 6) * 16;
   } else {
-    row = bx * 32 + (t >> 3);
-    l0 = by * 128 + (t & 7) * 16;
+    row = bx * 64 + (t >> 2);
+    l0 = by * 64 + (t & 3) * 16;
   }
+}
+
+// byte offset of (row, k) in a K-blocked plane [kp/64][rows_pad][64]
+__device__ __forceinline__ size_t kblocked(int row, int l, int rows_pad) {
+  return ((size_t)(l >> 6) * rows_pad + row) * OZ2_KBLK + (l & 63);
 }
 
 template <bool TRANS>
@@ -116,6 +123,7 @@ __device__ __forceinline__ void load_seg(const double* __restrict__ X, int ld, i
 template <bool TRANS>
 __global__ void k_codes(const double* __restrict__ X, int ld, int rows, int nrb, int k, int kp,
                         const unsigned long long* __restrict__ bits, uint8_t* __restrict__ codes) {
+  const int rows_pad = nrb * 64;
   int row, l0;
   seg_coords<TRANS>(nrb, row, l0);
   unsigned long long b = row < rows ? bits[row] : 0ull;
@@ -129,7 +137,7 @@ __global__ void k_codes(const double* __restrict__ X, int ld, int rows, int nrb,
     w[q] = pack4_fp8(code_of(x[4 * q], E), code_of(x[4 * q + 1], E), code_of(x[4 * q + 2], E),
                      code_of(x[4 * q + 3], E));
   uint4 v = make_uint4(w[0], w[1], w[2], w[3]);
-  *reinterpret_cast<uint4*>(codes + (size_t)row * kp + l0) = v;
+  *reinterpret_cast<uint4*>(codes + kblocked(row, l0, rows_pad)) = v;
 }
 
 // widths sigma = min(62, c - ceil(ell(R)/2)), ell(x) = ceil(log2 x) (0 for x <= 1)
@@ -259,7 +267,7 @@ __global__ void __launch_bounds__(256) k_split(Oz2Const c, const double* __restr
   }
   if (t2) atomicOr(flags + row, OZ2_T2);
   const size_t pstride = (size_t)rows_pad * kp;
-  uint8_t* base = planes + (size_t)row * kp + l0;
+  uint8_t* base = planes + kblocked(row, l0, rows_pad);
   for (int i = 0; i < c.r; ++i) {
     const int m = c.m[i], c32 = c.c32[i], s_ = c.sq[i];
     const double dinv = c.dinv[i];
@@ -329,8 +337,8 @@ hipError_t oz2_launch_codes(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, c
   dim3 ga((d.mp / 64) * (d.kp / 64));
   hipLaunchKernelGGL(k_codes<true>, ga, dim3(256), 0, s, A, lda, d.m, d.mp / 64, d.k, d.kp,
                      (const unsigned long long*)(ws + L.rowbits), ws + L.codesA);
-  dim3 gb((d.np / 32) * (d.kp / 128));
-  hipLaunchKernelGGL(k_codes<false>, gb, dim3(256), 0, s, B, ldb, d.n, d.np / 32, d.k, d.kp,
+  dim3 gb((d.np / 64) * (d.kp / 64));
+  hipLaunchKernelGGL(k_codes<false>, gb, dim3(256), 0, s, B, ldb, d.n, d.np / 64, d.k, d.kp,
                      (const unsigned long long*)(ws + L.colbits), ws + L.codesB);
   return hipGetLastError();
 }
@@ -354,8 +362,8 @@ hipError_t oz2_launch_split(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const
   hipLaunchKernelGGL(k_split<true>, ga, dim3(256), 0, s, c, A, lda, d.m, d.mp, d.mp / 64, d.k,
                      d.kp, (const int32_t*)(ws + L.sA), (uint32_t*)(ws + L.flagsA),
                      ws + L.planesA, tz);
-  dim3 gb((d.np / 32) * (d.kp / 128));
-  hipLaunchKernelGGL(k_split<false>, gb, dim3(256), 0, s, c, B, ldb, d.n, d.np, d.np / 32, d.k,
+  dim3 gb((d.np / 64) * (d.kp / 64));
+  hipLaunchKernelGGL(k_split<false>, gb, dim3(256), 0, s, c, B, ldb, d.n, d.np, d.np / 64, d.k,
                      d.kp, (const int32_t*)(ws + L.tB), (uint32_t*)(ws + L.flagsB),
                      ws + L.planesB, tz);
   return hipGetLastError();

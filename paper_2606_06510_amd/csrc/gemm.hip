@@ -1,4 +1,4 @@
-// FP8 MFMA GEMMs of Alg. 1 on gfx950 (v_mfma_f32_16x16x128_f8f6f4, E4M3 x E4M3,
+// FP8 MFMA GEMMs of Alg. 1 on gfx950 (v_mfma_f32_32x32x64_f8f6f4, E4M3 x E4M3,
 // FP32 accumulation):
 //
 //  * the max-magnitude pass ("+1" of alpha = 3r+1): G' = codesA * codesB^T,
@@ -10,281 +10,311 @@
 //    (Eq. (accum-exact): every partial sum is an integer of magnitude
 //    <= 2^24 for k <= 32768), then reduced to the centred residue.
 //
-// Design: one workgroup of 256 threads (4 waves) owns a 256x256 output tile;
-// each wave owns 128x128 = 8x8 MFMA tiles (256 FP32 accumulators per lane).
-// Operand tiles (256 rows x 128 k bytes per operand) are double buffered in
-// LDS, filled by asynchronous global_load_lds (no staging registers) with an
-// XOR swizzle of the 16-byte chunks so that fragment reads are bank-conflict
-// free.  Per K-step: read this stage's fragments, issue the copy of the next
-// stage into the other buffer, run the 64 MFMAs while it lands, then wait and
-// barrier.  The three products of a modulus are run as three
-// (square: two) sequential "chains" over K on ONE accumulator set: at the end
-// of a chain the exact integer accumulator is reduced mod m and re-seeded as
-// acc * (c_this / c_next) mod m, so the next chain continues the same
-// residue.  This trades a short VALU epilogue per chain for a 256x256 tile
-// (half the operand traffic of a 128x128 tile with three live accumulators).
+// Design.  One workgroup (8 waves, 2 per SIMD) owns a 256x256 output tile;
+// wave w owns 128x64 of it (4x2 MFMA tiles of 32x32, 128 FP32 accumulators
+// per lane), so while one wave of a SIMD waits at a barrier or runs a chain
+// transition the other keeps the matrix unit busy.  Operands are K-blocked
+// E4M3 planes ([k/64][rows][64 B]): one K=64 stage of a 256-row tile is one
+// contiguous 16 KiB block.  Stages stream into a 4-deep LDS ring (32 KiB per
+// stage) through global_load_lds_dwordx4 (issued by inline asm, so every
+// wait on it is explicit: s_waitcnt vmcnt + s_barrier), three stages ahead,
+// with an XOR swizzle of the 16-byte chunks (row bits 1..3) that keeps the
+// fragment reads bank-conflict free.  The three products of a modulus run as
+// sequential "chains" on ONE accumulator set: after each pair of planes the
+// exact integer accumulator is reduced mod m and re-seeded as
+// acc * (c_this / c_next) mod m, so the next chain continues the residue.
 #include "oz2_internal.h"
 
 namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
-typedef float v4f __attribute__((ext_vector_type(4)));
-
-constexpr int TILE = OZ2_TILE;          // 256
-constexpr int KS = OZ2_KSTEP;           // 128
-constexpr int OPB = TILE * KS;          // bytes of one operand stage: 32 KiB
-constexpr int STAGEB = 2 * OPB;         // A + B
-constexpr int LDS_BYTES = 2 * STAGEB;   // double buffered: 128 KiB
-
+typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
-// Asynchronous global -> LDS copy of one stage (A and B operand tiles of 256
-// rows x 128 k bytes) with global_load_lds_dwordx4: each instruction writes a
-// contiguous 1 KiB LDS block (lane L at +16 L), i.e. 8 tile rows; the XOR
-// swizzle (physical chunk = logical chunk ^ (row & 7)) is realised by
-// permuting the global addresses.  No VGPRs hold the data in flight.
-__device__ __forceinline__ void issue_stage(const uint8_t* __restrict__ a,
-                                            const uint8_t* __restrict__ b, int kp, int k0,
-                                            uint8_t* st) {
+constexpr int TILE = OZ2_TILE;   // 256
+constexpr int KS = OZ2_KBLK;     // 64 k bytes per stage
+constexpr int OPB = TILE * KS;   // 16 KiB per operand per stage
+constexpr int STB = 2 * OPB;     // 32 KiB per stage
+constexpr int NB = 4;            // ring depth
+constexpr int NT = 512;          // threads per workgroup
+
+__device__ __forceinline__ void bar() { asm volatile("s_barrier" ::: "memory"); }
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// chunk swizzle of LDS row r: conflict free for 16 consecutive rows
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
+
+// global_load_lds_dwordx4: lane L's 16 bytes land at M0 + 16 L.
+__device__ __forceinline__ void dma16(const uint8_t* sbase, uint32_t voff, uint32_t m0) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(m0)
+               : "memory");
+}
+
+struct Ctx {
+  const uint8_t* a0;   // first row of this tile in k-block 0 of the modulus' plane 0 (A)
+  const uint8_t* b0;   // same for B
+  size_t psA, psB;     // plane strides (bytes)
+  size_t kbA, kbB;     // k-block strides (padded rows * 64)
+  int kb0, nk, T, s;   // first k-block, stages per pair, total stages, sqrt(m) or 0
+};
+
+// planes of pair q: square  (1,0) (0,1) | (0,0);  nonsquare (1,1) | (0,0) | (2,2)
+__device__ __forceinline__ int planeA(int s, int q) {
+  return s ? (q == 0 ? 1 : 0) : (q == 0 ? 1 : (q == 1 ? 0 : 2));
+}
+__device__ __forceinline__ int planeB(int s, int q) {
+  return s ? (q == 1 ? 1 : 0) : (q == 0 ? 1 : (q == 1 ? 0 : 2));
+}
+
+// One stage = A tile (16 x 1 KiB blocks of 16 rows) + B tile (16 blocks);
+// wave w moves blocks w + 8j (j = 0..3); blocks 0..15 are A, 16..31 are B.
+// Lane L writes row 16 blk + L/4, physical chunk L%4 = logical chunk ^ swz.
+__device__ __forceinline__ void issue_stage(const Ctx& x, int it, uint32_t lbase) {
+  const int q = it / x.nk, ks = it - q * x.nk;
+  const int kb = x.kb0 + ks;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int r8 = lane >> 3;
-  const uint32_t lo = (uint32_t)(r8 * kp + 16 * ((lane & 7) ^ r8));   // per-lane, < 8 kp
-  const uint8_t* ab = a + k0 + (size_t)(8 * w) * kp;                   // wave-uniform bases
-  const uint8_t* bb = b + k0 + (size_t)(8 * w) * kp;
-  lds_u8* sl = (lds_u8*)st + w * 1024;
+  const int rb = lane >> 2;
+  const uint32_t lo = (uint32_t)(rb * KS + 16 * ((lane & 3) ^ swz(rb)));
+  const uint8_t* ab = x.a0 + (size_t)planeA(x.s, q) * x.psA + (size_t)kb * x.kbA;
+  const uint8_t* bb = x.b0 + (size_t)planeB(x.s, q) * x.psB + (size_t)kb * x.kbB;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const size_t rowj = (size_t)(32 * j) * kp;
-    __builtin_amdgcn_global_load_lds((const void*)(ab + rowj + lo),
-                                     (void __attribute__((address_space(3)))*)(sl + j * 4096), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds((const void*)(bb + rowj + lo),
-                                     (void __attribute__((address_space(3)))*)(sl + OPB + j * 4096), 16, 0,
-                                     0);
+  for (int j = 0; j < 4; ++j) {
+    const int blk = w + 8 * j;
+    if (blk < 16) dma16(ab + (size_t)blk * 1024, lo, lbase + blk * 1024);
+    else dma16(bb + (size_t)(blk - 16) * 1024, lo, lbase + OPB + (blk - 16) * 1024);
   }
 }
 
-__device__ __forceinline__ v8i frag(const uint8_t* p, int o0, int o1) {
+__device__ __forceinline__ v8i ldfrag(const uint8_t* p, int o0, int o1) {
   const uint4 lo = *reinterpret_cast<const uint4*>(p + o0);
   const uint4 hi = *reinterpret_cast<const uint4*>(p + o1);
   return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
 }
 
-// Fragments of one K-step for the wave's 128x128 sub-tile: 8 A and 8 B
-// 16x128 fragments (lane -> row lane&15, k bytes 32*(lane>>4)..+31).
-__device__ __forceinline__ void read_frags(const uint8_t* st, v8i (&fa)[8], v8i (&fb)[8]) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wr = w >> 1, wc = w & 1;
-  const int g = lane >> 4, sw = lane & 7;
-  const int o0 = 16 * ((2 * g) ^ sw), o1 = 16 * ((2 * g + 1) ^ sw);
-  const uint8_t* sa = st + (wr * 128 + (lane & 15)) * KS;
-  const uint8_t* sb = st + OPB + (wc * 128 + (lane & 15)) * KS;
+// Fragments of wave w: rows (w>>2)*128 + 32x + lane%32, columns (w&3)*64 + 32y
+// + lane%32; lane half h = lane/32 holds k bytes 32h..32h+31.
+__device__ __forceinline__ void frags(const uint8_t* st, v8i (&fa)[4], v8i (&fb)[2]) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wr = w >> 2, wc = w & 3;
+  const int h = lane >> 5, sw = swz(lane & 31);
+  const int o0 = 16 * ((2 * h) ^ sw), o1 = 16 * ((2 * h + 1) ^ sw);
+  const uint8_t* sa = st + (wr * 128 + (lane & 31)) * KS;
+  const uint8_t* sb = st + OPB + (wc * 64 + (lane & 31)) * KS;
 #pragma unroll
-  for (int x = 0; x < 8; ++x) {
-    fa[x] = frag(sa + x * 16 * KS, o0, o1);
-    fb[x] = frag(sb + x * 16 * KS, o0, o1);
+  for (int x = 0; x < 4; ++x) fa[x] = ldfrag(sa + x * 32 * KS, o0, o1);
+#pragma unroll
+  for (int y = 0; y < 2; ++y) fb[y] = ldfrag(sb + y * 32 * KS, o0, o1);
+}
+
+// Tile of block b.  Blocks are dispatched round-robin over the 8 XCDs (each
+// with its own L2); when the grid allows it each XCD gets a 4x8 group of
+// tiles per 256-block round (4 A row panels, 8 B column panels).
+__device__ __forceinline__ int tile_of(int b, int ntm, int ntn) {
+  if ((ntm % 4) || (ntn % 8) || ((ntm * ntn) % 256)) return b;
+  const int xcd = b & 7, slot = b >> 3;
+  const int grp = slot >> 5, in = slot & 31;
+  const int gid = grp * 8 + xcd, ngx = ntm / 4;
+  const int gm = gid % ngx, gn = gid / ngx;
+  return (gm * 4 + (in & 3)) + (gn * 8 + (in >> 2)) * ntm;
+}
+
+// Main loop over stages [it0, it0 + n) of the stage sequence.
+__device__ __forceinline__ void run_stages(const Ctx& x, uint8_t* LB, uint32_t lds0, int it0, int n,
+                                           v16f (&acc)[4][2]) {
+  const int T = x.T;
+  for (int it = it0; it < it0 + n; ++it) {
+    // this wave's DMA share is 4 instructions per stage; stages it+1, it+2
+    // may still be in flight
+    if (it + 2 < T) wait_vm<8>();
+    else if (it + 1 < T) wait_vm<4>();
+    else wait_vm<0>();
+    bar();
+    v8i fa[4], fb[2];
+    frags(LB + (it & 3) * STB, fa, fb);
+    if (it + 3 < T) issue_stage(x, it + 3, lds0 + ((it + 3) & 3) * STB);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[i], fb[j], acc[i][j], 0, 0,
+                                                                   0, 0, 0, 0);
   }
 }
 
-__device__ __forceinline__ void mma_stage(const v8i (&fa)[8], const v8i (&fb)[8], v4f (&acc)[8][8]) {
+__device__ __forceinline__ void prologue(const Ctx& x, uint32_t lds0) {
 #pragma unroll
-  for (int a = 0; a < 8; ++a)
-#pragma unroll
-    for (int b = 0; b < 8; ++b)
-      acc[a][b] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(fa[a], fb[b], acc[a][b], 0, 0, 0,
-                                                                  0, 0, 0);
+  for (int t = 0; t < NB - 1; ++t)
+    if (t < x.T) issue_stage(x, t, lds0 + t * STB);
 }
 
 // ------------------------------------------------------------- code GEMM
 // grid: (tiles, code slabs).  G'[i][j] <= 256 * 65536 = 2^24: exact in FP32.
-__global__ void __launch_bounds__(256, 1)
-k_codegemm(const uint8_t* __restrict__ cA, const uint8_t* __restrict__ cB, int mp, int np, int kp,
-           int k, uint32_t* Rmax, uint32_t* Kmax) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  const int ntm = mp / TILE;
-  const int tile = blockIdx.x, slab = blockIdx.y;
+__global__ void __launch_bounds__(NT, 1)
+k_codegemm(const uint8_t* __restrict__ cA, const uint8_t* __restrict__ cB, int mp, int np,
+           int kp, uint32_t* Rmax, uint32_t* Kmax) {
+  __shared__ __attribute__((aligned(16))) uint8_t LB[NB * STB];
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)LB;
+  const int ntm = mp / TILE, ntn = np / TILE;
+  const int tile = tile_of(blockIdx.x, ntm, ntn), slab = blockIdx.y;
   const int tm = tile % ntm, tn = tile / ntm;
-  const int kbeg = slab * OZ2_CSLAB;
-  const int kend = min(kp, kbeg + OZ2_CSLAB);
-  const int nk = (kend - kbeg) / KS;
-  const uint8_t* a = cA + (size_t)tm * TILE * kp;
-  const uint8_t* b = cB + (size_t)tn * TILE * kp;
+  const int kbeg = slab * OZ2_CSLAB, kend = min(kp, kbeg + OZ2_CSLAB);
+  Ctx x;
+  x.psA = x.psB = 0;
+  x.kbA = (size_t)mp * KS;
+  x.kbB = (size_t)np * KS;
+  x.a0 = cA + (size_t)tm * TILE * KS;
+  x.b0 = cB + (size_t)tn * TILE * KS;
+  x.kb0 = kbeg / KS;
+  x.nk = (kend - kbeg) / KS;
+  x.T = x.nk;
+  x.s = 0;
+  v16f acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = v16f{0.f};
+  prologue(x, lds0);
+  run_stages(x, LB, lds0, 0, x.T, acc);
 
-  v4f acc[8][8];
+  // lane holds rows 32x + 8(e/4) + 4(lane/32) + e%4 of column 32y + lane%32
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int row0 = tm * TILE + (w >> 2) * 128, col0 = tn * TILE + (w & 3) * 64;
 #pragma unroll
-  for (int x = 0; x < 8; ++x)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int y = 0; y < 8; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
-
-  issue_stage(a, b, kp, kbeg, lds);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  for (int it = 0; it < nk; ++it) {
-    v8i fa[8], fb[8];
-    read_frags(lds + (it & 1) * STAGEB, fa, fb);
-    if (it + 1 < nk) issue_stage(a, b, kp, kbeg + (it + 1) * KS, lds + ((it + 1) & 1) * STAGEB);
-    mma_stage(fa, fb, acc);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-  }
-
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wr = w >> 1, wc = w & 1;
-  const int row0 = tm * TILE + wr * 128, col0 = tn * TILE + wc * 128;
-  // row maxima: lane holds rows 4*(lane>>4)+j of column (lane & 15)
-#pragma unroll
-  for (int x = 0; x < 8; ++x)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float v = acc[x][0][j];
-#pragma unroll
-      for (int y = 1; y < 8; ++y) v = fmaxf(v, acc[x][y][j]);
+    for (int e = 0; e < 16; ++e) {
+      float v = fmaxf(acc[i][0][e], acc[i][1][e]);
       v = fmaxf(v, __shfl_xor(v, 1));
       v = fmaxf(v, __shfl_xor(v, 2));
       v = fmaxf(v, __shfl_xor(v, 4));
       v = fmaxf(v, __shfl_xor(v, 8));
-      if ((lane & 15) == 0)
-        atomicMax(Rmax + (size_t)slab * mp + row0 + x * 16 + 4 * (lane >> 4) + j, (uint32_t)v);
+      v = fmaxf(v, __shfl_xor(v, 16));
+      if ((lane & 31) == 0)
+        atomicMax(Rmax + (size_t)slab * mp + row0 + 32 * i + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3),
+                  (uint32_t)v);
     }
 #pragma unroll
-  for (int y = 0; y < 8; ++y) {
-    float v = acc[0][y][0];
+  for (int j = 0; j < 2; ++j) {
+    float v = acc[0][j][0];
 #pragma unroll
-    for (int x = 0; x < 8; ++x)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) v = fmaxf(v, acc[x][y][j]);
-    v = fmaxf(v, __shfl_xor(v, 16));
+      for (int e = 0; e < 16; ++e) v = fmaxf(v, acc[i][j][e]);
     v = fmaxf(v, __shfl_xor(v, 32));
-    if (lane < 16) atomicMax(Kmax + (size_t)slab * np + col0 + y * 16 + lane, (uint32_t)v);
+    if (lane < 32) atomicMax(Kmax + (size_t)slab * np + col0 + 32 * j + lane, (uint32_t)v);
   }
 }
 
 // ------------------------------------------------------------- residue GEMM
-// grid: (tiles, r).  One modulus per workgroup over K in [kbeg, kend).
-__global__ void __launch_bounds__(256, 1)
+// grid: (tiles, r).  One modulus per workgroup over k in [kbeg, kend).
+__global__ void __launch_bounds__(NT, 1)
 k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, int mp,
           int np, int kp, int kbeg, int kend, int accumulate, int16_t* __restrict__ res) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  const int ntm = mp / TILE;
-  const int tile = blockIdx.x, mi = blockIdx.y;
+  __shared__ __attribute__((aligned(16))) uint8_t LB[NB * STB];
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)LB;
+  const int ntm = mp / TILE, ntn = np / TILE;
+  const int tile = tile_of(blockIdx.x, ntm, ntn), mi = blockIdx.y;
   const int tm = tile % ntm, tn = tile / ntm;
   const int m = c.m[mi], s = c.sq[mi], pb = c.pbase[mi];
-  const float inv = c.finv[mi];
-  const size_t psA = (size_t)mp * kp, psB = (size_t)np * kp;
-  const uint8_t* a0 = PA + (size_t)pb * psA + (size_t)tm * TILE * kp;
-  const uint8_t* b0 = PB + (size_t)pb * psB + (size_t)tn * TILE * kp;
-  // pairs of planes (A plane, B plane) and chain boundaries:
-  //   square:    q=0 (1,0), q=1 (0,1)  -> chain 0 ends, x rho0 (= s)
-  //              q=2 (0,0)             -> final, x 1
-  //   nonsquare: q=0 (1,1)             -> chain 0 ends, x rho0 (= -16)
-  //              q=1 (0,0)             -> chain 1 ends, x rho1 (= -15/16)
-  //              q=2 (2,2)             -> final, x 16
-  auto planeA = [s](int q) { return s ? (q == 0 ? 1 : 0) : (q == 0 ? 1 : (q == 1 ? 0 : 2)); };
-  auto planeB = [s](int q) { return s ? (q == 1 ? 1 : 0) : (q == 0 ? 1 : (q == 1 ? 0 : 2)); };
-  const int nk = (kend - kbeg) / KS;
+  const float fm = (float)m, inv = c.finv[mi];
+  Ctx x;
+  x.psA = (size_t)mp * kp;
+  x.psB = (size_t)np * kp;
+  x.kbA = (size_t)mp * KS;
+  x.kbB = (size_t)np * KS;
+  x.a0 = PA + (size_t)pb * x.psA + (size_t)tm * TILE * KS;
+  x.b0 = PB + (size_t)pb * x.psB + (size_t)tn * TILE * KS;
+  x.kb0 = kbeg / KS;
+  x.nk = (kend - kbeg) / KS;
+  x.T = 3 * x.nk;
+  x.s = s;
+  v16f acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = v16f{0.f};
 
-  v4f acc[8][8];
+  // chain transition after a pair: acc <- (acc * rho) reduced mod m with
+  // |result| <= m/2 + 2, in exact fp32 (every intermediate is an integer
+  // below 2^24).  rho = 1 is a plain reduction inside the square chain.
+  auto transition = [&](const float rho) {
 #pragma unroll
-  for (int x = 0; x < 8; ++x)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int y = 0; y < 8; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float v = acc[i][j][e];
+          const float y = __builtin_fmaf(-rintf(v * inv), fm, v);
+          const float z = y * rho;
+          acc[i][j][e] = __builtin_fmaf(-rintf(z * inv), fm, z);
+        }
+  };
+  const float rho_a = s ? 1.0f : (float)c.rho0[mi];
+  const float rho_b = s ? (float)c.rho0[mi] : (float)c.rho1[mi];
+  prologue(x, lds0);
+  run_stages(x, LB, lds0, 0, x.nk, acc);
+  transition(rho_a);
+  run_stages(x, LB, lds0, x.nk, x.nk, acc);
+  transition(rho_b);
+  run_stages(x, LB, lds0, 2 * x.nk, x.nk, acc);
+  wait_vm<0>();
 
-  issue_stage(a0 + (size_t)planeA(0) * psA, b0 + (size_t)planeB(0) * psB, kp, kbeg, lds);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  for (int q = 0; q < 3; ++q) {
-    for (int ks = 0; ks < nk; ++ks) {
-      v8i fa[8], fb[8];
-      read_frags(lds + ((q * nk + ks) & 1) * STAGEB, fa, fb);
-      const int qn = (ks + 1 == nk) ? q + 1 : q, ksn = (ks + 1 == nk) ? 0 : ks + 1;
-      if (qn < 3)
-        issue_stage(a0 + (size_t)planeA(qn) * psA, b0 + (size_t)planeB(qn) * psB, kp,
-                    kbeg + ksn * KS, lds + ((q * nk + ks + 1) & 1) * STAGEB);
-      mma_stage(fa, fb, acc);
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-    }
-    if (s ? (q == 1) : (q < 2)) {
-      // chain transition: acc <- (acc * rho) reduced mod m, |result| <= m/2 + 2
-      const int rho = (q == 0 || s) ? c.rho0[mi] : c.rho1[mi];
-#pragma unroll
-      for (int x = 0; x < 8; ++x) {
-#pragma unroll
-        for (int y = 0; y < 8; ++y)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int v = (int)acc[x][y][j];
-            acc[x][y][j] = (float)oz2_red(oz2_red(v, m, inv) * rho, m, inv);
-          }
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-  }
-
-  // final epilogue: centred residue of fin * acc (+ previous slab's residue)
+  // final epilogue: centred residue of fin * acc (+ the previous slab's)
   const int fin = c.fin[mi];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int16_t* dst = res + (size_t)mi * mp * np + (size_t)tile * (TILE * TILE) + (size_t)w * 16384 +
-                 lane * 4;
+  int16_t* dst = res + (size_t)mi * mp * np + (size_t)tile * (TILE * TILE) + (size_t)w * 8192 +
+                 lane * 16;
 #pragma unroll
-  for (int x = 0; x < 8; ++x)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int y = 0; y < 8; ++y) {
-      int r4[4];
+    for (int j = 0; j < 2; ++j) {
+      int r16[16];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        int v = (int)acc[x][y][j];
-        if (fin != 1) v = oz2_red(v, m, inv) * fin;
-        r4[j] = oz2_centre(v, m, inv);
+      for (int e = 0; e < 16; ++e) {
+        float v = acc[i][j][e];
+        if (fin != 1) v = __builtin_fmaf(-rintf(v * inv), fm, v) * (float)fin;
+        r16[e] = oz2_centre((int)v, m, inv);
       }
-      uint2* p = reinterpret_cast<uint2*>(dst + (x * 8 + y) * 256);
+      uint4* p = reinterpret_cast<uint4*>(dst + (i * 2 + j) * 1024);
       if (accumulate) {
-        uint2 o = *p;
-        int o4[4] = {(int)(int16_t)(o.x & 0xFFFF), (int)(int16_t)(o.x >> 16),
-                     (int)(int16_t)(o.y & 0xFFFF), (int)(int16_t)(o.y >> 16)};
+        const uint4 o0 = p[0], o1 = p[1];
+        const uint32_t ow[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
 #pragma unroll
-        for (int j = 0; j < 4; ++j) r4[j] = oz2_centre(r4[j] + o4[j], m, inv);
+        for (int e = 0; e < 16; ++e) {
+          const int old = (int)(int16_t)((ow[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
+          r16[e] = oz2_centre(r16[e] + old, m, inv);
+        }
       }
-      uint2 o;
-      o.x = ((uint32_t)r4[0] & 0xFFFFu) | ((uint32_t)r4[1] << 16);
-      o.y = ((uint32_t)r4[2] & 0xFFFFu) | ((uint32_t)r4[3] << 16);
-      *p = o;
+      uint32_t pk[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        pk[e] = ((uint32_t)r16[2 * e] & 0xFFFFu) | ((uint32_t)r16[2 * e + 1] << 16);
+      p[0] = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+      p[1] = make_uint4(pk[4], pk[5], pk[6], pk[7]);
     }
-}
-
-bool g_attr_done = false;
-
-hipError_t set_attrs() {
-  if (g_attr_done) return hipSuccess;
-  hipError_t e = hipFuncSetAttribute((const void*)k_codegemm,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
-  if (e != hipSuccess) return e;
-  e = hipFuncSetAttribute((const void*)k_resgemm, hipFuncAttributeMaxDynamicSharedMemorySize,
-                          LDS_BYTES);
-  if (e != hipSuccess) return e;
-  g_attr_done = true;
-  return hipSuccess;
 }
 
 }  // namespace
 
 hipError_t oz2_launch_codegemm(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, hipStream_t s) {
-  hipError_t e = set_attrs();
-  if (e != hipSuccess) return e;
   dim3 grid((d.mp / TILE) * (d.np / TILE), d.cslabs);
-  hipLaunchKernelGGL(k_codegemm, grid, dim3(256), LDS_BYTES, s, ws + L.codesA, ws + L.codesB, d.mp,
-                     d.np, d.kp, d.k, (uint32_t*)(ws + L.Rmax), (uint32_t*)(ws + L.Kmax));
+  hipLaunchKernelGGL(k_codegemm, grid, dim3(NT), 0, s, ws + L.codesA, ws + L.codesB, d.mp, d.np,
+                     d.kp, (uint32_t*)(ws + L.Rmax), (uint32_t*)(ws + L.Kmax));
   return hipGetLastError();
 }
 
 hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
                               uint8_t* ws, hipStream_t s) {
-  hipError_t e = set_attrs();
-  if (e != hipSuccess) return e;
   dim3 grid((d.mp / TILE) * (d.np / TILE), c.r);
   for (int kb = 0, sl = 0; kb < d.kp; kb += OZ2_KSLAB, ++sl) {
-    int ke = kb + OZ2_KSLAB < d.kp ? kb + OZ2_KSLAB : d.kp;
-    hipLaunchKernelGGL(k_resgemm, grid, dim3(256), LDS_BYTES, s, c, ws + L.planesA, ws + L.planesB,
-                       d.mp, d.np, d.kp, kb, ke, sl > 0 ? 1 : 0, (int16_t*)(ws + L.res));
-    e = hipGetLastError();
+    const int ke = kb + OZ2_KSLAB < d.kp ? kb + OZ2_KSLAB : d.kp;
+    hipLaunchKernelGGL(k_resgemm, grid, dim3(NT), 0, s, c, ws + L.planesA, ws + L.planesB, d.mp,
+                       d.np, d.kp, kb, ke, sl > 0 ? 1 : 0, (int16_t*)(ws + L.res));
+    const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -5,9 +5,11 @@
 #include <stdint.h>
 
 #define OZ2_MAXR 16
-#define OZ2_NLIMB 5          // 36-bit limbs of the CRT sum: 180 bits >= log2(16 * 545 * M_max)
+#define OZ2_NLIMB 5          // 32-bit words of the exact integer: 160 bits > log2(M_max) + 1
 #define OZ2_TILE 256         // output tile of the FP8 GEMMs (rows and columns)
-#define OZ2_KSTEP 128        // K per LDS stage = K of one v_mfma_f32_16x16x128_f8f6f4
+#define OZ2_KBLK 64          // k bytes per block of the K-blocked planes = K of one
+                             // v_mfma_f32_32x32x64_f8f6f4 = one GEMM stage
+#define OZ2_KPAD 64          // k is padded to a multiple of this
 #define OZ2_KSLAB 32768      // residue GEMM: k per exact FP32 slab, Eq. (accum-exact)
 #define OZ2_CSLAB 65536      // code GEMM: codes <= 16, products <= 256: 65536*256 = 2^24
 
@@ -30,16 +32,16 @@ struct Oz2Const {
   float finv_s[OZ2_MAXR];     // RN(1/s) in fp32 (square moduli)
   double dinv[OZ2_MAXR];      // RN(1/m) in fp64
   // direct CRT sum: X = sum_i x_i W_i - q M, W_i = (M/m_i) * ((M/m_i)^-1 mod m_i)
-  double W[OZ2_MAXR][OZ2_NLIMB];  // 36-bit limbs of W_i (exact integers)
-  double wfrac[OZ2_MAXR];         // W_i / M rounded to fp64
-  double Ml[OZ2_NLIMB];           // 36-bit limbs of M
-  double Mhalf[OZ2_NLIMB];        // 36-bit limbs of floor(M/2)
+  double W[OZ2_MAXR][OZ2_NLIMB];  // 32-bit words of W_i (exact integers in fp64)
+  double wfrac[OZ2_MAXR];         // W_i / M = inv_i / m_i rounded to fp64
+  double Ml[OZ2_NLIMB];           // 32-bit words of M
+  double Mhalf[OZ2_NLIMB];        // 32-bit words of floor(M/2)
   int cA, cB;                     // width budgets of the scaling rule
 };
 
 struct Oz2Dims {
   int m, n, k;
-  int mp, np, kp;             // padded: mp, np multiples of OZ2_TILE; kp of OZ2_KSTEP
+  int mp, np, kp;             // padded: mp, np multiples of OZ2_TILE; kp of OZ2_KPAD
   int cslabs;                 // number of code-GEMM slabs
   unsigned flags;
 };
@@ -50,9 +52,10 @@ struct Oz2Layout {
   size_t flagsA, flagsB;      // uint32 [mp] / [np]
   size_t Rmax, Kmax;          // uint32 [cslabs][mp] / [cslabs][np]
   size_t sA, tB;              // int32 [mp] / [np]
-  size_t codesA, codesB;      // uint8 [mp][kp] / [np][kp]
-  size_t planesA, planesB;    // uint8 [P][mp][kp] / [P][np][kp]
-  size_t res;                 // int16 [r][mp*np] (MFMA-native tile order)
+  size_t codesA, codesB;      // uint8 [kp/64][mp][64] / [kp/64][np][64] (K-blocked)
+  size_t planesA, planesB;    // uint8 [P][kp/64][mp][64] / [P][kp/64][np][64] (K-blocked)
+  size_t res;                 // int16 [r][tile][wave 8][x 4][y 2][lane 64][16]
+                              //   (the GEMM's accumulator order, see gemm.hip)
   size_t counters;            // int32 [4]: fallback row / column counts
   size_t listA, listB;        // int32 [mp] / [np]: flagged row / column indices
   size_t total;

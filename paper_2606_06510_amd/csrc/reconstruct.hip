@@ -9,8 +9,8 @@
 // as Garner's Eq. (garner).  On this VALU the direct CRT sum is cheaper than
 // Garner's r(r-1)/2 dependent modular steps:
 //     X = sum_i x_i W_i - q M,  W_i = (M/m_i) ((M/m_i)^-1 mod m_i),
-// evaluated exactly in fp64 on 32-bit limbs (|x_i| <= 545, limbs < 2^32:
-// every partial limb sum is an integer below 2^46), with q = rint(sum_i x_i
+// evaluated exactly in fp64 on 32-bit words (|x_i| <= 545, words < 2^32:
+// every partial word sum is an integer below 2^46), with q = rint(sum_i x_i
 // W_i/M) (error < 2^-35; an exact range check fixes the rare ambiguous case).
 // The limbs are normalised to five 32-bit words (two's complement), and
 // rounded once to binary64 with the exponent shift -(s_i + t_j), including
@@ -21,18 +21,24 @@ namespace {
 
 constexpr int NL = OZ2_NLIMB;
 
-// Residues of 4 outputs, packed as the residue buffer holds them: per modulus
-// one uint2 = 4 int16 (output j in half j of the two words).
-template <int J>
-__device__ __forceinline__ int unpack(const uint2& v) {
-  const uint32_t wd = (J < 2) ? v.x : v.y;
-  return (J & 1) ? (int)(int16_t)(wd >> 16) : (int)(int16_t)(wd & 0xFFFFu);
+// Residues of a thread's 16 outputs, as the residue buffer holds them: per
+// modulus one uint4 pair = 16 int16 (output e in half e%2 of word e/2).
+struct Res16 {
+  uint4 lo, hi;
+};
+
+template <int E>
+__device__ __forceinline__ int unpack(const Res16& v) {
+  constexpr int wi = E >> 1;
+  const uint32_t wd = wi == 0 ? v.lo.x : wi == 1 ? v.lo.y : wi == 2 ? v.lo.z : wi == 3 ? v.lo.w
+                    : wi == 4 ? v.hi.x : wi == 5 ? v.hi.y : wi == 6 ? v.hi.z : v.hi.w;
+  return (E & 1) ? (int)(int16_t)(wd >> 16) : (int)(int16_t)(wd & 0xFFFFu);
 }
 
-// Exact integer of output J of the 4 from its r centred residues: 5 words,
+// Exact integer of output E of the 16 from its r centred residues: 5 words,
 // two's complement, little endian.
-template <int R, int J>
-__device__ __forceinline__ void crt_words(const Oz2Const& c, const uint2 (&x)[OZ2_MAXR],
+template <int R, int E>
+__device__ __forceinline__ void crt_words(const Oz2Const& c, const Res16 (&x)[OZ2_MAXR],
                                           uint32_t (&w)[NL]) {
   double S[NL];
 #pragma unroll
@@ -40,7 +46,7 @@ __device__ __forceinline__ void crt_words(const Oz2Const& c, const uint2 (&x)[OZ
   double f = 0.0;
 #pragma unroll
   for (int i = 0; i < R; ++i) {
-    const double xi = (double)unpack<J>(x[i]);
+    const double xi = (double)unpack<E>(x[i]);
 #pragma unroll
     for (int j = 0; j < NL; ++j) S[j] = fma(xi, c.W[i][j], S[j]);
     f = fma(xi, c.wfrac[i], f);
@@ -145,43 +151,70 @@ __device__ __forceinline__ double round_scaled(uint32_t (&w)[NL], int e) {
   return neg ? -r : r;
 }
 
-// Thread per (tile, wave, 16x16 block, lane): 4 outputs, rows 4*(lane>>4)+j of
-// column lane&15 of the block -- the MFMA-native order of the residue buffer.
+// Thread per (tile, wave, 32x32 block, lane): 16 outputs of column col,
+// rows row + 8(e/4) + (e%4), e = 0..15 -- the residue GEMM's accumulator order
+// (wave w owns rows (w>>2)*128 + 32x, columns (w&3)*64 + 32y of the tile).
 __device__ __forceinline__ void out_coords(int mp, size_t gid, int& row, int& col, size_t& roff) {
   const int ntm = mp / OZ2_TILE;
-  const size_t tile = gid >> 14;                  // 16384 threads per 256x256 tile
-  const int q = (int)(gid & 16383);
-  const int lane = q & 63, blk = q >> 6;          // blk = (w*8 + x)*8 + y
-  const int y = blk & 7, x = (blk >> 3) & 7, w = blk >> 6;
+  const size_t tile = gid >> 12;                  // 4096 threads per 256x256 tile
+  const int q = (int)(gid & 4095);
+  const int lane = q & 63, blk = q >> 6;          // blk = (w*4 + x)*2 + y
+  const int y = blk & 1, x = (blk >> 1) & 3, w = blk >> 3;
   const int tm = (int)(tile % ntm), tn = (int)(tile / ntm);
-  row = tm * OZ2_TILE + (w >> 1) * 128 + x * 16 + 4 * (lane >> 4);
-  col = tn * OZ2_TILE + (w & 1) * 128 + y * 16 + (lane & 15);
-  roff = tile * (OZ2_TILE * OZ2_TILE) + (size_t)q * 4;
+  row = tm * OZ2_TILE + (w >> 2) * 128 + x * 32 + 4 * (lane >> 5);
+  col = tn * OZ2_TILE + (w & 3) * 64 + y * 32 + (lane & 31);
+  roff = tile * (OZ2_TILE * OZ2_TILE) + (size_t)q * 16;
 }
 
 template <int R>
 __device__ __forceinline__ void load_residues(const int16_t* __restrict__ res, size_t plane,
-                                              size_t roff, uint2 (&x)[OZ2_MAXR]) {
+                                              size_t roff, Res16 (&x)[OZ2_MAXR]) {
 #pragma unroll
-  for (int i = 0; i < OZ2_MAXR; ++i)
-    x[i] = (i < R) ? *reinterpret_cast<const uint2*>(res + (size_t)i * plane + roff)
-                   : make_uint2(0u, 0u);
+  for (int i = 0; i < OZ2_MAXR; ++i) {
+    if (i < R) {
+      const uint4* p = reinterpret_cast<const uint4*>(res + (size_t)i * plane + roff);
+      x[i].lo = p[0];
+      x[i].hi = p[1];
+    } else {
+      x[i].lo = x[i].hi = make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
 }
 
-// one output of the 4 held by a thread: reconstruct, rescale, store
-template <int R, int J>
+// one output of the 16 held by a thread: reconstruct, rescale, store
+template <int R, int E>
 __device__ __forceinline__ void finish_one(const Oz2Const& c, const Oz2Dims& d,
-                                           const uint2 (&x)[OZ2_MAXR], int i, int tj,
+                                           const Res16 (&x)[OZ2_MAXR], int row, int tj,
                                            const int32_t* __restrict__ sA,
                                            const uint32_t* __restrict__ fA, bool acc, bool nofb,
                                            double* out) {
+  const int i = row + 8 * (E >> 2) + (E & 3);
   if (i >= d.m) return;
   if (!nofb && (fA[i] & (OZ2_T1 | OZ2_T2))) return;
   uint32_t w[NL];
-  crt_words<R, J>(c, x, w);
+  crt_words<R, E>(c, x, w);
   const double v = round_scaled(w, sA[i] + tj);
   out[i] = acc ? out[i] + v : v;
 }
+
+template <int R, int E>
+struct Finish {
+  __device__ __forceinline__ static void run(const Oz2Const& c, const Oz2Dims& d,
+                                             const Res16 (&x)[OZ2_MAXR], int row, int tj,
+                                             const int32_t* __restrict__ sA,
+                                             const uint32_t* __restrict__ fA, bool acc, bool nofb,
+                                             double* out) {
+    finish_one<R, E>(c, d, x, row, tj, sA, fA, acc, nofb, out);
+    Finish<R, E + 1>::run(c, d, x, row, tj, sA, fA, acc, nofb, out);
+  }
+};
+template <int R>
+struct Finish<R, 16> {
+  __device__ __forceinline__ static void run(const Oz2Const&, const Oz2Dims&,
+                                             const Res16 (&)[OZ2_MAXR], int, int,
+                                             const int32_t* __restrict__,
+                                             const uint32_t* __restrict__, bool, bool, double*) {}
+};
 
 template <int R>
 __global__ void __launch_bounds__(256)
@@ -199,14 +232,33 @@ k_reconstruct(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res,
   const uint32_t fc = fB[col];
   if (!nofb && (force || (fc & (OZ2_T1 | OZ2_T2)))) return;
   const int tj = tB[col];
-  uint2 x[OZ2_MAXR];
+  Res16 x[OZ2_MAXR];
   load_residues<R>(res, (size_t)d.mp * d.np, roff, x);
   double* out = C + (size_t)col * ldc;
-  finish_one<R, 0>(c, d, x, row + 0, tj, sA, fA, acc, nofb, out);
-  finish_one<R, 1>(c, d, x, row + 1, tj, sA, fA, acc, nofb, out);
-  finish_one<R, 2>(c, d, x, row + 2, tj, sA, fA, acc, nofb, out);
-  finish_one<R, 3>(c, d, x, row + 3, tj, sA, fA, acc, nofb, out);
+  Finish<R, 0>::run(c, d, x, row, tj, sA, fA, acc, nofb, out);
 }
+
+template <int R, int E>
+struct IntOut {
+  __device__ __forceinline__ static void run(const Oz2Const& c, const Oz2Dims& d,
+                                             const Res16 (&x)[OZ2_MAXR], int row, int col,
+                                             uint32_t* out) {
+    const int i = row + 8 * (E >> 2) + (E & 3);
+    if (i < d.m) {
+      uint32_t w[NL];
+      crt_words<R, E>(c, x, w);
+      uint32_t* o = out + ((size_t)col * d.m + i) * NL;
+#pragma unroll
+      for (int q = 0; q < NL; ++q) o[q] = w[q];
+    }
+    IntOut<R, E + 1>::run(c, d, x, row, col, out);
+  }
+};
+template <int R>
+struct IntOut<R, 16> {
+  __device__ __forceinline__ static void run(const Oz2Const&, const Oz2Dims&,
+                                             const Res16 (&)[OZ2_MAXR], int, int, uint32_t*) {}
+};
 
 template <int R>
 __global__ void __launch_bounds__(256)
@@ -216,21 +268,9 @@ k_integers(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res, uint32_t* out
   size_t roff;
   out_coords(d.mp, gid, row, col, roff);
   if (col >= d.n || row >= d.m) return;
-  uint2 x[OZ2_MAXR];
+  Res16 x[OZ2_MAXR];
   load_residues<R>(res, (size_t)d.mp * d.np, roff, x);
-  uint32_t w[4][NL];
-  crt_words<R, 0>(c, x, w[0]);
-  crt_words<R, 1>(c, x, w[1]);
-  crt_words<R, 2>(c, x, w[2]);
-  crt_words<R, 3>(c, x, w[3]);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int i = row + j;
-    if (i >= d.m) break;
-    uint32_t* o = out + ((size_t)col * d.m + i) * NL;
-#pragma unroll
-    for (int q = 0; q < NL; ++q) o[q] = w[j][q];
-  }
+  IntOut<R, 0>::run(c, d, x, row, col, out);
 }
 
 // Compaction of flagged rows / columns into index lists (order irrelevant:
@@ -290,7 +330,7 @@ __global__ void k_fill(double* C, int m, int n, int ldc) {
 template <int R>
 void launch_reconstruct_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
                           double* C, int ldc, hipStream_t s) {
-  const size_t threads = (size_t)d.mp * d.np / 4;
+  const size_t threads = (size_t)d.mp * d.np / 16;
   hipLaunchKernelGGL(k_reconstruct<R>, dim3((unsigned)(threads / 256)), dim3(256), 0, s, c, d,
                      (const int16_t*)(ws + L.res), (const int32_t*)(ws + L.sA),
                      (const int32_t*)(ws + L.tB), (const uint32_t*)(ws + L.flagsA),
@@ -300,7 +340,7 @@ void launch_reconstruct_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& 
 template <int R>
 void launch_integers_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
                        uint32_t* out, hipStream_t s) {
-  const size_t threads = (size_t)d.mp * d.np / 4;
+  const size_t threads = (size_t)d.mp * d.np / 16;
   hipLaunchKernelGGL(k_integers<R>, dim3((unsigned)(threads / 256)), dim3(256), 0, s, c, d,
                      (const int16_t*)(ws + L.res), out);
 }
