@@ -115,6 +115,12 @@ bool make_const(int r, Oz2Const& c) {
     c.wfrac[i] = (double)inv / (double)m;   // W_i / M exactly = inv_i / m_i
   }
   c.P = pb;
+  int off = 0;
+  for (int i = 0; i < r; ++i) {
+    c.toff[i] = off + ms[i] / 2;
+    off += ms[i];
+  }
+  c.tabsz = off;
   Big Mh = M;
   Mh.shr1();
   for (int j = 0; j < OZ2_NLIMB; ++j) {
@@ -165,6 +171,7 @@ Oz2Layout make_layout(const Oz2Dims& d, const Oz2Const& c) {
   L.codesB = take((size_t)d.np * d.kp);
   L.planesA = take((size_t)c.P * d.mp * d.kp);
   L.planesB = take((size_t)c.P * d.np * d.kp);
+  L.tabs = take((size_t)c.tabsz * 4);
   L.res = take((size_t)c.r * d.mp * d.np * 2);
   L.total = o;
   return L;
@@ -243,6 +250,7 @@ int run_deconstruct(ozaki2_plan_s& p, hipStream_t s) {
     if (e == hipSuccess) e = oz2_launch_codegemm(d, p.L, p.ws, s);
   }
   if (e == hipSuccess) e = oz2_launch_scales(d, p.L, p.c, p.ws, s);
+  if (e == hipSuccess) e = oz2_launch_tables(p.L, p.c, p.ws, s);
   if (e == hipSuccess) e = oz2_launch_split(d, p.L, p.c, p.ws, p.A, p.lda, p.B, p.ldb, s);
   return hip_status(e);
 }

@@ -84,23 +84,17 @@ __device__ __forceinline__ uint32_t pack4_fp8(float a, float b, float c, float d
   return (uint32_t)w;
 }
 
-// Row segment of 16 consecutive k for one row of A (TRANS) or column of B;
-// a block of 256 threads covers 64 rows x 64 k.  A-side lanes run along the
-// rows (each load instruction reads 512 contiguous bytes of a column of A);
-// B-side lanes run along k (4 lanes read 512 contiguous bytes of a column
-// of B).  The grid is one-dimensional: block b covers row block b % nrb and
-// k block b / nrb (nrb = padded rows / 64).
-template <bool TRANS>
-__device__ __forceinline__ void seg_coords(int nrb, int& row, int& l0) {
+// Row segment of 16 consecutive k for one row of A (TRANS) or column of B.
+// A tile of 256 threads covers 64 rows x 64 k (one K-block): thread t owns
+// row t/4, k chunk t%4, so every 16-byte store of a wave fills 1 KiB of
+// contiguous K-blocked plane; A's loads read 4 x 128 B per instruction, B's
+// 4 lanes read 512 contiguous bytes of a column.  Tile tl of a 1-D sequence
+// covers row block tl % nrb and k block tl / nrb (nrb = padded rows / 64).
+__device__ __forceinline__ void seg_coords(int tl, int nrb, int& row, int& l0) {
   const int t = threadIdx.x;
-  const int bx = (int)(blockIdx.x % (unsigned)nrb), by = (int)(blockIdx.x / (unsigned)nrb);
-  if (TRANS) {
-    row = bx * 64 + (t & 63);
-    l0 = by * 64 + (t >> 6) * 16;
-  } else {
-    row = bx * 64 + (t >> 2);
-    l0 = by * 64 + (t & 3) * 16;
-  }
+  const int bx = tl % nrb, by = tl / nrb;
+  row = bx * 64 + (t >> 2);
+  l0 = by * 64 + (t & 3) * 16;
 }
 
 // byte offset of (row, k) in a K-blocked plane [kp/64][rows_pad][64]
@@ -125,7 +119,7 @@ __global__ void k_codes(const double* __restrict__ X, int ld, int rows, int nrb,
                         const unsigned long long* __restrict__ bits, uint8_t* __restrict__ codes) {
   const int rows_pad = nrb * 64;
   int row, l0;
-  seg_coords<TRANS>(nrb, row, l0);
+  seg_coords(blockIdx.x, nrb, row, l0);
   unsigned long long b = row < rows ? bits[row] : 0ull;
   bool t1 = b >= kInfBits;
   int E = (b == 0 || t1) ? 0 : exp_of_bits(b);
@@ -198,109 +192,132 @@ __global__ void k_scales(Oz2Dims d, const unsigned long long* __restrict__ rowbi
   }
 }
 
-// Centred residue of the exact integer a (|a| <= 2^62, a double) modulo m:
-// a = ah 2^32 + al (exact), t = ah (2^32 mod m) + al (exact, |t| < 2^42),
-// r = t - m floor(t/m) with one correction each way (the fp64 quotient
-// estimate of |t| < 2^42 is within 2^-18 of the true one).
-__device__ __forceinline__ int centred_residue(double ah, double al, int m, int c32, double dinv) {
-  double t = fma(ah, (double)c32, al);
-  double q = floor(t * dinv);
-  double r = fma(-q, (double)m, t);
-  r = (r < 0.0) ? r + (double)m : r;
-  r = (r >= (double)m) ? r - (double)m : r;
-  int ri = (int)r;
-  return (ri >= ((m + 1) >> 1)) ? ri - m : ri;
+// Centred residue of the exact integer a = ah 2^32 + al (|a| <= 2^62) modulo m:
+// t = ah (2^32 mod m) + al is exact (|t| < 2^42) and congruent to a; then
+// q = floor(t/m + 1/2) and d = t - q m is the centred residue in
+// [-floor(m/2), ceil(m/2) - 1].  The fp64 value of t/m + 1/2 is within 2^-18
+// of the true one, and the true one is never within 1/(2m) of an integer for
+// odd m (t/m is never a half-integer); for m = 1024 every step is exact.  So
+// the floor is always the exact one.
+__device__ __forceinline__ int centred_residue(double ah, double al, double m, double c32,
+                                               double dinv) {
+  const double t = fma(ah, c32, al);
+  const double q = floor(fma(t, dinv, 0.5));
+  return (int)fma(-q, m, t);
 }
 
-// Balanced base-s digits of a centred residue of m = s^2 (Eq. (sq-shortcut)):
-// d0 = ((d + floor(s/2)) mod s) - floor(s/2), d1 = (d - d0)/s.
-__device__ __forceinline__ void split_square(int dres, int s, int m, float inv_s, int& d0, int& d1) {
-  int h = s >> 1;
-  int u = dres + h + m;                  // in [0, 2m)
-  int q = (int)((float)u * inv_s);
-  int r = u - q * s;
-  r += (r < 0) ? s : 0;
-  r -= (r >= s) ? s : 0;
-  d0 = r - h;
-  d1 = (int)rintf((float)(dres - d0) * inv_s);
-}
-
-// Balanced base-16 digits with the carry correction of the "e4m3 layout
-// envelope" paragraph: if d0+d1 is not E4M3-exact (odd and above 16 in
-// magnitude), move one unit of base weight: (d0 - 16 sgn(d0), d1 + sgn(d0)).
-__device__ __forceinline__ void split_tail(int dres, int& d0, int& d1) {
-  d0 = ((dres + 8) & 15) - 8;
-  d1 = (dres - d0) >> 4;
-  int sm = d0 + d1;
-  int am = sm < 0 ? -sm : sm;
-  if (am > 16 && (am & 1)) {
-    int sg = d0 > 0 ? 1 : -1;
-    d0 -= 16 * sg;
-    d1 += sg;
+// Digit planes of a centred residue d of m (the E4M3-exact layouts of the
+// "frozen plane kernel" section):
+//  * square m = s^2, Eq. (sq-shortcut): balanced base-s digits
+//    d0 = ((d + floor(s/2)) mod s) - floor(s/2), d1 = (d - d0)/s;
+//  * nonsquare, Eq. (kar) with b = 4: balanced base-16 digits with the carry
+//    correction of the "e4m3 layout envelope" paragraph (if d0+d1 is not
+//    E4M3-exact -- odd and above 16 in magnitude -- move one unit of base
+//    weight: (d0 - 16 sgn(d0), d1 + sgn(d0))), plus the sum plane d0+d1.
+__device__ __forceinline__ void digits(int d, int m, int s, int& d0, int& d1) {
+  if (s) {
+    const int h = s >> 1;
+    int u = (d + h) % s;
+    u += (u < 0) ? s : 0;
+    d0 = u - h;
+    d1 = (d - d0) / s;
+  } else {
+    d0 = ((d + 8) & 15) - 8;
+    d1 = (d - d0) >> 4;
+    const int sm = d0 + d1, am = sm < 0 ? -sm : sm;
+    if (am > 16 && (am & 1)) {
+      const int sg = d0 > 0 ? 1 : -1;
+      d0 -= 16 * sg;
+      d1 += sg;
+    }
   }
 }
 
+// residue -> plane bytes: entry toff[i] + d = E4M3(d0) | E4M3(d1) << 8 |
+// E4M3(d0 + d1) << 16 (the third byte unused for square moduli)
+__global__ void k_plane_tables(Oz2Const c, uint32_t* tab) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= c.tabsz) return;
+  int i = 0;
+  while (i + 1 < c.r && idx >= c.toff[i + 1] - c.m[i + 1] / 2) ++i;
+  const int m = c.m[i];
+  const int d = idx - c.toff[i];
+  int d0, d1;
+  digits(d, m, c.sq[i], d0, d1);
+  const int lo = __builtin_amdgcn_cvt_pk_fp8_f32((float)d0, (float)d1, 0, false);
+  const int hi = __builtin_amdgcn_cvt_pk_fp8_f32((float)(d0 + d1), 0.0f, 0, false);
+  tab[idx] = ((uint32_t)lo & 0xFFFFu) | (((uint32_t)hi & 0xFFu) << 16);
+}
+
+// bytes p of four table entries, packed (element j in byte j)
+__device__ __forceinline__ uint32_t gather_byte(uint32_t e0, uint32_t e1, uint32_t e2, uint32_t e3,
+                                                uint32_t sel) {
+  const uint32_t x01 = __builtin_amdgcn_perm(e1, e0, sel);
+  const uint32_t x23 = __builtin_amdgcn_perm(e3, e2, sel);
+  return __builtin_amdgcn_perm(x23, x01, 0x05040100u);
+}
+
+// Quantise (Eq. (scale)) and split into E4M3 digit planes.  A persistent-style
+// grid walks the 64x64 tiles; each workgroup first copies the residue->bytes
+// tables (sum of the moduli entries, <= 42 KiB) into LDS.
 template <bool TRANS>
 __global__ void __launch_bounds__(256) k_split(Oz2Const c, const double* __restrict__ X, int ld,
-                                               int rows, int rows_pad, int nrb, int k, int kp,
-                                               const int32_t* __restrict__ scale,
-                                               uint32_t* flags, uint8_t* __restrict__ planes,
-                                               unsigned quant_tz) {
-  int row, l0;
-  seg_coords<TRANS>(nrb, row, l0);
-  bool inrow = row < rows;
-  uint32_t f = inrow ? flags[row] : 0u;
-  int s = inrow ? scale[row] : 0;
-  double x[16];
-  load_seg<TRANS>(X, ld, rows, k, row, l0, (f & OZ2_T1) != 0, x);
-  // quantise, Eq. (scale): exact (|a| <= 2^62 with at most 53 significant bits)
-  double ah[16], al[16];
-  bool t2 = false;
-#pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    double y = ldexp(x[j], s);
-    double a = quant_tz ? trunc(y) : rint(y);
-    t2 |= (x[j] != 0.0) && (a == 0.0);
-    double h = floor(a * 0x1p-32);
-    ah[j] = h;
-    al[j] = fma(-h, 0x1p32, a);
-  }
-  if (t2) atomicOr(flags + row, OZ2_T2);
+                                               int rows, int rows_pad, int nrb, int ntiles, int k,
+                                               int kp, const int32_t* __restrict__ scale,
+                                               uint32_t* flags, const uint32_t* __restrict__ gtab,
+                                               uint8_t* __restrict__ planes, unsigned quant_tz) {
+  extern __shared__ uint32_t tab[];
+  for (int i = threadIdx.x; i < c.tabsz; i += blockDim.x) tab[i] = gtab[i];
+  __syncthreads();
   const size_t pstride = (size_t)rows_pad * kp;
-  uint8_t* base = planes + kblocked(row, l0, rows_pad);
-  for (int i = 0; i < c.r; ++i) {
-    const int m = c.m[i], c32 = c.c32[i], s_ = c.sq[i];
-    const double dinv = c.dinv[i];
-    float p0[16], p1[16], p2[16];
+  for (int tl = blockIdx.x; tl < ntiles; tl += gridDim.x) {
+    int row, l0;
+    seg_coords(tl, nrb, row, l0);
+    const bool inrow = row < rows;
+    const uint32_t f = inrow ? flags[row] : 0u;
+    const int sc = inrow ? scale[row] : 0;
+    double x[16];
+    load_seg<TRANS>(X, ld, rows, k, row, l0, (f & OZ2_T1) != 0, x);
+    // quantise: exact (|a| <= 2^62 with at most 53 significant bits)
+    double ah[16], al[16];
+    bool t2 = false;
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
-      int dres = centred_residue(ah[j], al[j], m, c32, dinv);
-      int d0, d1;
-      if (s_) split_square(dres, s_, m, c.finv_s[i], d0, d1);
-      else split_tail(dres, d0, d1);
-      p0[j] = (float)d0;
-      p1[j] = (float)d1;
-      p2[j] = (float)(d0 + d1);
+      const double y = ldexp(x[j], sc);
+      const double a = quant_tz ? trunc(y) : rint(y);
+      t2 |= (x[j] != 0.0) && (a == 0.0);
+      const double h = floor(a * 0x1p-32);
+      ah[j] = h;
+      al[j] = fma(-h, 0x1p32, a);
     }
-    uint8_t* dst = base + (size_t)c.pbase[i] * pstride;
-    uint4 v0, v1;
-    v0.x = pack4_fp8(p0[0], p0[1], p0[2], p0[3]);
-    v0.y = pack4_fp8(p0[4], p0[5], p0[6], p0[7]);
-    v0.z = pack4_fp8(p0[8], p0[9], p0[10], p0[11]);
-    v0.w = pack4_fp8(p0[12], p0[13], p0[14], p0[15]);
-    v1.x = pack4_fp8(p1[0], p1[1], p1[2], p1[3]);
-    v1.y = pack4_fp8(p1[4], p1[5], p1[6], p1[7]);
-    v1.z = pack4_fp8(p1[8], p1[9], p1[10], p1[11]);
-    v1.w = pack4_fp8(p1[12], p1[13], p1[14], p1[15]);
-    *reinterpret_cast<uint4*>(dst) = v0;
-    *reinterpret_cast<uint4*>(dst + pstride) = v1;
-    if (!s_) {
-      uint4 v2;
-      v2.x = pack4_fp8(p2[0], p2[1], p2[2], p2[3]);
-      v2.y = pack4_fp8(p2[4], p2[5], p2[6], p2[7]);
-      v2.z = pack4_fp8(p2[8], p2[9], p2[10], p2[11]);
-      v2.w = pack4_fp8(p2[12], p2[13], p2[14], p2[15]);
-      *reinterpret_cast<uint4*>(dst + 2 * pstride) = v2;
+    if (t2) atomicOr(flags + row, OZ2_T2);
+    uint8_t* base = planes + kblocked(row, l0, rows_pad);
+    for (int i = 0; i < c.r; ++i) {
+      const double m = (double)c.m[i], c32 = (double)c.c32[i], dinv = c.dinv[i];
+      const int to = c.toff[i];
+      uint32_t e[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) e[j] = tab[to + centred_residue(ah[j], al[j], m, c32, dinv)];
+      uint8_t* dst = base + (size_t)c.pbase[i] * pstride;
+      uint4 v0, v1;
+      v0.x = gather_byte(e[0], e[1], e[2], e[3], 0x05010400u);
+      v0.y = gather_byte(e[4], e[5], e[6], e[7], 0x05010400u);
+      v0.z = gather_byte(e[8], e[9], e[10], e[11], 0x05010400u);
+      v0.w = gather_byte(e[12], e[13], e[14], e[15], 0x05010400u);
+      v1.x = gather_byte(e[0], e[1], e[2], e[3], 0x05010501u);
+      v1.y = gather_byte(e[4], e[5], e[6], e[7], 0x05010501u);
+      v1.z = gather_byte(e[8], e[9], e[10], e[11], 0x05010501u);
+      v1.w = gather_byte(e[12], e[13], e[14], e[15], 0x05010501u);
+      *reinterpret_cast<uint4*>(dst) = v0;
+      *reinterpret_cast<uint4*>(dst + pstride) = v1;
+      if (!c.sq[i]) {
+        uint4 v2;
+        v2.x = gather_byte(e[0], e[1], e[2], e[3], 0x05010602u);
+        v2.y = gather_byte(e[4], e[5], e[6], e[7], 0x05010602u);
+        v2.z = gather_byte(e[8], e[9], e[10], e[11], 0x05010602u);
+        v2.w = gather_byte(e[12], e[13], e[14], e[15], 0x05010602u);
+        *reinterpret_cast<uint4*>(dst + 2 * pstride) = v2;
+      }
     }
   }
 }
@@ -355,16 +372,25 @@ hipError_t oz2_launch_scales(const Oz2Dims& d, const Oz2Layout& L, const Oz2Cons
   return hipGetLastError();
 }
 
+hipError_t oz2_launch_tables(const Oz2Layout& L, const Oz2Const& c, uint8_t* ws, hipStream_t s) {
+  hipLaunchKernelGGL(k_plane_tables, dim3((c.tabsz + 255) / 256), dim3(256), 0, s, c,
+                     (uint32_t*)(ws + L.tabs));
+  return hipGetLastError();
+}
+
 hipError_t oz2_launch_split(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
                             const double* A, int lda, const double* B, int ldb, hipStream_t s) {
   unsigned tz = (d.flags & 4u) ? 1u : 0u;   // OZ2_QUANT_TZ
-  dim3 ga((d.mp / 64) * (d.kp / 64));
-  hipLaunchKernelGGL(k_split<true>, ga, dim3(256), 0, s, c, A, lda, d.m, d.mp, d.mp / 64, d.k,
-                     d.kp, (const int32_t*)(ws + L.sA), (uint32_t*)(ws + L.flagsA),
-                     ws + L.planesA, tz);
-  dim3 gb((d.np / 64) * (d.kp / 64));
-  hipLaunchKernelGGL(k_split<false>, gb, dim3(256), 0, s, c, B, ldb, d.n, d.np, d.np / 64, d.k,
-                     d.kp, (const int32_t*)(ws + L.tB), (uint32_t*)(ws + L.flagsB),
-                     ws + L.planesB, tz);
+  const size_t lds = (size_t)c.tabsz * 4;
+  const int tA = (d.mp / 64) * (d.kp / 64), tB = (d.np / 64) * (d.kp / 64);
+  // persistent-style: as many workgroups as the LDS tables let stay resident
+  const int per_cu = (int)(163840 / lds) < 8 ? (int)(163840 / lds) : 8;
+  const int cap = 256 * (per_cu > 0 ? per_cu : 1);
+  hipLaunchKernelGGL(k_split<true>, dim3(tA < cap ? tA : cap), dim3(256), lds, s, c, A, lda, d.m,
+                     d.mp, d.mp / 64, tA, d.k, d.kp, (const int32_t*)(ws + L.sA),
+                     (uint32_t*)(ws + L.flagsA), (const uint32_t*)(ws + L.tabs), ws + L.planesA, tz);
+  hipLaunchKernelGGL(k_split<false>, dim3(tB < cap ? tB : cap), dim3(256), lds, s, c, B, ldb, d.n,
+                     d.np, d.np / 64, tB, d.k, d.kp, (const int32_t*)(ws + L.tB),
+                     (uint32_t*)(ws + L.flagsB), (const uint32_t*)(ws + L.tabs), ws + L.planesB, tz);
   return hipGetLastError();
 }

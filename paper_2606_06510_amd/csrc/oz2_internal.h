@@ -37,6 +37,9 @@ struct Oz2Const {
   double Ml[OZ2_NLIMB];           // 32-bit words of M
   double Mhalf[OZ2_NLIMB];        // 32-bit words of floor(M/2)
   int cA, cB;                     // width budgets of the scaling rule
+  // residue -> plane-bytes tables: entry toff[i] + d for the centred residue d
+  int toff[OZ2_MAXR];             // (sum of the earlier moduli) + floor(m_i/2)
+  int tabsz;                      // sum of the moduli (entries)
 };
 
 struct Oz2Dims {
@@ -54,6 +57,7 @@ struct Oz2Layout {
   size_t sA, tB;              // int32 [mp] / [np]
   size_t codesA, codesB;      // uint8 [kp/64][mp][64] / [kp/64][np][64] (K-blocked)
   size_t planesA, planesB;    // uint8 [P][kp/64][mp][64] / [P][kp/64][np][64] (K-blocked)
+  size_t tabs;                // uint32 [tabsz]: E4M3 plane bytes of every centred residue
   size_t res;                 // int16 [r][tile][wave 8][x 4][y 2][lane 64][16]
                               //   (the GEMM's accumulator order, see gemm.hip)
   size_t counters;            // int32 [4]: fallback row / column counts
@@ -71,6 +75,7 @@ hipError_t oz2_launch_codes(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
 hipError_t oz2_launch_codegemm(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, hipStream_t s);
 hipError_t oz2_launch_scales(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
                              uint8_t* ws, hipStream_t s);
+hipError_t oz2_launch_tables(const Oz2Layout& L, const Oz2Const& c, uint8_t* ws, hipStream_t s);
 hipError_t oz2_launch_split(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
                             const double* A, int lda, const double* B, int ldb, hipStream_t s);
 hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
