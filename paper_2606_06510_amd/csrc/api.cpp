@@ -127,6 +127,13 @@ bool make_const(int r, Oz2Const& c) {
     c.Ml[j] = (double)M.word(j);
     c.Mhalf[j] = (double)Mh.word(j);
   }
+  // the reconstruction kernels are specialised on r with nw = 3 (r <= 10),
+  // 4 (r <= 13), 5 words: [-M/2, M/2) must fit nw words of two's complement
+  c.nw = r <= 10 ? 3 : (r <= 13 ? 4 : 5);
+  if (M.bitlen() + 1 > 32 * c.nw) return false;
+  double Md = 0.0;
+  for (int j = OZ2_NLIMB - 1; j >= 0; --j) Md = Md * 4294967296.0 + (double)M.word(j);
+  c.mtop = std::ldexp(1.0, 32 * (c.nw - 1)) / Md;
   const int cc = (M.bitlen() - 1) + 6;     // floor(log2 M) + 6
   c.cA = cc / 2;
   c.cB = cc - c.cA;

@@ -114,6 +114,25 @@ __device__ __forceinline__ void load_seg(const double* __restrict__ X, int ld, i
   }
 }
 
+// As load_seg; a full 16-element segment of a contiguous column (B side) is
+// read with 16-byte loads when the caller has checked X and ld for alignment.
+template <bool TRANS>
+__device__ __forceinline__ void load_seg_fast(const double* __restrict__ X, int ld, int rows, int k,
+                                              int row, int l0, bool zero, bool vec,
+                                              double (&x)[16]) {
+  if (!TRANS && vec && !zero && row < rows && l0 + 16 <= k) {
+    const double2* p = reinterpret_cast<const double2*>(X + (size_t)row * ld + l0);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const double2 v = p[j];
+      x[2 * j] = v.x;
+      x[2 * j + 1] = v.y;
+    }
+  } else {
+    load_seg<TRANS>(X, ld, rows, k, row, l0, zero, x);
+  }
+}
+
 template <bool TRANS>
 __global__ void k_codes(const double* __restrict__ X, int ld, int rows, int nrb, int k, int kp,
                         const unsigned long long* __restrict__ bits, uint8_t* __restrict__ codes) {
@@ -265,7 +284,8 @@ __global__ void __launch_bounds__(256) k_split(Oz2Const c, const double* __restr
                                                int rows, int rows_pad, int nrb, int ntiles, int k,
                                                int kp, const int32_t* __restrict__ scale,
                                                uint32_t* flags, const uint32_t* __restrict__ gtab,
-                                               uint8_t* __restrict__ planes, unsigned quant_tz) {
+                                               uint8_t* __restrict__ planes, unsigned quant_tz,
+                                               unsigned vec) {
   extern __shared__ uint32_t tab[];
   for (int i = threadIdx.x; i < c.tabsz; i += blockDim.x) tab[i] = gtab[i];
   __syncthreads();
@@ -277,7 +297,7 @@ __global__ void __launch_bounds__(256) k_split(Oz2Const c, const double* __restr
     const uint32_t f = inrow ? flags[row] : 0u;
     const int sc = inrow ? scale[row] : 0;
     double x[16];
-    load_seg<TRANS>(X, ld, rows, k, row, l0, (f & OZ2_T1) != 0, x);
+    load_seg_fast<TRANS>(X, ld, rows, k, row, l0, (f & OZ2_T1) != 0, vec != 0, x);
     // quantise: exact (|a| <= 2^62 with at most 53 significant bits)
     double ah[16], al[16];
     bool t2 = false;
@@ -378,19 +398,46 @@ hipError_t oz2_launch_tables(const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
   return hipGetLastError();
 }
 
+// workgroups of k_split that stay resident on the whole device for a given
+// LDS table size (cached per size: the table size depends only on r)
+template <bool TRANS>
+static int split_resident(size_t lds) {
+  static int cache_lds[OZ2_MAXR + 1] = {0}, cache_n[OZ2_MAXR + 1] = {0};
+  static int cus = 0;
+  if (!cus) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      cus = 256;
+  }
+  const int slot = (int)(lds % (OZ2_MAXR + 1));
+  if (cache_lds[slot] == (int)lds) return cache_n[slot];
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_split<TRANS>, 256, lds) !=
+          hipSuccess ||
+      per_cu <= 0)
+    per_cu = 1;
+  cache_lds[slot] = (int)lds;
+  cache_n[slot] = per_cu * cus;
+  return per_cu * cus;
+}
+
 hipError_t oz2_launch_split(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
                             const double* A, int lda, const double* B, int ldb, hipStream_t s) {
   unsigned tz = (d.flags & 4u) ? 1u : 0u;   // OZ2_QUANT_TZ
   const size_t lds = (size_t)c.tabsz * 4;
   const int tA = (d.mp / 64) * (d.kp / 64), tB = (d.np / 64) * (d.kp / 64);
-  // persistent-style: as many workgroups as the LDS tables let stay resident
-  const int per_cu = (int)(163840 / lds) < 8 ? (int)(163840 / lds) : 8;
-  const int cap = 256 * (per_cu > 0 ? per_cu : 1);
-  hipLaunchKernelGGL(k_split<true>, dim3(tA < cap ? tA : cap), dim3(256), lds, s, c, A, lda, d.m,
+  // persistent-style grids: one resident round of workgroups walks the tiles
+  const int capA = split_resident<true>(lds), capB = split_resident<false>(lds);
+  const unsigned vecB = ((uintptr_t)B % 16 == 0 && ldb % 2 == 0) ? 1u : 0u;
+  hipLaunchKernelGGL(k_split<true>, dim3(tA < capA ? tA : capA), dim3(256), lds, s, c, A, lda, d.m,
                      d.mp, d.mp / 64, tA, d.k, d.kp, (const int32_t*)(ws + L.sA),
-                     (uint32_t*)(ws + L.flagsA), (const uint32_t*)(ws + L.tabs), ws + L.planesA, tz);
-  hipLaunchKernelGGL(k_split<false>, dim3(tB < cap ? tB : cap), dim3(256), lds, s, c, B, ldb, d.n,
+                     (uint32_t*)(ws + L.flagsA), (const uint32_t*)(ws + L.tabs), ws + L.planesA, tz,
+                     0u);
+  hipLaunchKernelGGL(k_split<false>, dim3(tB < capB ? tB : capB), dim3(256), lds, s, c, B, ldb, d.n,
                      d.np, d.np / 64, tB, d.k, d.kp, (const int32_t*)(ws + L.tB),
-                     (uint32_t*)(ws + L.flagsB), (const uint32_t*)(ws + L.tabs), ws + L.planesB, tz);
+                     (uint32_t*)(ws + L.flagsB), (const uint32_t*)(ws + L.tabs), ws + L.planesB, tz,
+                     vecB);
   return hipGetLastError();
 }

@@ -36,6 +36,8 @@ struct Oz2Const {
   double wfrac[OZ2_MAXR];         // W_i / M = inv_i / m_i rounded to fp64
   double Ml[OZ2_NLIMB];           // 32-bit words of M
   double Mhalf[OZ2_NLIMB];        // 32-bit words of floor(M/2)
+  int nw;                         // words of the two's complement integer in [-M/2, M/2)
+  double mtop;                    // 2^(32 (nw - 1)) / M, rounded
   int cA, cB;                     // width budgets of the scaling rule
   // residue -> plane-bytes tables: entry toff[i] + d for the centred residue d
   int toff[OZ2_MAXR];             // (sum of the earlier moduli) + floor(m_i/2)

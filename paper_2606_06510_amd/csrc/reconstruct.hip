@@ -21,256 +21,302 @@ namespace {
 
 constexpr int NL = OZ2_NLIMB;
 
-// Residues of a thread's 16 outputs, as the residue buffer holds them: per
-// modulus one uint4 pair = 16 int16 (output e in half e%2 of word e/2).
-struct Res16 {
-  uint4 lo, hi;
+// 32-bit words of the two's complement integer in [-M/2, M/2) for r moduli
+// (log2 M = 76.0, 85.0, 94.0, 102.9, 111.8, 120.8, 129.7, 138.5, 147.4 for
+// r = 8..16; the host checks the same rule).
+template <int R>
+struct NWords {
+  static constexpr int value = R <= 10 ? 3 : (R <= 13 ? 4 : 5);
 };
 
-template <int E>
-__device__ __forceinline__ int unpack(const Res16& v) {
-  constexpr int wi = E >> 1;
-  const uint32_t wd = wi == 0 ? v.lo.x : wi == 1 ? v.lo.y : wi == 2 ? v.lo.z : wi == 3 ? v.lo.w
-                    : wi == 4 ? v.hi.x : wi == 5 ? v.hi.y : wi == 6 ? v.hi.z : v.hi.w;
-  return (E & 1) ? (int)(int16_t)(wd >> 16) : (int)(int16_t)(wd & 0xFFFFu);
+// Residue I of the 8 a thread holds for one modulus (int16 I of the uint4).
+template <int I>
+__device__ __forceinline__ double res_at(const uint4& v) {
+  constexpr int wi = I >> 1;
+  const uint32_t wd = wi == 0 ? v.x : wi == 1 ? v.y : wi == 2 ? v.z : v.w;
+  return (double)((I & 1) ? ((int32_t)wd >> 16) : (int32_t)(int16_t)(wd & 0xFFFFu));
 }
 
-// Exact integer of output E of the 16 from its r centred residues: 5 words,
-// two's complement, little endian.
-template <int R, int E>
-__device__ __forceinline__ void crt_words(const Oz2Const& c, const Res16 (&x)[OZ2_MAXR],
-                                          uint32_t (&w)[NL]) {
-  double S[NL];
+// limbs j < NW-1 into [0, 2^32) with carries upward (every step exact:
+// integers below 2^48)
+template <int NW>
+__device__ __forceinline__ void normalise(double (&S)[NW]) {
 #pragma unroll
-  for (int j = 0; j < NL; ++j) S[j] = 0.0;
-  double f = 0.0;
-#pragma unroll
-  for (int i = 0; i < R; ++i) {
-    const double xi = (double)unpack<E>(x[i]);
-#pragma unroll
-    for (int j = 0; j < NL; ++j) S[j] = fma(xi, c.W[i][j], S[j]);
-    f = fma(xi, c.wfrac[i], f);
-  }
-  const double q = rint(f);
-#pragma unroll
-  for (int j = 0; j < NL; ++j) S[j] = fma(-q, c.Ml[j], S[j]);
-  // normalise: limbs 0..NL-2 into [0, 2^32), carries upward (all exact)
-#pragma unroll
-  for (int j = 0; j < NL - 1; ++j) {
-    double cy = floor(S[j] * 0x1p-32);
+  for (int j = 0; j < NW - 1; ++j) {
+    const double cy = floor(S[j] * 0x1p-32);
     S[j] = fma(-cy, 0x1p32, S[j]);
     S[j + 1] += cy;
   }
-  // the fp64 estimate of X/M is ambiguous only within 2^-35 of +-1/2
-  double d = f - q;
-  if (fabs(d) > 0.49999) {
+}
+
+// Exact integer of output I of a thread from its R centred residues:
+// NW words, two's complement, little endian.
+template <int R, int NW, int I>
+__device__ __forceinline__ void crt_words(const Oz2Const& c, const uint4 (&x)[R],
+                                          uint32_t (&w)[NW]) {
+  double S[NW];
+#pragma unroll
+  for (int j = 0; j < NW; ++j) S[j] = 0.0;
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const double xi = res_at<I>(x[i]);
+#pragma unroll
+    for (int j = 0; j < NW; ++j) S[j] = fma(xi, c.W[i][j], S[j]);
+  }
+  // quotient estimate q = rint(X / M) from the three top (unnormalised)
+  // limbs: |S_j| < 2^45, |X/M| <= sum |x_i| < 2^13, so the estimate of X/M
+  // is within 2^-36 of the true value; only within that of +-1/2 can q be
+  // off by one, and an exact range check below settles those.
+  double f = fma(S[NW - 2], 0x1p-32, S[NW - 1]);
+  f = fma(S[NW - 3], 0x1p-64, f);
+  f *= c.mtop;
+  const double q = rint(f);
+#pragma unroll
+  for (int j = 0; j < NW; ++j) S[j] = fma(-q, c.Ml[j], S[j]);
+  normalise<NW>(S);
+  if (fabs(f - q) > 0.49999) {
     // exact range check, X in [-floor(M/2), ceil(M/2) - 1]:
     //   P = X - M + floor(M/2) >= 0  <=>  X >= ceil(M/2)   -> X -= M
     //   N = X + floor(M/2) < 0       <=>  X < -floor(M/2)  -> X += M
     // (the sign of a normalised limb vector is the sign of its top limb)
-    double P[NL], N[NL];
+    double P[NW], N[NW];
 #pragma unroll
-    for (int j = 0; j < NL; ++j) { P[j] = S[j] - c.Ml[j] + c.Mhalf[j]; N[j] = S[j] + c.Mhalf[j]; }
-#pragma unroll
-    for (int j = 0; j < NL - 1; ++j) {
-      double cp = floor(P[j] * 0x1p-32); P[j] = fma(-cp, 0x1p32, P[j]); P[j + 1] += cp;
-      double cn = floor(N[j] * 0x1p-32); N[j] = fma(-cn, 0x1p32, N[j]); N[j + 1] += cn;
+    for (int j = 0; j < NW; ++j) {
+      P[j] = S[j] - c.Ml[j] + c.Mhalf[j];
+      N[j] = S[j] + c.Mhalf[j];
     }
-    if (P[NL - 1] >= 0.0) {
+    normalise<NW>(P);
+    normalise<NW>(N);
+    const double adj = (P[NW - 1] >= 0.0) ? -1.0 : ((N[NW - 1] < 0.0) ? 1.0 : 0.0);
 #pragma unroll
-      for (int j = 0; j < NL; ++j) S[j] -= c.Ml[j];
-    } else if (N[NL - 1] < 0.0) {
-#pragma unroll
-      for (int j = 0; j < NL; ++j) S[j] += c.Ml[j];
-    }
-#pragma unroll
-    for (int j = 0; j < NL - 1; ++j) {
-      double cy = floor(S[j] * 0x1p-32);
-      S[j] = fma(-cy, 0x1p32, S[j]);
-      S[j + 1] += cy;
-    }
+    for (int j = 0; j < NW; ++j) S[j] = fma(adj, c.Ml[j], S[j]);
+    normalise<NW>(S);
   }
 #pragma unroll
-  for (int j = 0; j < NL - 1; ++j) w[j] = (uint32_t)S[j];
-  w[NL - 1] = (uint32_t)(int32_t)S[NL - 1];
+  for (int j = 0; j < NW - 1; ++j) w[j] = (uint32_t)S[j];
+  w[NW - 1] = (uint32_t)(int32_t)S[NW - 1];
 }
 
-__device__ __forceinline__ uint32_t word_at(const uint32_t (&w)[NL], int i) {
+template <int NW>
+__device__ __forceinline__ uint32_t word_at(const uint32_t (&w)[NW], int i) {
   uint32_t r = 0;
 #pragma unroll
-  for (int j = 0; j < NL; ++j) r = (i == j) ? w[j] : r;
+  for (int j = 0; j < NW; ++j) r = (i == j) ? w[j] : r;
   return r;
 }
 
-// RN-even binary64 value of X * 2^-e for the 160-bit two's-complement X.
-__device__ __forceinline__ double round_scaled(uint32_t (&w)[NL], int e) {
-  const bool neg = (int32_t)w[NL - 1] < 0;
-  if (neg) {                      // magnitude: two's complement negate
-    uint32_t carry = 1;
+// RN-even value of |X| 2^-e for a nonzero magnitude whose result is
+// subnormal or zero (the rare path): explicit round and sticky bits at the
+// reduced precision of the subnormal range.
+template <int NW>
+__device__ __forceinline__ double round_subnormal(const uint32_t (&w)[NW], int tb, int e) {
+  const int E = tb - 1 - e;
+  const int p = 53 - (-1022 - E);   // bits kept, < 53
+  if (p < 0) return 0.0;            // below half the smallest subnormal
+  const int sh = tb - p;            // bits below position sh are rounded off (sh > 0)
+  const int wi = sh >> 5, bo = sh & 31;
+  const unsigned long long lo = ((unsigned long long)word_at(w, wi + 1) << 32) | word_at(w, wi);
+  const unsigned long long top = word_at(w, wi + 2);
+  unsigned long long mant = (lo >> bo) | (bo ? (top << (64 - bo)) : 0ull);
+  const int rb = sh - 1;
+  const int rwi = rb >> 5, rbo = rb & 31;
+  const uint32_t rw = word_at(w, rwi);
+  const bool round = (rw >> rbo) & 1u;
+  bool sticky = (rw & ((1u << rbo) - 1u)) != 0u;
 #pragma unroll
-    for (int j = 0; j < NL; ++j) {
-      uint32_t v = ~w[j] + carry;
-      carry = (carry && v == 0) ? 1u : 0u;
-      w[j] = v;
-    }
-  }
-  int h = -1;
-#pragma unroll
-  for (int j = 0; j < NL; ++j) h = w[j] ? j : h;
-  if (h < 0) return 0.0;         // exact zero is +0.0
-  const int tb = 32 * h + (32 - __clz((int)word_at(w, h)));   // X in [2^(tb-1), 2^tb)
-  const int E = tb - 1 - e;                                   // unbiased exponent of the result
-  int p = 53;
-  if (E < -1022) p = 53 - (-1022 - E);                        // subnormal precision
-  double r;
-  if (p < 0) {
-    r = 0.0;                       // below half the smallest subnormal
-  } else {
-    const int sh = tb - p;         // bits below position sh are rounded off
-    unsigned long long mant;
-    if (sh <= 0) {
-      mant = ((unsigned long long)w[1] << 32) | w[0];   // X < 2^53: exact
-      r = ldexp((double)mant, -e);
-    } else {
-      const int wi = sh >> 5, bo = sh & 31;
-      unsigned long long lo = ((unsigned long long)word_at(w, wi + 1) << 32) | word_at(w, wi);
-      unsigned long long top = word_at(w, wi + 2);
-      mant = (lo >> bo) | (bo ? (top << (64 - bo)) : 0ull);
-      // round bit = bit sh-1; sticky = bits below sh-1
-      const int rb = sh - 1;
-      const int rwi = rb >> 5, rbo = rb & 31;
-      const uint32_t rw = word_at(w, rwi);
-      const bool round = (rw >> rbo) & 1u;
-      bool sticky = (rw & ((1u << rbo) - 1u)) != 0u;
-#pragma unroll
-      for (int j = 0; j < NL; ++j) sticky |= (j < rwi) && (w[j] != 0u);
-      if (round && (sticky || (mant & 1ull))) mant += 1ull;
-      r = ldexp((double)mant, sh - e);
-    }
-  }
-  return neg ? -r : r;
+  for (int j = 0; j < NW; ++j) sticky |= (j < rwi) && (w[j] != 0u);
+  if (round && (sticky || (mant & 1ull))) mant += 1ull;
+  return ldexp((double)mant, sh - e);
 }
 
-// Thread per (tile, wave, 32x32 block, lane): 16 outputs of column col,
-// rows row + 8(e/4) + (e%4), e = 0..15 -- the residue GEMM's accumulator order
-// (wave w owns rows (w>>2)*128 + 32x, columns (w&3)*64 + 32y of the tile).
-__device__ __forceinline__ void out_coords(int mp, size_t gid, int& row, int& col, size_t& roff) {
+// RN-even binary64 value of X 2^-e for the NW-word two's complement X.
+// The top 64 bits of |X| (leading bit at bit 63) with a sticky bit OR-ed
+// into bit 0 round to the same 53-bit value as |X| itself (64 > 53 + 2), and
+// one fma of the two 32-bit halves performs that rounding; the power-of-two
+// scaling is exact (or overflows to infinity, the correctly rounded result)
+// unless the result is subnormal, which takes the explicit path.
+template <int NW>
+__device__ __forceinline__ double round_scaled(const uint32_t (&x)[NW], int e) {
+  const uint32_t sm = (uint32_t)((int32_t)x[NW - 1] >> 31);   // all ones if X < 0
+  uint32_t w[NW];
+  uint32_t cy = sm & 1u;
+#pragma unroll
+  for (int j = 0; j < NW; ++j) {   // |X| = (X ^ sm) + (sm & 1)
+    const uint32_t v = (x[j] ^ sm) + cy;
+    cy = (v < cy) ? 1u : 0u;
+    w[j] = v;
+  }
+  uint32_t P[NW];                  // prefix ORs for the sticky bit
+  P[0] = w[0];
+#pragma unroll
+  for (int j = 1; j < NW; ++j) P[j] = P[j - 1] | w[j];
+  // a, b, c: the top nonzero word and the two below it; st: OR of the rest
+  uint32_t a = w[NW - 1], b = w[NW - 2], c = w[NW - 3];
+  uint32_t st = NW >= 4 ? P[NW >= 4 ? NW - 4 : 0] : 0u;
+  int top = NW - 1;
+#pragma unroll
+  for (int s = 0; s < NW - 1; ++s) {
+    const bool z = (a == 0u);
+    const int ni = NW - 4 - s;     // word that enters below c on a shift
+    const uint32_t nxt = ni >= 0 ? w[ni >= 0 ? ni : 0] : 0u;
+    const uint32_t nst = ni >= 1 ? P[ni >= 1 ? ni - 1 : 0] : 0u;
+    a = z ? b : a;
+    b = z ? c : b;
+    c = z ? nxt : c;
+    st = z ? nst : st;
+    top -= z ? 1 : 0;
+  }
+  if (a == 0u) return 0.0;         // exact zero is +0.0
+  const int lz = __clz((int)a);
+  const int tb = 32 * top + 32 - lz;                  // |X| in [2^(tb-1), 2^tb)
+  double v;
+  if (tb - 1 - e < -1022) {
+    v = round_subnormal<NW>(w, tb, e);
+  } else {
+    const uint32_t hi = lz ? __builtin_amdgcn_alignbit(a, b, 32 - lz) : a;
+    const uint32_t lo = lz ? __builtin_amdgcn_alignbit(b, c, 32 - lz) : b;
+    const uint32_t stk = ((st | (c << lz)) != 0u) ? 1u : 0u;
+    v = ldexp(fma((double)hi, 0x1p32, (double)(lo | stk)), tb - 64 - e);
+  }
+  return sm ? -v : v;
+}
+
+// Thread mapping shared by the reconstruction kernels.  The residue GEMM
+// leaves, per modulus, each 32x32 output block (wave w of a 256x256 tile,
+// sub-block x, y) as 1024 int16 in its accumulator order: lane L holds 16
+// outputs of column L%32, rows 4(L/32) + 8(e/4) + e%4, e = 0..15.  Here two
+// threads share a lane's 16 (t = 2L + h takes e = 8h..8h+7), so the 128
+// threads of a block read 2 KiB contiguous per modulus; a workgroup of 256
+// takes two blocks.
+struct BlockMap {
+  size_t roff;      // int16 offset of the thread's 8 residues in a modulus plane
+  int row0, col0;   // block origin in C
+  int cl;           // column within the block
+  int rb;           // row within the block of output i: rb + 8(i/4) + i%4
+  int hb, tt;       // block of the pair, thread within the block
+};
+
+__device__ __forceinline__ BlockMap block_map(int mp) {
+  BlockMap b;
+  const int t = threadIdx.x;
+  b.hb = t >> 7;
+  b.tt = t & 127;
+  const size_t G = (size_t)blockIdx.x * 2 + b.hb;
+  const size_t tile = G >> 6;
+  const int blk = (int)(G & 63);
   const int ntm = mp / OZ2_TILE;
-  const size_t tile = gid >> 12;                  // 4096 threads per 256x256 tile
-  const int q = (int)(gid & 4095);
-  const int lane = q & 63, blk = q >> 6;          // blk = (w*4 + x)*2 + y
-  const int y = blk & 1, x = (blk >> 1) & 3, w = blk >> 3;
   const int tm = (int)(tile % ntm), tn = (int)(tile / ntm);
-  row = tm * OZ2_TILE + (w >> 2) * 128 + x * 32 + 4 * (lane >> 5);
-  col = tn * OZ2_TILE + (w & 3) * 64 + y * 32 + (lane & 31);
-  roff = tile * (OZ2_TILE * OZ2_TILE) + (size_t)q * 16;
+  const int y = blk & 1, x = (blk >> 1) & 3, w = blk >> 3;
+  b.row0 = tm * OZ2_TILE + (w >> 2) * 128 + x * 32;
+  b.col0 = tn * OZ2_TILE + (w & 3) * 64 + y * 32;
+  const int lane = b.tt >> 1, h = b.tt & 1;
+  b.cl = lane & 31;
+  b.rb = 4 * (lane >> 5) + 16 * h;
+  b.roff = tile * (OZ2_TILE * OZ2_TILE) + (size_t)blk * 1024 + (size_t)b.tt * 8;
+  return b;
 }
 
 template <int R>
 __device__ __forceinline__ void load_residues(const int16_t* __restrict__ res, size_t plane,
-                                              size_t roff, Res16 (&x)[OZ2_MAXR]) {
+                                              size_t roff, uint4 (&x)[R]) {
 #pragma unroll
-  for (int i = 0; i < OZ2_MAXR; ++i) {
-    if (i < R) {
-      const uint4* p = reinterpret_cast<const uint4*>(res + (size_t)i * plane + roff);
-      x[i].lo = p[0];
-      x[i].hi = p[1];
-    } else {
-      x[i].lo = x[i].hi = make_uint4(0u, 0u, 0u, 0u);
-    }
-  }
+  for (int i = 0; i < R; ++i)
+    x[i] = *reinterpret_cast<const uint4*>(res + (size_t)i * plane + roff);
 }
 
-// one output of the 16 held by a thread: reconstruct, rescale, store
-template <int R, int E>
-__device__ __forceinline__ void finish_one(const Oz2Const& c, const Oz2Dims& d,
-                                           const Res16 (&x)[OZ2_MAXR], int row, int tj,
-                                           const int32_t* __restrict__ sA,
-                                           const uint32_t* __restrict__ fA, bool acc, bool nofb,
-                                           double* out) {
-  const int i = row + 8 * (E >> 2) + (E & 3);
-  if (i >= d.m) return;
-  if (!nofb && (fA[i] & (OZ2_T1 | OZ2_T2))) return;
-  uint32_t w[NL];
-  crt_words<R, E>(c, x, w);
-  const double v = round_scaled(w, sA[i] + tj);
-  out[i] = acc ? out[i] + v : v;
-}
-
-template <int R, int E>
-struct Finish {
+template <int R, int I>
+struct Outputs {
   __device__ __forceinline__ static void run(const Oz2Const& c, const Oz2Dims& d,
-                                             const Res16 (&x)[OZ2_MAXR], int row, int tj,
-                                             const int32_t* __restrict__ sA,
-                                             const uint32_t* __restrict__ fA, bool acc, bool nofb,
-                                             double* out) {
-    finish_one<R, E>(c, d, x, row, tj, sA, fA, acc, nofb, out);
-    Finish<R, E + 1>::run(c, d, x, row, tj, sA, fA, acc, nofb, out);
+                                             const uint4 (&x)[R], const BlockMap& b, int tj,
+                                             const int32_t* __restrict__ sA, double (*tr)[33]) {
+    constexpr int NW = NWords<R>::value;
+    const int rr = b.rb + 8 * (I >> 2) + (I & 3);
+    const int row = b.row0 + rr;
+    const int si = row < d.m ? sA[row] : 0;
+    uint32_t w[NW];
+    crt_words<R, NW, I>(c, x, w);
+    tr[b.cl][rr] = round_scaled<NW>(w, si + tj);
+    Outputs<R, I + 1>::run(c, d, x, b, tj, sA, tr);
   }
 };
 template <int R>
-struct Finish<R, 16> {
-  __device__ __forceinline__ static void run(const Oz2Const&, const Oz2Dims&,
-                                             const Res16 (&)[OZ2_MAXR], int, int,
-                                             const int32_t* __restrict__,
-                                             const uint32_t* __restrict__, bool, bool, double*) {}
+struct Outputs<R, 8> {
+  __device__ __forceinline__ static void run(const Oz2Const&, const Oz2Dims&, const uint4 (&)[R],
+                                             const BlockMap&, int, const int32_t* __restrict__,
+                                             double (*)[33]) {}
 };
 
+// Reconstruct, rescale and store: the block's 32x32 results go through LDS so
+// that each store instruction writes whole 256-byte column segments of C.
+// Entries of flagged rows / columns are left to the fallback kernel.
 template <int R>
 __global__ void __launch_bounds__(256)
 k_reconstruct(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res,
               const int32_t* __restrict__ sA, const int32_t* __restrict__ tB,
               const uint32_t* __restrict__ fA, const uint32_t* __restrict__ fB, double* C, int ldc) {
-  const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  int row, col;
-  size_t roff;
-  out_coords(d.mp, gid, row, col, roff);
-  if (col >= d.n || row >= d.m) return;
+  __shared__ double tr[2][32][33];
+  const BlockMap b = block_map(d.mp);
+  {
+    uint4 x[R];
+    load_residues<R>(res, (size_t)d.mp * d.np, b.roff, x);
+    const int col = b.col0 + b.cl;
+    const int tj = col < d.n ? tB[col] : 0;
+    Outputs<R, 0>::run(c, d, x, b, tj, sA, tr[b.hb]);
+  }
+  __syncthreads();
   const bool acc = (d.flags & 1u) != 0;        // OZ2_ACCUMULATE
   const bool nofb = (d.flags & 8u) != 0;       // OZ2_NO_FALLBACK
   const bool force = (d.flags & 16u) != 0;     // OZ2_FORCE_FALLBACK
-  const uint32_t fc = fB[col];
-  if (!nofb && (force || (fc & (OZ2_T1 | OZ2_T2)))) return;
-  const int tj = tB[col];
-  Res16 x[OZ2_MAXR];
-  load_residues<R>(res, (size_t)d.mp * d.np, roff, x);
-  double* out = C + (size_t)col * ldc;
-  Finish<R, 0>::run(c, d, x, row, tj, sA, fA, acc, nofb, out);
+  const int rr = b.tt & 31;
+  const int row = b.row0 + rr;
+  if (row >= d.m) return;
+  const bool rowfb = !nofb && (force || (fA[row] & (OZ2_T1 | OZ2_T2)));
+  if (rowfb) return;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int cc = j * 4 + (b.tt >> 5);
+    const int col = b.col0 + cc;
+    if (col < d.n && (nofb || !(fB[col] & (OZ2_T1 | OZ2_T2)))) {
+      double* o = C + (size_t)col * ldc + row;
+      const double v = tr[b.hb][cc][rr];
+      *o = acc ? *o + v : v;
+    }
+  }
 }
 
-template <int R, int E>
+template <int R, int I>
 struct IntOut {
   __device__ __forceinline__ static void run(const Oz2Const& c, const Oz2Dims& d,
-                                             const Res16 (&x)[OZ2_MAXR], int row, int col,
+                                             const uint4 (&x)[R], const BlockMap& b,
                                              uint32_t* out) {
-    const int i = row + 8 * (E >> 2) + (E & 3);
-    if (i < d.m) {
-      uint32_t w[NL];
-      crt_words<R, E>(c, x, w);
-      uint32_t* o = out + ((size_t)col * d.m + i) * NL;
+    constexpr int NW = NWords<R>::value;
+    const int row = b.row0 + b.rb + 8 * (I >> 2) + (I & 3);
+    const int col = b.col0 + b.cl;
+    if (row < d.m && col < d.n) {
+      uint32_t w[NW];
+      crt_words<R, NW, I>(c, x, w);
+      uint32_t* o = out + ((size_t)col * d.m + row) * NL;
+      const uint32_t ext = (uint32_t)((int32_t)w[NW - 1] >> 31);
 #pragma unroll
-      for (int q = 0; q < NL; ++q) o[q] = w[q];
+      for (int q = 0; q < NL; ++q) o[q] = q < NW ? w[q < NW ? q : 0] : ext;
     }
-    IntOut<R, E + 1>::run(c, d, x, row, col, out);
+    IntOut<R, I + 1>::run(c, d, x, b, out);
   }
 };
 template <int R>
-struct IntOut<R, 16> {
-  __device__ __forceinline__ static void run(const Oz2Const&, const Oz2Dims&,
-                                             const Res16 (&)[OZ2_MAXR], int, int, uint32_t*) {}
+struct IntOut<R, 8> {
+  __device__ __forceinline__ static void run(const Oz2Const&, const Oz2Dims&, const uint4 (&)[R],
+                                             const BlockMap&, uint32_t*) {}
 };
 
+// the exact integers themselves, [n][m][5] words (a diagnostic query)
 template <int R>
 __global__ void __launch_bounds__(256)
 k_integers(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res, uint32_t* out) {
-  const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  int row, col;
-  size_t roff;
-  out_coords(d.mp, gid, row, col, roff);
-  if (col >= d.n || row >= d.m) return;
-  Res16 x[OZ2_MAXR];
-  load_residues<R>(res, (size_t)d.mp * d.np, roff, x);
-  IntOut<R, 0>::run(c, d, x, row, col, out);
+  const BlockMap b = block_map(d.mp);
+  uint4 x[R];
+  load_residues<R>(res, (size_t)d.mp * d.np, b.roff, x);
+  IntOut<R, 0>::run(c, d, x, b, out);
 }
 
 // Compaction of flagged rows / columns into index lists (order irrelevant:
@@ -327,11 +373,12 @@ __global__ void k_fill(double* C, int m, int n, int ldc) {
   C[i + j * ldc] = 0.0;
 }
 
+// one workgroup of 256 threads per two 32x32 output blocks
 template <int R>
 void launch_reconstruct_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
                           double* C, int ldc, hipStream_t s) {
-  const size_t threads = (size_t)d.mp * d.np / 16;
-  hipLaunchKernelGGL(k_reconstruct<R>, dim3((unsigned)(threads / 256)), dim3(256), 0, s, c, d,
+  const size_t blocks = (size_t)d.mp * d.np / 2048;
+  hipLaunchKernelGGL(k_reconstruct<R>, dim3((unsigned)blocks), dim3(256), 0, s, c, d,
                      (const int16_t*)(ws + L.res), (const int32_t*)(ws + L.sA),
                      (const int32_t*)(ws + L.tB), (const uint32_t*)(ws + L.flagsA),
                      (const uint32_t*)(ws + L.flagsB), C, ldc);
@@ -340,8 +387,8 @@ void launch_reconstruct_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& 
 template <int R>
 void launch_integers_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
                        uint32_t* out, hipStream_t s) {
-  const size_t threads = (size_t)d.mp * d.np / 16;
-  hipLaunchKernelGGL(k_integers<R>, dim3((unsigned)(threads / 256)), dim3(256), 0, s, c, d,
+  const size_t blocks = (size_t)d.mp * d.np / 2048;
+  hipLaunchKernelGGL(k_integers<R>, dim3((unsigned)blocks), dim3(256), 0, s, c, d,
                      (const int16_t*)(ws + L.res), out);
 }
 
