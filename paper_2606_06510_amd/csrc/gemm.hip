@@ -56,15 +56,11 @@ __device__ __forceinline__ void dma16(const uint8_t* sbase, uint32_t voff, uint3
                : "memory");
 }
 
-struct Ctx {
-  const uint8_t* a0;   // first row of this tile in k-block 0 of the modulus' plane 0 (A)
-  const uint8_t* b0;   // same for B
-  size_t psA, psB;     // plane strides (bytes)
-  size_t kbA, kbB;     // k-block strides (padded rows * 64)
-  int kb0, nk, T, s;   // first k-block, stages per pair, total stages, sqrt(m) or 0
-};
-
-// planes of pair q: square  (1,0) (0,1) | (0,0);  nonsquare (1,1) | (0,0) | (2,2)
+// Per-wave DMA stream: operand base pointers of the three plane products (the
+// tile's first row, k-block kbeg), the next stage's block pointers, and how
+// many stages remain in the current product.  All of it is uniform (SGPRs),
+// so a stage costs four DMA instructions and a few scalar adds.
+// planes of product q: square  (1,0) (0,1) | (0,0);  nonsquare (1,1) | (0,0) | (2,2)
 __device__ __forceinline__ int planeA(int s, int q) {
   return s ? (q == 0 ? 1 : 0) : (q == 0 ? 1 : (q == 1 ? 0 : 2));
 }
@@ -72,23 +68,52 @@ __device__ __forceinline__ int planeB(int s, int q) {
   return s ? (q == 1 ? 1 : 0) : (q == 0 ? 1 : (q == 1 ? 0 : 2));
 }
 
+struct Ctx {
+  const uint8_t* aq[3];   // A: plane of product q at k-block kbeg, tile row 0
+  const uint8_t* bq[3];   // B: same
+  size_t kbA, kbB;        // k-block strides (padded rows * 64)
+  int nk, T;              // stages per product, total stages
+};
+
+struct Dma {
+  const uint8_t* pa;
+  const uint8_t* pb;
+  int left, q;
+  uint32_t vo0, vo1;      // lane offsets of blocks w and w + 8 (VGPR)
+  uint32_t mw;            // w * 1 KiB (uniform)
+};
+
 // One stage = A tile (16 x 1 KiB blocks of 16 rows) + B tile (16 blocks);
-// wave w moves blocks w + 8j (j = 0..3); blocks 0..15 are A, 16..31 are B.
-// Lane L writes row 16 blk + L/4, physical chunk L%4 = logical chunk ^ swz.
-__device__ __forceinline__ void issue_stage(const Ctx& x, int it, uint32_t lbase) {
-  const int q = it / x.nk, ks = it - q * x.nk;
-  const int kb = x.kb0 + ks;
+// wave w moves blocks w and w + 8 of each.  Lane L writes row 16 blk + L/4,
+// physical chunk L%4 = logical chunk ^ swz.
+__device__ __forceinline__ Dma dma_init(const Ctx& x) {
+  Dma d;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int rb = lane >> 2;
   const uint32_t lo = (uint32_t)(rb * KS + 16 * ((lane & 3) ^ swz(rb)));
-  const uint8_t* ab = x.a0 + (size_t)planeA(x.s, q) * x.psA + (size_t)kb * x.kbA;
-  const uint8_t* bb = x.b0 + (size_t)planeB(x.s, q) * x.psB + (size_t)kb * x.kbB;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int blk = w + 8 * j;
-    if (blk < 16) dma16(ab + (size_t)blk * 1024, lo, lbase + blk * 1024);
-    else dma16(bb + (size_t)(blk - 16) * 1024, lo, lbase + OPB + (blk - 16) * 1024);
+  d.vo0 = lo + (uint32_t)w * 1024u;
+  d.vo1 = d.vo0 + 8u * 1024u;
+  d.mw = (uint32_t)w * 1024u;
+  d.pa = x.aq[0];
+  d.pb = x.bq[0];
+  d.left = x.nk;
+  d.q = 0;
+  return d;
+}
+
+__device__ __forceinline__ void issue_stage(const Ctx& x, Dma& d, uint32_t lbase) {
+  dma16(d.pa, d.vo0, lbase + d.mw);
+  dma16(d.pa, d.vo1, lbase + d.mw + 8u * 1024u);
+  dma16(d.pb, d.vo0, lbase + OPB + d.mw);
+  dma16(d.pb, d.vo1, lbase + OPB + d.mw + 8u * 1024u);
+  d.pa += x.kbA;
+  d.pb += x.kbB;
+  if (--d.left == 0) {
+    ++d.q;
+    d.left = x.nk;
+    d.pa = d.q == 1 ? x.aq[1] : x.aq[2];
+    d.pb = d.q == 1 ? x.bq[1] : x.bq[2];
   }
 }
 
@@ -125,8 +150,8 @@ __device__ __forceinline__ int tile_of(int b, int ntm, int ntn) {
 }
 
 // Main loop over stages [it0, it0 + n) of the stage sequence.
-__device__ __forceinline__ void run_stages(const Ctx& x, uint8_t* LB, uint32_t lds0, int it0, int n,
-                                           v16f (&acc)[4][2]) {
+__device__ __forceinline__ void run_stages(const Ctx& x, Dma& dm, uint8_t* LB, uint32_t lds0, int it0,
+                                           int n, v16f (&acc)[4][2]) {
   const int T = x.T;
   for (int it = it0; it < it0 + n; ++it) {
     // this wave's DMA share is 4 instructions per stage; stages it+1, it+2
@@ -137,7 +162,7 @@ __device__ __forceinline__ void run_stages(const Ctx& x, uint8_t* LB, uint32_t l
     bar();
     v8i fa[4], fb[2];
     frags(LB + (it & 3) * STB, fa, fb);
-    if (it + 3 < T) issue_stage(x, it + 3, lds0 + ((it + 3) & 3) * STB);
+    if (it + 3 < T) issue_stage(x, dm, lds0 + ((it + 3) & 3) * STB);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -147,10 +172,10 @@ __device__ __forceinline__ void run_stages(const Ctx& x, uint8_t* LB, uint32_t l
   }
 }
 
-__device__ __forceinline__ void prologue(const Ctx& x, uint32_t lds0) {
+__device__ __forceinline__ void prologue(const Ctx& x, Dma& dm, uint32_t lds0) {
 #pragma unroll
   for (int t = 0; t < NB - 1; ++t)
-    if (t < x.T) issue_stage(x, t, lds0 + t * STB);
+    if (t < x.T) issue_stage(x, dm, lds0 + t * STB);
 }
 
 // ------------------------------------------------------------- code GEMM
@@ -165,22 +190,20 @@ k_codegemm(const uint8_t* __restrict__ cA, const uint8_t* __restrict__ cB, int m
   const int tm = tile % ntm, tn = tile / ntm;
   const int kbeg = slab * OZ2_CSLAB, kend = min(kp, kbeg + OZ2_CSLAB);
   Ctx x;
-  x.psA = x.psB = 0;
   x.kbA = (size_t)mp * KS;
   x.kbB = (size_t)np * KS;
-  x.a0 = cA + (size_t)tm * TILE * KS;
-  x.b0 = cB + (size_t)tn * TILE * KS;
-  x.kb0 = kbeg / KS;
+  x.aq[0] = x.aq[1] = x.aq[2] = cA + (size_t)tm * TILE * KS + (size_t)(kbeg / KS) * x.kbA;
+  x.bq[0] = x.bq[1] = x.bq[2] = cB + (size_t)tn * TILE * KS + (size_t)(kbeg / KS) * x.kbB;
   x.nk = (kend - kbeg) / KS;
   x.T = x.nk;
-  x.s = 0;
+  Dma dm = dma_init(x);
   v16f acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = v16f{0.f};
-  prologue(x, lds0);
-  run_stages(x, LB, lds0, 0, x.T, acc);
+  prologue(x, dm, lds0);
+  run_stages(x, dm, LB, lds0, 0, x.T, acc);
 
   // lane holds rows 32x + 8(e/4) + 4(lane/32) + e%4 of column 32y + lane%32
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -224,16 +247,19 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
   const int m = c.m[mi], s = c.sq[mi], pb = c.pbase[mi];
   const float fm = (float)m, inv = c.finv[mi];
   Ctx x;
-  x.psA = (size_t)mp * kp;
-  x.psB = (size_t)np * kp;
+  const size_t psA = (size_t)mp * kp, psB = (size_t)np * kp;
   x.kbA = (size_t)mp * KS;
   x.kbB = (size_t)np * KS;
-  x.a0 = PA + (size_t)pb * x.psA + (size_t)tm * TILE * KS;
-  x.b0 = PB + (size_t)pb * x.psB + (size_t)tn * TILE * KS;
-  x.kb0 = kbeg / KS;
+  const uint8_t* a0 = PA + (size_t)pb * psA + (size_t)tm * TILE * KS + (size_t)(kbeg / KS) * x.kbA;
+  const uint8_t* b0 = PB + (size_t)pb * psB + (size_t)tn * TILE * KS + (size_t)(kbeg / KS) * x.kbB;
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    x.aq[q] = a0 + (size_t)planeA(s, q) * psA;
+    x.bq[q] = b0 + (size_t)planeB(s, q) * psB;
+  }
   x.nk = (kend - kbeg) / KS;
   x.T = 3 * x.nk;
-  x.s = s;
+  Dma dm = dma_init(x);
   v16f acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -257,17 +283,17 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
           acc[i][j][e] = __builtin_fmaf(-rintf(v * inv), fm, v) * rho;
         }
   };
-  prologue(x, lds0);
+  prologue(x, dm, lds0);
   if (s) {
-    run_stages(x, LB, lds0, 0, 2 * x.nk, acc);
+    run_stages(x, dm, LB, lds0, 0, 2 * x.nk, acc);
     transition((float)s);
-    run_stages(x, LB, lds0, 2 * x.nk, x.nk, acc);
+    run_stages(x, dm, LB, lds0, 2 * x.nk, x.nk, acc);
   } else {
-    run_stages(x, LB, lds0, 0, x.nk, acc);
+    run_stages(x, dm, LB, lds0, 0, x.nk, acc);
     transition((float)c.rho0[mi]);
-    run_stages(x, LB, lds0, x.nk, x.nk, acc);
+    run_stages(x, dm, LB, lds0, x.nk, x.nk, acc);
     transition((float)c.rho1[mi]);
-    run_stages(x, LB, lds0, 2 * x.nk, x.nk, acc);
+    run_stages(x, dm, LB, lds0, 2 * x.nk, x.nk, acc);
   }
   wait_vm<0>();
 
