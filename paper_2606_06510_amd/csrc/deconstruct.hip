@@ -38,34 +38,62 @@ __global__ void k_init(unsigned long long* rowbits, int mp, unsigned long long* 
   if (i < nK) Kmax[i] = 0;
 }
 
-// rows of a column-major matrix: lanes along the (contiguous) row index
-__global__ void k_scan_rows(const double* __restrict__ A, int lda, int m, int k, int kchunk,
-                            unsigned long long* rowbits) {
-  int i = blockIdx.x * blockDim.x + threadIdx.x;
+// rows of a column-major matrix: lanes along the (contiguous) row index, two
+// rows per thread (16-byte loads when the caller has checked the alignment),
+// eight loads in flight; one k-chunk per grid row, combined with atomicMax.
+__global__ void __launch_bounds__(256) k_scan_rows(const double* __restrict__ A, int lda, int m, int k,
+                                                   int kchunk, unsigned vec,
+                                                   unsigned long long* rowbits) {
+  const int i = 2 * (blockIdx.x * blockDim.x + threadIdx.x);
   if (i >= m) return;
-  int l0 = blockIdx.y * kchunk;
-  int l1 = min(k, l0 + kchunk);
-  const double* p = A + i + (size_t)l0 * lda;
-  unsigned long long mx = 0;
+  const int l0 = blockIdx.y * kchunk;
+  const int l1 = min(k, l0 + kchunk);
+  const bool pair = vec && i + 1 < m;
+  unsigned long long m0 = 0, m1 = 0;
   int l = l0;
-  for (; l + 4 <= l1; l += 4) {
-    double x0 = p[0], x1 = p[(size_t)lda], x2 = p[2 * (size_t)lda], x3 = p[3 * (size_t)lda];
-    mx = max(mx, max(max(abs_bits(x0), abs_bits(x1)), max(abs_bits(x2), abs_bits(x3))));
-    p += 4 * (size_t)lda;
+  if (pair) {
+    const double* p = A + i + (size_t)l0 * lda;
+    for (; l + 8 <= l1; l += 8) {
+      double2 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = *reinterpret_cast<const double2*>(p + (size_t)u * lda);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        m0 = max(m0, abs_bits(v[u].x));
+        m1 = max(m1, abs_bits(v[u].y));
+      }
+      p += 8 * (size_t)lda;
+    }
   }
-  for (; l < l1; ++l, p += lda) mx = max(mx, abs_bits(*p));
-  atomicMax(rowbits + i, mx);
+  for (; l < l1; ++l) {
+    const double* p = A + i + (size_t)l * lda;
+    m0 = max(m0, abs_bits(p[0]));
+    if (i + 1 < m) m1 = max(m1, abs_bits(p[1]));
+  }
+  atomicMax(rowbits + i, m0);
+  if (i + 1 < m) atomicMax(rowbits + i + 1, m1);
 }
 
-// contiguous columns: one wave per column
-__global__ void k_scan_cols(const double* __restrict__ B, int ldb, int n, int k,
-                            unsigned long long* colbits) {
+// contiguous columns: one wave per column, 16-byte loads (1 KiB per wave
+// instruction), four in flight per lane
+__global__ void __launch_bounds__(256) k_scan_cols(const double* __restrict__ B, int ldb, int n, int k,
+                                                   unsigned vec, unsigned long long* colbits) {
   int j = (int)((blockIdx.x * (size_t)blockDim.x + threadIdx.x) >> 6);
   int lane = threadIdx.x & 63;
   if (j >= n) return;
   const double* p = B + (size_t)j * ldb;
   unsigned long long mx = 0;
-  for (int l = lane; l < k; l += 64) mx = max(mx, abs_bits(p[l]));
+  int l = 0;
+  if (vec) {
+    for (; l + 512 <= k; l += 512) {
+      double2 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const double2*>(p + l + 128 * u + 2 * lane);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) mx = max(mx, max(abs_bits(v[u].x), abs_bits(v[u].y)));
+    }
+  }
+  for (l += lane; l < k; l += 64) mx = max(mx, abs_bits(p[l]));
   for (int off = 32; off; off >>= 1) mx = max(mx, (unsigned long long)__shfl_xor((long long)mx, off));
   if (lane == 0) colbits[j] = mx;
 }
@@ -133,9 +161,51 @@ __device__ __forceinline__ void load_seg_fast(const double* __restrict__ X, int 
   }
 }
 
+// Contiguous-column operand (B): a tile of 64 columns x 64 k is read with
+// coalesced 16-byte loads (32 lanes per 512-byte column segment) into LDS, and
+// each thread then takes its 16 consecutive k of column t/4 (the layout the
+// plane stores need).  The caller synchronises before the tile is reused.
+constexpr int TPITCH = 66;   // doubles per staged column: 16-byte aligned, banks spread
+
+__device__ __forceinline__ void stage_cols(const double* __restrict__ X, int ld, int rows, int k,
+                                           int row0, int l00, bool vec, double* tile) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int it = 0; it < 8; ++it) {
+    const int idx = it * 256 + t;
+    const int c = idx >> 5, kk = (idx & 31) << 1;
+    const int r = row0 + c, l = l00 + kk;
+    double2 v = make_double2(0.0, 0.0);
+    if (r < rows) {
+      const double* p = X + (size_t)r * ld + l;
+      if (vec && l + 1 < k) {
+        v = *reinterpret_cast<const double2*>(p);
+      } else {
+        if (l < k) v.x = p[0];
+        if (l + 1 < k) v.y = p[1];
+      }
+    }
+    *reinterpret_cast<double2*>(tile + c * TPITCH + kk) = v;
+  }
+}
+
+__device__ __forceinline__ void take_cols(const double* tile, bool zero, double (&x)[16]) {
+  const int t = threadIdx.x;
+  const double* p = tile + (t >> 2) * TPITCH + (t & 3) * 16;
+#pragma unroll
+  for (int j = 0; j < 16; j += 2) {
+    const double2 v = *reinterpret_cast<const double2*>(p + j);
+    x[j] = zero ? 0.0 : v.x;
+    x[j + 1] = zero ? 0.0 : v.y;
+  }
+}
+
 template <bool TRANS>
-__global__ void k_codes(const double* __restrict__ X, int ld, int rows, int nrb, int k, int kp,
-                        const unsigned long long* __restrict__ bits, uint8_t* __restrict__ codes) {
+__global__ void __launch_bounds__(256) k_codes(const double* __restrict__ X, int ld, int rows,
+                                               int nrb, int k, int kp,
+                                               const unsigned long long* __restrict__ bits,
+                                               uint8_t* __restrict__ codes, unsigned vec) {
+  __shared__ __attribute__((aligned(16))) double tile[TRANS ? 2 : 64 * TPITCH];
   const int rows_pad = nrb * 64;
   int row, l0;
   seg_coords(blockIdx.x, nrb, row, l0);
@@ -143,7 +213,14 @@ __global__ void k_codes(const double* __restrict__ X, int ld, int rows, int nrb,
   bool t1 = b >= kInfBits;
   int E = (b == 0 || t1) ? 0 : exp_of_bits(b);
   double x[16];
-  load_seg<TRANS>(X, ld, rows, k, row, l0, t1, x);
+  if (TRANS) {
+    load_seg<TRANS>(X, ld, rows, k, row, l0, t1, x);
+  } else {
+    const int bx = (int)(blockIdx.x % (unsigned)nrb), by = (int)(blockIdx.x / (unsigned)nrb);
+    stage_cols(X, ld, rows, k, bx * 64, by * 64, vec != 0, tile);
+    __syncthreads();
+    take_cols(tile, t1, x);
+  }
   uint32_t w[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q)
@@ -286,7 +363,7 @@ __global__ void __launch_bounds__(256) k_split(Oz2Const c, const double* __restr
                                                uint32_t* flags, const uint32_t* __restrict__ gtab,
                                                uint8_t* __restrict__ planes, unsigned quant_tz,
                                                unsigned vec) {
-  extern __shared__ uint32_t tab[];
+  extern __shared__ __attribute__((aligned(16))) uint32_t tab[];
   for (int i = threadIdx.x; i < c.tabsz; i += blockDim.x) tab[i] = gtab[i];
   __syncthreads();
   const size_t pstride = (size_t)rows_pad * kp;
@@ -358,13 +435,18 @@ hipError_t oz2_launch_init(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, hi
 
 hipError_t oz2_launch_scan(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, const double* A,
                            int lda, const double* B, int ldb, hipStream_t s) {
-  int kchunk = 256;
-  while ((d.k + kchunk - 1) / kchunk > 16384) kchunk *= 2;   // keep grid.y small
-  dim3 ga((d.m + 255) / 256, (d.k + kchunk - 1) / kchunk);
-  hipLaunchKernelGGL(k_scan_rows, ga, dim3(256), 0, s, A, lda, d.m, d.k, kchunk,
+  // rows: 512 per workgroup; k chunks sized for >= ~2048 workgroups when k allows
+  const int gx = (d.m + 511) / 512;
+  int kchunk = 32;
+  while ((long long)gx * ((d.k + kchunk - 1) / kchunk) > 4096 && kchunk < 4096) kchunk *= 2;
+  while ((d.k + kchunk - 1) / kchunk > 65535) kchunk *= 2;
+  const unsigned vecA = ((uintptr_t)A % 16 == 0 && lda % 2 == 0) ? 1u : 0u;
+  dim3 ga(gx, (d.k + kchunk - 1) / kchunk);
+  hipLaunchKernelGGL(k_scan_rows, ga, dim3(256), 0, s, A, lda, d.m, d.k, kchunk, vecA,
                      (unsigned long long*)(ws + L.rowbits));
   dim3 gb((d.n + 3) / 4);
-  hipLaunchKernelGGL(k_scan_cols, gb, dim3(256), 0, s, B, ldb, d.n, d.k,
+  const unsigned vecB = ((uintptr_t)B % 16 == 0 && ldb % 2 == 0) ? 1u : 0u;
+  hipLaunchKernelGGL(k_scan_cols, gb, dim3(256), 0, s, B, ldb, d.n, d.k, vecB,
                      (unsigned long long*)(ws + L.colbits));
   return hipGetLastError();
 }
@@ -373,10 +455,11 @@ hipError_t oz2_launch_codes(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, c
                             int lda, const double* B, int ldb, hipStream_t s) {
   dim3 ga((d.mp / 64) * (d.kp / 64));
   hipLaunchKernelGGL(k_codes<true>, ga, dim3(256), 0, s, A, lda, d.m, d.mp / 64, d.k, d.kp,
-                     (const unsigned long long*)(ws + L.rowbits), ws + L.codesA);
+                     (const unsigned long long*)(ws + L.rowbits), ws + L.codesA, 0u);
   dim3 gb((d.np / 64) * (d.kp / 64));
+  const unsigned vecB = ((uintptr_t)B % 16 == 0 && ldb % 2 == 0) ? 1u : 0u;
   hipLaunchKernelGGL(k_codes<false>, gb, dim3(256), 0, s, B, ldb, d.n, d.np / 64, d.k, d.kp,
-                     (const unsigned long long*)(ws + L.colbits), ws + L.codesB);
+                     (const unsigned long long*)(ws + L.colbits), ws + L.codesB, vecB);
   return hipGetLastError();
 }
 
@@ -413,6 +496,9 @@ static int split_resident(size_t lds) {
   }
   const int slot = (int)(lds % (OZ2_MAXR + 1));
   if (cache_lds[slot] == (int)lds) return cache_n[slot];
+  // dynamic LDS above 64 KiB (tables for r = 16 plus the staged tile) must be opted into
+  (void)hipFuncSetAttribute((const void*)k_split<TRANS>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds);
   int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_split<TRANS>, 256, lds) !=
           hipSuccess ||
