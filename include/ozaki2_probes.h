@@ -1,0 +1,53 @@
+/* gfx950 probes behind the emulated DGEMM: the hardware facts its exactness
+ * argument rests on, and the measured peaks its roofline fractions are also
+ * quoted against.  Diagnostics only; the GEMM path never calls them.
+ *
+ * Conventions as in ozaki2.h: device pointers owned by the caller, work
+ * enqueued on `stream` (a hipStream_t, NULL = default stream), status codes
+ * OZ2_OK / OZ2_E_INVALID / OZ2_E_DEVICE / OZ2_E_UNSUPPORTED.
+ */
+#ifndef OZAKI2_PROBES_H
+#define OZAKI2_PROBES_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* E4M3 (OCP E4M3FN) encoding by the conversion instruction the plane split
+ * uses (v_cvt_pk_fp8_f32): out[i] = fp8(x[i]) for i < n.  x: float[n],
+ * out: uint8[n], device.  The digit planes of Eq. (sq-shortcut) / Eq. (kar)
+ * are exact only if every integer they hold encodes exactly; the test
+ * compares this against the format's definition.  n < 0 -> OZ2_E_INVALID. */
+int ozaki2_probe_e4m3(const float* x, unsigned char* out, int n, void* stream);
+
+/* Exactness of FP32 accumulation in the FP8 MFMA (Eq. (accum-exact)): one
+ * 32x32x64 E4M3 product, accumulated `chain` times into the same FP32
+ * accumulator (v_mfma_f32_32x32x64_f8f6f4).  a, b: 64 lanes x 32 bytes of
+ * E4M3 operand (lane L holds row / column L%32, k bytes 32(L/32)..+31),
+ * out: float[64][16] accumulator registers (lane L, register e holds row
+ * 8(e/4) + 4(L/32) + e%4, column L%32).  1 <= chain <= 2^20. */
+int ozaki2_probe_accum(const unsigned char* a, const unsigned char* b, int chain, float* out,
+                       void* stream);
+
+/* Plain copy kernel (16 bytes per lane, grid-stride), bytes % 16 == 0 and
+ * 16-byte aligned pointers; the HBM copy reference for bandwidth fractions and
+ * for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE. */
+int ozaki2_probe_copy(const void* src, void* dst, size_t bytes, void* stream);
+
+/* Measured dense FP8 MFMA rate: independent 32x32x64 MFMAs on every SIMD
+ * (2 waves per SIMD), timed with HIP events on an internal stream;
+ * synchronous.  iters >= 1.  *tflops = FP8 TFLOP/s. */
+int ozaki2_probe_mfma_peak(int iters, double* tflops);
+
+/* Measured HBM copy bandwidth: copies `bytes` (>= 16 MiB) between two
+ * internally allocated buffers `reps` times; synchronous; frees the buffers.
+ * *gbs = (read + write bytes) / s / 1e9. */
+int ozaki2_probe_copy_peak(size_t bytes, int reps, double* gbs);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OZAKI2_PROBES_H */

@@ -46,6 +46,12 @@ EXPORTS = [
     "ozaki2_status_string", "ozaki2_finalize",
 ]
 
+# include/ozaki2_probes.h
+PROBE_EXPORTS = [
+    "ozaki2_probe_e4m3", "ozaki2_probe_accum", "ozaki2_probe_copy", "ozaki2_probe_mfma_peak",
+    "ozaki2_probe_copy_peak",
+]
+
 
 class Ozaki2Error(RuntimeError):
     def __init__(self, fn, status):
@@ -81,6 +87,11 @@ def load():
         "ozaki2_plan_query": (i, [p, i, p, sz]),
         "ozaki2_status_string": (ctypes.c_char_p, [i]),
         "ozaki2_finalize": (None, []),
+        "ozaki2_probe_e4m3": (i, [p, p, i, p]),
+        "ozaki2_probe_accum": (i, [p, p, i, p, p]),
+        "ozaki2_probe_copy": (i, [p, p, sz, p]),
+        "ozaki2_probe_mfma_peak": (i, [i, ctypes.POINTER(ctypes.c_double)]),
+        "ozaki2_probe_copy_peak": (i, [sz, i, ctypes.POINTER(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -203,3 +214,34 @@ def ozaki2_status_string(status):
 
 def ozaki2_finalize():
     load().ozaki2_finalize()
+
+
+# ------------------------------------------------------------ probes (ozaki2_probes.h)
+
+def ozaki2_probe_e4m3(x, out, n, stream=None):
+    return _check("ozaki2_probe_e4m3", load().ozaki2_probe_e4m3(_ptr(x), _ptr(out), n,
+                                                                _stream(stream)))
+
+
+def ozaki2_probe_accum(a, b, chain, out, stream=None):
+    return _check("ozaki2_probe_accum", load().ozaki2_probe_accum(_ptr(a), _ptr(b), chain,
+                                                                  _ptr(out), _stream(stream)))
+
+
+def ozaki2_probe_copy(src, dst, nbytes, stream=None):
+    return _check("ozaki2_probe_copy", load().ozaki2_probe_copy(_ptr(src), _ptr(dst), nbytes,
+                                                                _stream(stream)))
+
+
+def ozaki2_probe_mfma_peak(iters):
+    """Measured dense FP8 MFMA TFLOP/s (synchronous)."""
+    v = ctypes.c_double(0.0)
+    _check("ozaki2_probe_mfma_peak", load().ozaki2_probe_mfma_peak(iters, ctypes.byref(v)))
+    return v.value
+
+
+def ozaki2_probe_copy_peak(nbytes, reps):
+    """Measured HBM copy GB/s, read + write bytes (synchronous)."""
+    v = ctypes.c_double(0.0)
+    _check("ozaki2_probe_copy_peak", load().ozaki2_probe_copy_peak(nbytes, reps, ctypes.byref(v)))
+    return v.value

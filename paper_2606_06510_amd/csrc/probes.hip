@@ -1,0 +1,191 @@
+// gfx950 probes (see include/ozaki2_probes.h): E4M3 encoding, FP32
+// accumulation exactness of the FP8 MFMA, MFMA peak, HBM copy peak.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <cstring>
+
+#include "../../include/ozaki2.h"
+#include "../../include/ozaki2_probes.h"
+
+namespace {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+__global__ void k_e4m3(const float* __restrict__ x, uint8_t* __restrict__ out, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int w = __builtin_amdgcn_cvt_pk_fp8_f32(x[i], 0.0f, 0, false);
+  out[i] = (uint8_t)(w & 0xFF);
+}
+
+__global__ void __launch_bounds__(64) k_accum(const uint8_t* __restrict__ a,
+                                              const uint8_t* __restrict__ b, int chain,
+                                              float* __restrict__ out) {
+  const int l = threadIdx.x;
+  v8i av, bv;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    av[i] = (int)(a[32 * l + 4 * i] | (a[32 * l + 4 * i + 1] << 8) | (a[32 * l + 4 * i + 2] << 16) |
+                  ((uint32_t)a[32 * l + 4 * i + 3] << 24));
+    bv[i] = (int)(b[32 * l + 4 * i] | (b[32 * l + 4 * i + 1] << 8) | (b[32 * l + 4 * i + 2] << 16) |
+                  ((uint32_t)b[32 * l + 4 * i + 3] << 24));
+  }
+  v16f acc = v16f{0.f};
+  for (int c = 0; c < chain; ++c)
+    acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, acc, 0, 0, 0, 0, 0, 0);
+#pragma unroll
+  for (int e = 0; e < 16; ++e) out[16 * l + e] = acc[e];
+}
+
+// grid-stride 16-byte copy; 4 workgroups per CU measured fastest among
+// 1K-64K workgroups and 1-8 loads in flight per lane
+__global__ void __launch_bounds__(256) k_copy(const uint4* __restrict__ src, uint4* __restrict__ dst,
+                                              size_t n16) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
+    dst[i] = src[i];
+}
+
+// 8 independent accumulators per wave, 2 waves per SIMD (512 threads per CU)
+__global__ void __launch_bounds__(512) k_mfma_peak(int iters, float* sink) {
+  v8i a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = 0x38383838 + (int)threadIdx.x;
+    b[i] = 0x30303030 + i;
+  }
+  v16f acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = v16f{0.f};
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      acc[j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, acc[j], 0, 0, 0, 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s += acc[j][e];
+  if (s == 1.0e30f) sink[threadIdx.x] = s;   // keeps the MFMAs live; never true
+}
+
+int gfx950_ok() {
+  int dev = 0;
+  hipDeviceProp_t prop;
+  if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess)
+    return OZ2_E_DEVICE;
+  return std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? OZ2_OK : OZ2_E_UNSUPPORTED;
+}
+
+int status(hipError_t e) { return e == hipSuccess ? OZ2_OK : OZ2_E_DEVICE; }
+
+}  // namespace
+
+extern "C" {
+
+int ozaki2_probe_e4m3(const float* x, unsigned char* out, int n, void* stream) {
+  if (n < 0 || (n > 0 && (!x || !out))) return OZ2_E_INVALID;
+  if (n == 0) return OZ2_OK;
+  int st = gfx950_ok();
+  if (st != OZ2_OK) return st;
+  hipLaunchKernelGGL(k_e4m3, dim3((n + 255) / 256), dim3(256), 0, (hipStream_t)stream, x, out, n);
+  return status(hipGetLastError());
+}
+
+int ozaki2_probe_accum(const unsigned char* a, const unsigned char* b, int chain, float* out,
+                       void* stream) {
+  if (!a || !b || !out || chain < 1 || chain > (1 << 20)) return OZ2_E_INVALID;
+  int st = gfx950_ok();
+  if (st != OZ2_OK) return st;
+  hipLaunchKernelGGL(k_accum, dim3(1), dim3(64), 0, (hipStream_t)stream, a, b, chain, out);
+  return status(hipGetLastError());
+}
+
+int ozaki2_probe_copy(const void* src, void* dst, size_t bytes, void* stream) {
+  if (bytes % 16 || ((uintptr_t)src % 16) || ((uintptr_t)dst % 16)) return OZ2_E_INVALID;
+  if (bytes == 0) return OZ2_OK;
+  if (!src || !dst) return OZ2_E_INVALID;
+  int st = gfx950_ok();
+  if (st != OZ2_OK) return st;
+  const size_t n16 = bytes / 16;
+  size_t blocks = (n16 + 255) / 256;
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(k_copy, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
+                     (const uint4*)src, (uint4*)dst, n16);
+  return status(hipGetLastError());
+}
+
+int ozaki2_probe_mfma_peak(int iters, double* tflops) {
+  if (iters < 1 || !tflops) return OZ2_E_INVALID;
+  int st = gfx950_ok();
+  if (st != OZ2_OK) return st;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return OZ2_E_DEVICE;
+  float* sink = nullptr;
+  hipStream_t s = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  hipError_t e = hipMalloc(&sink, 512 * sizeof(float));
+  if (e == hipSuccess) e = hipStreamCreate(&s);
+  if (e == hipSuccess) e = hipEventCreate(&e0);
+  if (e == hipSuccess) e = hipEventCreate(&e1);
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL(k_mfma_peak, dim3(cus), dim3(512), 0, s, iters, sink);   // warm-up
+    e = hipEventRecord(e0, s);
+  }
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL(k_mfma_peak, dim3(cus), dim3(512), 0, s, iters, sink);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess) e = hipEventRecord(e1, s);
+  if (e == hipSuccess) e = hipEventSynchronize(e1);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  if (e == hipSuccess) {
+    const double flop = 2.0 * 32 * 32 * 64 * 8.0 * iters * 8.0 * cus;   // 8 waves x 8 MFMAs x iters
+    *tflops = flop / (ms * 1e-3) / 1e12;
+  }
+  if (e1) (void)hipEventDestroy(e1);
+  if (e0) (void)hipEventDestroy(e0);
+  if (s) (void)hipStreamDestroy(s);
+  if (sink) (void)hipFree(sink);
+  return status(e);
+}
+
+int ozaki2_probe_copy_peak(size_t bytes, int reps, double* gbs) {
+  if (bytes < ((size_t)16 << 20) || bytes % 16 || reps < 1 || !gbs) return OZ2_E_INVALID;
+  int st = gfx950_ok();
+  if (st != OZ2_OK) return st;
+  void *src = nullptr, *dst = nullptr;
+  hipStream_t s = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  hipError_t e = hipMalloc(&src, bytes);
+  if (e == hipSuccess) e = hipMalloc(&dst, bytes);
+  if (e == hipSuccess) e = hipMemset(src, 0x5A, bytes);
+  if (e == hipSuccess) e = hipStreamCreate(&s);
+  if (e == hipSuccess) e = hipEventCreate(&e0);
+  if (e == hipSuccess) e = hipEventCreate(&e1);
+  auto copy = [&]() {
+    return ozaki2_probe_copy(src, dst, bytes, s) == OZ2_OK ? hipSuccess : hipErrorLaunchFailure;
+  };
+  if (e == hipSuccess) e = copy();   // warm-up
+  if (e == hipSuccess) e = hipEventRecord(e0, s);
+  for (int i = 0; i < reps && e == hipSuccess; ++i) e = copy();
+  if (e == hipSuccess) e = hipEventRecord(e1, s);
+  if (e == hipSuccess) e = hipEventSynchronize(e1);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  if (e == hipSuccess) *gbs = 2.0 * (double)bytes * reps / (ms * 1e-3) / 1e9;
+  if (e1) (void)hipEventDestroy(e1);
+  if (e0) (void)hipEventDestroy(e0);
+  if (s) (void)hipStreamDestroy(s);
+  if (dst) (void)hipFree(dst);
+  if (src) (void)hipFree(src);
+  return status(e);
+}
+
+}  // extern "C"

@@ -1,0 +1,89 @@
+"""Render rocprofv3 output into the short text summaries kept under profiles/.
+
+    python -m paper_2606_06510_amd.rocprof_summary stats STATS_CSV OUT_MD TITLE COMMAND
+    python -m paper_2606_06510_amd.rocprof_summary traffic FETCH_CSV WRITE_CSV OUT_TXT \\
+        KERNEL COPY_BYTES SOURCE CMD_FETCH CMD_WRITE
+
+``stats`` turns a ``--kernel-trace --stats`` kernel_stats.csv into a markdown
+table.  ``traffic`` reads two ``--pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE``
+counter_collection.csv files (KiB per dispatch), takes the mean per launch of
+KERNEL and of the plain copy kernel (COPY_BYTES read and written), and scales
+the kernel's figures by copy_bytes / copy_reading; the result carries the
+sha256 of SOURCE so that bench.py uses it only for the kernel it was taken on.
+"""
+from __future__ import annotations
+
+import collections
+import csv
+import hashlib
+import sys
+
+
+def _short(name):
+    if name.startswith("Cijk_"):
+        return "rocBLAS DGEMM " + name.split("_")[3] + " (torch.matmul float64, baseline)"
+    return name.replace("(anonymous namespace)::", "").split("(")[0]
+
+
+def stats(src, dst, title, cmd):
+    rows = list(csv.DictReader(open(src)))
+    with open(dst, "w") as f:
+        f.write(f"# {title}\n\nCommand (from the repository root, on one MI355X):\n\n```\n{cmd}\n```\n\n")
+        f.write("| kernel | calls | avg (us) | min (us) | max (us) | share |\n|---|---|---|---|---|---|\n")
+        for r in rows:
+            f.write(f"| {_short(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                    f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
+                    f"{float(r['Percentage']):.1f}% |\n")
+
+
+def _per_launch(path, counter):
+    """{kernel short name: mean over dispatches of the summed counter value}."""
+    per = collections.defaultdict(float)
+    names = {}
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] != counter:
+            continue
+        key = r["Dispatch_Id"]
+        per[key] += float(r["Counter_Value"])
+        names[key] = _short(r["Kernel_Name"])
+    by = collections.defaultdict(list)
+    for key, v in per.items():
+        by[names[key]].append(v)
+    return {k: sum(v) / len(v) for k, v in by.items()}
+
+
+def traffic(fetch_csv, write_csv, dst, kernel, copy_bytes, source, cmd_fetch, cmd_write):
+    fetch = _per_launch(fetch_csv, "FETCH_SIZE")
+    write = _per_launch(write_csv, "WRITE_SIZE")
+    copy = next(k for k in fetch if k.startswith("k_copy"))
+    sf = copy_bytes / (fetch[copy] * 1024.0)
+    sw = copy_bytes / (write[copy] * 1024.0)
+    kf, kw = fetch[kernel] * 1024.0 * sf, write[kernel] * 1024.0 * sw
+    sha = hashlib.sha256(open(source, "rb").read()).hexdigest()
+    with open(dst, "w") as f:
+        f.write(f"# HBM traffic per launch of {kernel}: rocprofv3 FETCH_SIZE and WRITE_SIZE (KiB per\n"
+                f"# dispatch), each scaled by the reading of a plain copy kernel of {copy_bytes} bytes.\n")
+        f.write(f"command_fetch: {cmd_fetch}\ncommand_write: {cmd_write}\n")
+        f.write(f"kernel: {kernel}\nkernel_source: {source}\nkernel_source_sha256: {sha}\n")
+        f.write(f"copy_fetch_kib: {fetch[copy]:.1f}\ncopy_write_kib: {write[copy]:.1f}\n")
+        f.write(f"fetch_scale: {sf:.4f}\nwrite_scale: {sw:.4f}\n")
+        f.write(f"kernel_fetch_kib_per_launch: {fetch[kernel]:.1f}\n"
+                f"kernel_write_kib_per_launch: {write[kernel]:.1f}\n")
+        f.write(f"fetch_bytes_per_launch: {kf:.0f}\nwrite_bytes_per_launch: {kw:.0f}\n")
+        f.write(f"traffic_bytes_per_launch: {kf + kw:.0f}\n")
+        f.write("# all kernels (KiB per launch, unscaled): fetch / write\n")
+        for k in sorted(fetch):
+            f.write(f"#   {k}: {fetch[k]:.1f} / {write.get(k, float('nan')):.1f}\n")
+
+
+def main(argv):
+    if argv[0] == "stats":
+        stats(*argv[1:5])
+    elif argv[0] == "traffic":
+        traffic(argv[1], argv[2], argv[3], argv[4], int(argv[5]), argv[6], argv[7], argv[8])
+    else:
+        raise SystemExit(__doc__)
+
+
+if __name__ == "__main__":
+    main(sys.argv[1:])

@@ -12,19 +12,39 @@ from paper_2606_06510_amd import _lib
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def _declared():
-    src = open(os.path.join(ROOT, "include", "ozaki2.h")).read()
+def _declared(header):
+    src = open(os.path.join(ROOT, "include", header)).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(ozaki2_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(ozaki2_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_library_exports_every_declared_symbol():
     L = oz.load()
-    names = _declared()
+    names = _declared("ozaki2.h")
     assert len(names) == 14
     for n in names:
         assert hasattr(L, n), n
     assert sorted(_lib.EXPORTS) == names
+    probes = _declared("ozaki2_probes.h")
+    assert len(probes) == 5
+    for n in probes:
+        assert hasattr(L, n), n
+    assert sorted(_lib.PROBE_EXPORTS) == probes
+    headers = sorted(f for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h"))
+    assert headers == ["ozaki2.h", "ozaki2_probes.h"]
+
+
+def test_probe_argument_checks():
+    with pytest.raises(oz.Ozaki2Error):
+        oz.ozaki2_probe_e4m3(0, 0, -1, 0)
+    with pytest.raises(oz.Ozaki2Error):
+        oz.ozaki2_probe_accum(0, 0, 1, 0, 0)          # null pointers
+    with pytest.raises(oz.Ozaki2Error):
+        oz.ozaki2_probe_copy(16, 32, 15, 0)           # size not a multiple of 16
+    with pytest.raises(oz.Ozaki2Error):
+        oz.ozaki2_probe_mfma_peak(0)
+    with pytest.raises(oz.Ozaki2Error):
+        oz.ozaki2_probe_copy_peak(1 << 20, 1)         # below 16 MiB
 
 
 def test_status_strings():
