@@ -41,6 +41,9 @@ def parse():
     ap.add_argument("--no-probes", action="store_true", help="skip the measured-peak probes")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB copy kernel (rocprofv3 counter calibration)")
+    ap.add_argument("--accuracy-sweep", action="store_true",
+                    help="instead of the bench line: max componentwise error of a sampled set "
+                         "of outputs against the exact product for r = 8..16")
     return ap.parse_args()
 
 
@@ -84,18 +87,26 @@ def main():
 
     cfg = dict(synth.CONFIGS[args.config])
     r = args.moduli or cfg["r"]
-    if cfg["kind"] in ("batched",):
-        print("bench.py: the batched workload is not a bench line", file=sys.stderr)
-        sys.exit(2)
+    dev = torch.device("cuda:0")
+    if cfg["kind"] == "batched":
+        batched_line(args, cfg, r, dev)
+        return
     drawn = synth.make(args.config)
     A, B = drawn[0], drawn[1]
     m, k = A.shape
     n = B.shape[1]
-    dev = torch.device("cuda:0")
+    if args.accuracy_sweep:
+        accuracy_sweep(A, B, dev)
+        return
     Ad = oz.to_device_colmajor(A, dev)
     Bd = oz.to_device_colmajor(B, dev)
-    Cd = oz.colmajor_empty(m, n, device=dev)
-    plan = oz.Plan(m, n, k, r, 0, device=dev)
+    flags = 0
+    if cfg["kind"] == "rankk":
+        Cd = oz.to_device_colmajor(drawn[2], dev)      # C += A B on the drawn C_in
+        flags = oz.OZ2_ACCUMULATE
+    else:
+        Cd = oz.colmajor_empty(m, n, device=dev)
+    plan = oz.Plan(m, n, k, r, flags, device=dev)
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
@@ -163,7 +174,7 @@ def main():
         del src, dst
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and cfg["kind"] != "rankk":
         cpu = cpu_baseline(A, B, r, Cd, args.cpu_sample)
 
     tag = f"resgemm_{args.config}_r{r}"
@@ -210,6 +221,80 @@ def main():
             "deconstruct_hbm": round(dec_gbs / peaks["hbm_copy_gbs"], 4),
             "reconstruct_hbm": round(rec_gbs / peaks["hbm_copy_gbs"], 4)}
     print(json.dumps(out))
+
+
+def accuracy_sweep(A, B, dev):
+    """Max componentwise error |C - AB| / (|A||B|) over 256 sampled outputs
+    (exact error by compensated summation) for every moduli count."""
+    import torch
+    import paper_2606_06510_amd as oz
+    from oracle import refgemm
+    m, k = A.shape
+    n = B.shape[1]
+    rng = np.random.default_rng(4321)
+    rows = rng.integers(0, m, 256)
+    cols = rng.integers(0, n, 256)
+    Ad = oz.to_device_colmajor(A, dev)
+    Bd = oz.to_device_colmajor(B, dev)
+    Cd = oz.colmajor_empty(m, n, device=dev)
+    chart = {}
+    for r in range(8, 17):
+        plan = oz.Plan(m, n, k, r, 0, device=dev)
+        plan.deconstruct(Ad, Bd)
+        plan.residue_gemm()
+        plan.reconstruct(Cd)
+        torch.cuda.synchronize()
+        C = oz.from_device_colmajor(Cd)[rows, cols]
+        chart[r] = {"alpha": 3 * r + 1,
+                    "max_componentwise_err": refgemm.componentwise_ratio(C, A, B, rows, cols)}
+        del plan
+    print(json.dumps({"accuracy_vs_moduli": chart, "sample": "256 random outputs",
+                      "m": m, "n": n, "k": k}))
+
+
+def batched_line(args, cfg, r, dev):
+    """Strided-batched workload: one ozaki2_dgemm_strided_batched call per step."""
+    import torch
+    import synth
+    import paper_2606_06510_amd as oz
+    Ab, Bb = synth.make(args.config)
+    nb, m, k = Ab.shape
+    n = Bb.shape[2]
+    Ad = torch.from_numpy(np.ascontiguousarray(Ab.transpose(0, 2, 1))).to(dev)
+    Bd = torch.from_numpy(np.ascontiguousarray(Bb.transpose(0, 2, 1))).to(dev)
+    Cd = torch.empty((nb, n, m), dtype=torch.float64, device=dev)
+
+    def step():
+        oz.ozaki2_dgemm_strided_batched(m, n, k, Ad, m, m * k, Bd, k, k * n, Cd, m, m * n, nb, r)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    flop = 2.0 * m * n * k * nb
+    At = Ad.transpose(1, 2)
+    Bt = Bd.transpose(1, 2)
+    for _ in range(2):
+        torch.bmm(At.contiguous(), Bt.contiguous())
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for _ in range(5):
+        torch.bmm(At.contiguous(), Bt.contiguous())
+    torch.cuda.synchronize()
+    native = flop / ((time.perf_counter() - t) / 5) / 1e12
+    print(json.dumps({
+        "metric": "effective FP64 TFLOPS of emulated DGEMM (Ozaki-II on FP8 MFMA)",
+        "value": round(flop / (ms * 1e-3) / 1e12, 4), "unit": "TFLOPS", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "fp8-e4m3 MFMA -> exact int -> f64", "data": "synthetic (seeded numpy PCG64)",
+        "config": {"workload": f"{args.config}: {nb} strided-batched {m}x{n}x{k} products, r={r}",
+                   "batch": nb, "m": m, "n": n, "k": k, "num_moduli": r},
+        "native_fp64_tflops": round(native, 3)}))
 
 
 def plan_pstore(r):

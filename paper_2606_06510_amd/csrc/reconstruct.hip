@@ -334,35 +334,97 @@ __global__ void k_fallback_lists(Oz2Dims d, const uint32_t* __restrict__ fA,
   }
 }
 
-// Native FP64 for flagged entries: one FMA per k in ascending k.  A
-// grid-stride loop over the device-side counts, so the launch needs no host
-// synchronisation and every wave exits when the list is exhausted.
+// Native FP64 for flagged entries: one FMA per k in ascending k for every
+// output (the same order as a plain dot product loop), register-tiled so the
+// flagged rows run at FP64 FMA speed.  Work = (flagged rows of A) x (all
+// columns) + (all unflagged rows) x (flagged columns of B), in 64 x 64 output
+// tiles walked by a grid-stride loop over the device-side counts (no host
+// synchronisation; every workgroup exits when the tiles are exhausted).  A
+// tile stages 64 rows x 16 k of A and 16 k x 64 columns of B through LDS;
+// each thread owns 4 x 4 outputs (rows ty + 16 u, columns tx + 16 v).
+constexpr int FB_T = 64, FB_K = 16;
+
 __global__ void __launch_bounds__(256)
 k_fallback(Oz2Dims d, const double* __restrict__ A, int lda, const double* __restrict__ B, int ldb,
            double* C, int ldc, const int* __restrict__ counters, const int* __restrict__ listA,
            const int* __restrict__ listB, const uint32_t* __restrict__ fA) {
-  const size_t na = (size_t)counters[0], nb = (size_t)counters[1];
-  const size_t itemsA = na * (size_t)d.n, total = itemsA + nb * (size_t)d.m;
+  __shared__ double sa[FB_K][FB_T + 1];
+  __shared__ double sb[FB_K][FB_T + 1];
+  __shared__ int rowid[FB_T], colid[FB_T];
+  const int na = counters[0], nb = counters[1];
   const bool acc = (d.flags & 1u) != 0;
   const bool force = (d.flags & 16u) != 0;
-  for (size_t it = (size_t)blockIdx.x * blockDim.x + threadIdx.x; it < total;
-       it += (size_t)gridDim.x * blockDim.x) {
-    int i, j;
-    if (it < itemsA) {
-      i = listA[it / d.n];
-      j = (int)(it % d.n);
+  // part 1: ceil(na/64) x ceil(n/64) tiles; part 2: ceil(m/64) x ceil(nb/64) tiles
+  const int t1r = (na + FB_T - 1) / FB_T, t1c = (d.n + FB_T - 1) / FB_T;
+  const int t2r = (d.m + FB_T - 1) / FB_T, t2c = (nb + FB_T - 1) / FB_T;
+  const long long tiles1 = (long long)t1r * t1c, total = tiles1 + (long long)t2r * t2c;
+  const int t = threadIdx.x, tx = t & 15, ty = t >> 4;
+  for (long long tile = blockIdx.x; tile < total; tile += gridDim.x) {
+    int nr, nc;                 // valid rows / columns of this tile
+    if (tile < tiles1) {
+      const int tr = (int)(tile / t1c), tc = (int)(tile % t1c);
+      nr = min(FB_T, na - tr * FB_T);
+      nc = min(FB_T, d.n - tc * FB_T);
+      if (t < FB_T) {
+        rowid[t] = t < nr ? listA[tr * FB_T + t] : -1;
+        colid[t] = t < nc ? tc * FB_T + t : -1;
+      }
     } else {
-      const size_t u = it - itemsA;
-      j = listB[u / d.m];
-      i = (int)(u % d.m);
-      if (force || (fA[i] & (OZ2_T1 | OZ2_T2))) continue;   // done as a flagged row
+      const long long u = tile - tiles1;
+      const int tr = (int)(u / t2c), tc = (int)(u % t2c);
+      nr = min(FB_T, d.m - tr * FB_T);
+      nc = min(FB_T, nb - tc * FB_T);
+      if (t < FB_T) {
+        int i = tr * FB_T + t;
+        // rows already recomputed in part 1 (flagged rows) are skipped here
+        rowid[t] = (t < nr && !(force || (fA[i] & (OZ2_T1 | OZ2_T2)))) ? i : -1;
+        colid[t] = t < nc ? listB[tc * FB_T + t] : -1;
+      }
     }
-    const double* a = A + i;
-    const double* b = B + (size_t)j * ldb;
-    double s = 0.0;
-    for (int l = 0; l < d.k; ++l) s = fma(a[(size_t)l * lda], b[l], s);
-    double* o = C + i + (size_t)j * ldc;
-    *o = acc ? *o + s : s;
+    __syncthreads();
+    double s[4][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) s[u][v] = 0.0;
+    for (int l0 = 0; l0 < d.k; l0 += FB_K) {
+      // stage A (64 rows x 16 k) and B (16 k x 64 columns); out-of-range -> 0
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = t + 256 * q;             // 0..1023
+        const int rr = e & 63, kk = e >> 6;    // A: rows fastest (column-major A)
+        const int i = rowid[rr], l = l0 + kk;
+        sa[kk][rr] = (i >= 0 && l < d.k) ? A[(size_t)i + (size_t)l * lda] : 0.0;
+        const int cc = e >> 4, kb = e & 15;    // B: k fastest (column-major B)
+        const int j = colid[cc], lb = l0 + kb;
+        sb[kb][cc] = (j >= 0 && lb < d.k) ? B[(size_t)lb + (size_t)j * ldb] : 0.0;
+      }
+      __syncthreads();
+      const int kn = min(FB_K, d.k - l0);
+      for (int kk = 0; kk < kn; ++kk) {
+        double a[4], b[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) a[u] = sa[kk][ty + 16 * u];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) b[v] = sb[kk][tx + 16 * v];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) s[u][v] = fma(a[u], b[v], s[u][v]);
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int i = rowid[ty + 16 * u], j = colid[tx + 16 * v];
+        if (i >= 0 && j >= 0) {
+          double* o = C + (size_t)i + (size_t)j * ldc;
+          *o = acc ? *o + s[u][v] : s[u][v];
+        }
+      }
+    __syncthreads();   // rowid / colid are rewritten by the next tile
   }
 }
 
