@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(os.path.dirname(HERE), "_build")
 LIB = os.path.join(HERE, "libozaki2.so")
-SOURCES = ["api.cpp", "deconstruct.hip", "gemm.hip", "reconstruct.hip", "probes.hip"]
+SOURCES = ["api.cpp", "deconstruct.hip", "gemm.hip", "reconstruct.hip", "batched.hip", "probes.hip"]
 
 
 def hipcc():

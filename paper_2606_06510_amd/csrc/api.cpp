@@ -449,6 +449,24 @@ int ozaki2_dgemm_strided_batched(int m, int n, int k, const double* A, int lda, 
   if (st != OZ2_OK) return st;
   if (batch == 0 || m == 0 || n == 0) return OZ2_OK;
   if (batch > 1 && (size_t)strideC * sizeof(double) < span_bytes(m, n, ldc)) return OZ2_E_INVALID;
+  if (m <= 64 && n <= 64 && k <= 64 && k > 0) {
+    // one launch for all problems: every stage inside one workgroup per problem
+    Oz2Const c;
+    if (!make_const(num_moduli, c)) return OZ2_E_INVALID;
+    st = device_ok();
+    if (st != OZ2_OK) return st;
+    void* ws = nullptr;
+    st = pool_get(align256((size_t)c.tabsz * 4), &ws);
+    if (st != OZ2_OK) return st;
+    Oz2Layout L{};
+    L.tabs = 0;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = oz2_launch_tables(L, c, (uint8_t*)ws, s);
+    if (e == hipSuccess)
+      e = oz2_launch_batched(c, m, n, k, batch, A, lda, strideA, B, ldb, strideB, C, ldc, strideC,
+                             (const uint32_t*)ws, s);
+    return e == hipSuccess ? OZ2_OK : OZ2_E_DEVICE;
+  }
   size_t need = ozaki2_workspace_bytes(m, n, k, num_moduli, 0);
   if (need == 0) return OZ2_E_INVALID;
   st = device_ok();

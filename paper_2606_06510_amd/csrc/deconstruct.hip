@@ -9,24 +9,9 @@
 // with lanes along the rows so every load instruction is a contiguous 512 B;
 // B's columns are contiguous along k.  Outputs (codes, planes) are K-blocked
 // byte planes [k/64][rows][64] (the GEMM's stage order), 16 bytes per lane.
-#include "oz2_internal.h"
+#include "oz2_device.h"
 
 namespace {
-
-constexpr unsigned long long kAbsMask = 0x7FFFFFFFFFFFFFFFull;
-constexpr unsigned long long kInfBits = 0x7FF0000000000000ull;
-
-__device__ __forceinline__ unsigned long long abs_bits(double x) {
-  return (unsigned long long)__double_as_longlong(x) & kAbsMask;
-}
-
-// frexp exponent of the finite positive double with bit pattern b (b != 0):
-// x = f * 2^E with f in [1/2, 1).
-__device__ __forceinline__ int exp_of_bits(unsigned long long b) {
-  int e = (int)(b >> 52);
-  if (e) return e - 1022;
-  return (64 - __clzll((long long)b)) - 1074;
-}
 
 __global__ void k_init(unsigned long long* rowbits, int mp, unsigned long long* colbits, int np,
                        uint32_t* Rmax, uint32_t* Kmax, int cslabs) {
@@ -96,20 +81,6 @@ __global__ void __launch_bounds__(256) k_scan_cols(const double* __restrict__ B,
   for (l += lane; l < k; l += 64) mx = max(mx, abs_bits(p[l]));
   for (int off = 32; off; off >>= 1) mx = max(mx, (unsigned long long)__shfl_xor((long long)mx, off));
   if (lane == 0) colbits[j] = mx;
-}
-
-// 4-bit magnitude code c = ceil(16 |x| 2^-E), 0 iff x == 0, else in [1, 16].
-// |x| < 2^E so c <= 16; the scaled value is exact whenever it is >= 1.
-__device__ __forceinline__ float code_of(double x, int E) {
-  if (x == 0.0) return 0.0f;
-  double y = ceil(ldexp(fabs(x), 4 - E));
-  return (float)fmax(y, 1.0);
-}
-
-__device__ __forceinline__ uint32_t pack4_fp8(float a, float b, float c, float d) {
-  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
-  w = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
-  return (uint32_t)w;
 }
 
 // Row segment of 16 consecutive k for one row of A (TRANS) or column of B.
@@ -230,12 +201,6 @@ __global__ void __launch_bounds__(256) k_codes(const double* __restrict__ X, int
   *reinterpret_cast<uint4*>(codes + kblocked(row, l0, rows_pad)) = v;
 }
 
-// widths sigma = min(62, c - ceil(ell(R)/2)), ell(x) = ceil(log2 x) (0 for x <= 1)
-__device__ __forceinline__ int width_of(unsigned long long R, int budget) {
-  int ell = (R > 1) ? (64 - __clzll((long long)(R - 1))) : 0;
-  return min(62, budget - ((ell + 1) >> 1));
-}
-
 __global__ void k_scales(Oz2Dims d, const unsigned long long* __restrict__ rowbits,
                          const unsigned long long* __restrict__ colbits,
                          const uint32_t* __restrict__ Rmax, const uint32_t* __restrict__ Kmax,
@@ -288,47 +253,6 @@ __global__ void k_scales(Oz2Dims d, const unsigned long long* __restrict__ rowbi
   }
 }
 
-// Centred residue of the exact integer a = ah 2^32 + al (|a| <= 2^62) modulo m:
-// t = ah (2^32 mod m) + al is exact (|t| < 2^42) and congruent to a; then
-// q = floor(t/m + 1/2) and d = t - q m is the centred residue in
-// [-floor(m/2), ceil(m/2) - 1].  The fp64 value of t/m + 1/2 is within 2^-18
-// of the true one, and the true one is never within 1/(2m) of an integer for
-// odd m (t/m is never a half-integer); for m = 1024 every step is exact.  So
-// the floor is always the exact one.
-__device__ __forceinline__ int centred_residue(double ah, double al, double m, double c32,
-                                               double dinv) {
-  const double t = fma(ah, c32, al);
-  const double q = floor(fma(t, dinv, 0.5));
-  return (int)fma(-q, m, t);
-}
-
-// Digit planes of a centred residue d of m (the E4M3-exact layouts of the
-// "frozen plane kernel" section):
-//  * square m = s^2, Eq. (sq-shortcut): balanced base-s digits
-//    d0 = ((d + floor(s/2)) mod s) - floor(s/2), d1 = (d - d0)/s;
-//  * nonsquare, Eq. (kar) with b = 4: balanced base-16 digits with the carry
-//    correction of the "e4m3 layout envelope" paragraph (if d0+d1 is not
-//    E4M3-exact -- odd and above 16 in magnitude -- move one unit of base
-//    weight: (d0 - 16 sgn(d0), d1 + sgn(d0))), plus the sum plane d0+d1.
-__device__ __forceinline__ void digits(int d, int m, int s, int& d0, int& d1) {
-  if (s) {
-    const int h = s >> 1;
-    int u = (d + h) % s;
-    u += (u < 0) ? s : 0;
-    d0 = u - h;
-    d1 = (d - d0) / s;
-  } else {
-    d0 = ((d + 8) & 15) - 8;
-    d1 = (d - d0) >> 4;
-    const int sm = d0 + d1, am = sm < 0 ? -sm : sm;
-    if (am > 16 && (am & 1)) {
-      const int sg = d0 > 0 ? 1 : -1;
-      d0 -= 16 * sg;
-      d1 += sg;
-    }
-  }
-}
-
 // residue -> plane bytes: entry toff[i] + d = E4M3(d0) | E4M3(d1) << 8 |
 // E4M3(d0 + d1) << 16 (the third byte unused for square moduli)
 __global__ void k_plane_tables(Oz2Const c, uint32_t* tab) {
@@ -343,14 +267,6 @@ __global__ void k_plane_tables(Oz2Const c, uint32_t* tab) {
   const int lo = __builtin_amdgcn_cvt_pk_fp8_f32((float)d0, (float)d1, 0, false);
   const int hi = __builtin_amdgcn_cvt_pk_fp8_f32((float)(d0 + d1), 0.0f, 0, false);
   tab[idx] = ((uint32_t)lo & 0xFFFFu) | (((uint32_t)hi & 0xFFu) << 16);
-}
-
-// bytes p of four table entries, packed (element j in byte j)
-__device__ __forceinline__ uint32_t gather_byte(uint32_t e0, uint32_t e1, uint32_t e2, uint32_t e3,
-                                                uint32_t sel) {
-  const uint32_t x01 = __builtin_amdgcn_perm(e1, e0, sel);
-  const uint32_t x23 = __builtin_amdgcn_perm(e3, e2, sel);
-  return __builtin_amdgcn_perm(x23, x01, 0x05040100u);
 }
 
 // Quantise (Eq. (scale)) and split into E4M3 digit planes.  A persistent-style

@@ -1,0 +1,254 @@
+// Device helpers shared by the deconstruction, reconstruction and batched
+// kernels (each translation unit gets its own inline copies).
+#pragma once
+#include "oz2_internal.h"
+
+namespace {
+
+constexpr int NL = OZ2_NLIMB;
+
+constexpr unsigned long long kAbsMask = 0x7FFFFFFFFFFFFFFFull;
+constexpr unsigned long long kInfBits = 0x7FF0000000000000ull;
+
+__device__ __forceinline__ unsigned long long abs_bits(double x) {
+  return (unsigned long long)__double_as_longlong(x) & kAbsMask;
+}
+
+// frexp exponent of the finite positive double with bit pattern b (b != 0):
+// x = f * 2^E with f in [1/2, 1).
+__device__ __forceinline__ int exp_of_bits(unsigned long long b) {
+  int e = (int)(b >> 52);
+  if (e) return e - 1022;
+  return (64 - __clzll((long long)b)) - 1074;
+}
+
+// 4-bit magnitude code c = ceil(16 |x| 2^-E), 0 iff x == 0, else in [1, 16].
+// |x| < 2^E so c <= 16; the scaled value is exact whenever it is >= 1.
+__device__ __forceinline__ float code_of(double x, int E) {
+  if (x == 0.0) return 0.0f;
+  double y = ceil(ldexp(fabs(x), 4 - E));
+  return (float)fmax(y, 1.0);
+}
+
+__device__ __forceinline__ uint32_t pack4_fp8(float a, float b, float c, float d) {
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
+  return (uint32_t)w;
+}
+
+// widths sigma = min(62, c - ceil(ell(R)/2)), ell(x) = ceil(log2 x) (0 for x <= 1)
+__device__ __forceinline__ int width_of(unsigned long long R, int budget) {
+  int ell = (R > 1) ? (64 - __clzll((long long)(R - 1))) : 0;
+  return min(62, budget - ((ell + 1) >> 1));
+}
+
+// Centred residue of the exact integer a = ah 2^32 + al (|a| <= 2^62) modulo m:
+// t = ah (2^32 mod m) + al is exact (|t| < 2^42) and congruent to a; then
+// q = floor(t/m + 1/2) and d = t - q m is the centred residue in
+// [-floor(m/2), ceil(m/2) - 1].  The fp64 value of t/m + 1/2 is within 2^-18
+// of the true one, and the true one is never within 1/(2m) of an integer for
+// odd m (t/m is never a half-integer); for m = 1024 every step is exact.  So
+// the floor is always the exact one.
+__device__ __forceinline__ int centred_residue(double ah, double al, double m, double c32,
+                                               double dinv) {
+  const double t = fma(ah, c32, al);
+  const double q = floor(fma(t, dinv, 0.5));
+  return (int)fma(-q, m, t);
+}
+
+// Digit planes of a centred residue d of m (the E4M3-exact layouts of the
+// "frozen plane kernel" section):
+//  * square m = s^2, Eq. (sq-shortcut): balanced base-s digits
+//    d0 = ((d + floor(s/2)) mod s) - floor(s/2), d1 = (d - d0)/s;
+//  * nonsquare, Eq. (kar) with b = 4: balanced base-16 digits with the carry
+//    correction of the "e4m3 layout envelope" paragraph (if d0+d1 is not
+//    E4M3-exact -- odd and above 16 in magnitude -- move one unit of base
+//    weight: (d0 - 16 sgn(d0), d1 + sgn(d0))), plus the sum plane d0+d1.
+__device__ __forceinline__ void digits(int d, int m, int s, int& d0, int& d1) {
+  if (s) {
+    const int h = s >> 1;
+    int u = (d + h) % s;
+    u += (u < 0) ? s : 0;
+    d0 = u - h;
+    d1 = (d - d0) / s;
+  } else {
+    d0 = ((d + 8) & 15) - 8;
+    d1 = (d - d0) >> 4;
+    const int sm = d0 + d1, am = sm < 0 ? -sm : sm;
+    if (am > 16 && (am & 1)) {
+      const int sg = d0 > 0 ? 1 : -1;
+      d0 -= 16 * sg;
+      d1 += sg;
+    }
+  }
+}
+
+// bytes p of four table entries, packed (element j in byte j)
+__device__ __forceinline__ uint32_t gather_byte(uint32_t e0, uint32_t e1, uint32_t e2, uint32_t e3,
+                                                uint32_t sel) {
+  const uint32_t x01 = __builtin_amdgcn_perm(e1, e0, sel);
+  const uint32_t x23 = __builtin_amdgcn_perm(e3, e2, sel);
+  return __builtin_amdgcn_perm(x23, x01, 0x05040100u);
+}
+
+// 32-bit words of the two's complement integer in [-M/2, M/2) for r moduli
+// (log2 M = 76.0, 85.0, 94.0, 102.9, 111.8, 120.8, 129.7, 138.5, 147.4 for
+// r = 8..16; the host checks the same rule).
+template <int R>
+struct NWords {
+  static constexpr int value = R <= 10 ? 3 : (R <= 13 ? 4 : 5);
+};
+
+// Residue I of the 8 a thread holds for one modulus (int16 I of the uint4).
+template <int I>
+__device__ __forceinline__ double res_at(const uint4& v) {
+  constexpr int wi = I >> 1;
+  const uint32_t wd = wi == 0 ? v.x : wi == 1 ? v.y : wi == 2 ? v.z : v.w;
+  return (double)((I & 1) ? ((int32_t)wd >> 16) : (int32_t)(int16_t)(wd & 0xFFFFu));
+}
+
+// limbs j < NW-1 into [0, 2^32) with carries upward (every step exact:
+// integers below 2^48)
+template <int NW>
+__device__ __forceinline__ void normalise(double (&S)[NW]) {
+#pragma unroll
+  for (int j = 0; j < NW - 1; ++j) {
+    const double cy = floor(S[j] * 0x1p-32);
+    S[j] = fma(-cy, 0x1p32, S[j]);
+    S[j + 1] += cy;
+  }
+}
+
+// Exact integer of output I of a thread from its R centred residues:
+// NW words, two's complement, little endian.
+template <int R, int NW, int I>
+__device__ __forceinline__ void crt_words(const Oz2Const& c, const uint4 (&x)[R],
+                                          uint32_t (&w)[NW]) {
+  double S[NW];
+#pragma unroll
+  for (int j = 0; j < NW; ++j) S[j] = 0.0;
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const double xi = res_at<I>(x[i]);
+#pragma unroll
+    for (int j = 0; j < NW; ++j) S[j] = fma(xi, c.W[i][j], S[j]);
+  }
+  // quotient estimate q = rint(X / M) from the three top (unnormalised)
+  // limbs: |S_j| < 2^45, |X/M| <= sum |x_i| < 2^13, so the estimate of X/M
+  // is within 2^-36 of the true value; only within that of +-1/2 can q be
+  // off by one, and an exact range check below settles those.
+  double f = fma(S[NW - 2], 0x1p-32, S[NW - 1]);
+  f = fma(S[NW - 3], 0x1p-64, f);
+  f *= c.mtop;
+  const double q = rint(f);
+#pragma unroll
+  for (int j = 0; j < NW; ++j) S[j] = fma(-q, c.Ml[j], S[j]);
+  normalise<NW>(S);
+  if (fabs(f - q) > 0.49999) {
+    // exact range check, X in [-floor(M/2), ceil(M/2) - 1]:
+    //   P = X - M + floor(M/2) >= 0  <=>  X >= ceil(M/2)   -> X -= M
+    //   N = X + floor(M/2) < 0       <=>  X < -floor(M/2)  -> X += M
+    // (the sign of a normalised limb vector is the sign of its top limb)
+    double P[NW], N[NW];
+#pragma unroll
+    for (int j = 0; j < NW; ++j) {
+      P[j] = S[j] - c.Ml[j] + c.Mhalf[j];
+      N[j] = S[j] + c.Mhalf[j];
+    }
+    normalise<NW>(P);
+    normalise<NW>(N);
+    const double adj = (P[NW - 1] >= 0.0) ? -1.0 : ((N[NW - 1] < 0.0) ? 1.0 : 0.0);
+#pragma unroll
+    for (int j = 0; j < NW; ++j) S[j] = fma(adj, c.Ml[j], S[j]);
+    normalise<NW>(S);
+  }
+#pragma unroll
+  for (int j = 0; j < NW - 1; ++j) w[j] = (uint32_t)S[j];
+  w[NW - 1] = (uint32_t)(int32_t)S[NW - 1];
+}
+
+template <int NW>
+__device__ __forceinline__ uint32_t word_at(const uint32_t (&w)[NW], int i) {
+  uint32_t r = 0;
+#pragma unroll
+  for (int j = 0; j < NW; ++j) r = (i == j) ? w[j] : r;
+  return r;
+}
+
+// RN-even value of |X| 2^-e for a nonzero magnitude whose result is
+// subnormal or zero (the rare path): explicit round and sticky bits at the
+// reduced precision of the subnormal range.
+template <int NW>
+__device__ __forceinline__ double round_subnormal(const uint32_t (&w)[NW], int tb, int e) {
+  const int E = tb - 1 - e;
+  const int p = 53 - (-1022 - E);   // bits kept, < 53
+  if (p < 0) return 0.0;            // below half the smallest subnormal
+  const int sh = tb - p;            // bits below position sh are rounded off (sh > 0)
+  const int wi = sh >> 5, bo = sh & 31;
+  const unsigned long long lo = ((unsigned long long)word_at(w, wi + 1) << 32) | word_at(w, wi);
+  const unsigned long long top = word_at(w, wi + 2);
+  unsigned long long mant = (lo >> bo) | (bo ? (top << (64 - bo)) : 0ull);
+  const int rb = sh - 1;
+  const int rwi = rb >> 5, rbo = rb & 31;
+  const uint32_t rw = word_at(w, rwi);
+  const bool round = (rw >> rbo) & 1u;
+  bool sticky = (rw & ((1u << rbo) - 1u)) != 0u;
+#pragma unroll
+  for (int j = 0; j < NW; ++j) sticky |= (j < rwi) && (w[j] != 0u);
+  if (round && (sticky || (mant & 1ull))) mant += 1ull;
+  return ldexp((double)mant, sh - e);
+}
+
+// RN-even binary64 value of X 2^-e for the NW-word two's complement X.
+// The top 64 bits of |X| (leading bit at bit 63) with a sticky bit OR-ed
+// into bit 0 round to the same 53-bit value as |X| itself (64 > 53 + 2), and
+// one fma of the two 32-bit halves performs that rounding; the power-of-two
+// scaling is exact (or overflows to infinity, the correctly rounded result)
+// unless the result is subnormal, which takes the explicit path.
+template <int NW>
+__device__ __forceinline__ double round_scaled(const uint32_t (&x)[NW], int e) {
+  const uint32_t sm = (uint32_t)((int32_t)x[NW - 1] >> 31);   // all ones if X < 0
+  uint32_t w[NW];
+  uint32_t cy = sm & 1u;
+#pragma unroll
+  for (int j = 0; j < NW; ++j) {   // |X| = (X ^ sm) + (sm & 1)
+    const uint32_t v = (x[j] ^ sm) + cy;
+    cy = (v < cy) ? 1u : 0u;
+    w[j] = v;
+  }
+  uint32_t P[NW];                  // prefix ORs for the sticky bit
+  P[0] = w[0];
+#pragma unroll
+  for (int j = 1; j < NW; ++j) P[j] = P[j - 1] | w[j];
+  // a, b, c: the top nonzero word and the two below it; st: OR of the rest
+  uint32_t a = w[NW - 1], b = w[NW - 2], c = w[NW - 3];
+  uint32_t st = NW >= 4 ? P[NW >= 4 ? NW - 4 : 0] : 0u;
+  int top = NW - 1;
+#pragma unroll
+  for (int s = 0; s < NW - 1; ++s) {
+    const bool z = (a == 0u);
+    const int ni = NW - 4 - s;     // word that enters below c on a shift
+    const uint32_t nxt = ni >= 0 ? w[ni >= 0 ? ni : 0] : 0u;
+    const uint32_t nst = ni >= 1 ? P[ni >= 1 ? ni - 1 : 0] : 0u;
+    a = z ? b : a;
+    b = z ? c : b;
+    c = z ? nxt : c;
+    st = z ? nst : st;
+    top -= z ? 1 : 0;
+  }
+  if (a == 0u) return 0.0;         // exact zero is +0.0
+  const int lz = __clz((int)a);
+  const int tb = 32 * top + 32 - lz;                  // |X| in [2^(tb-1), 2^tb)
+  double v;
+  if (tb - 1 - e < -1022) {
+    v = round_subnormal<NW>(w, tb, e);
+  } else {
+    const uint32_t hi = lz ? __builtin_amdgcn_alignbit(a, b, 32 - lz) : a;
+    const uint32_t lo = lz ? __builtin_amdgcn_alignbit(b, c, 32 - lz) : b;
+    const uint32_t stk = ((st | (c << lz)) != 0u) ? 1u : 0u;
+    v = ldexp(fma((double)hi, 0x1p32, (double)(lo | stk)), tb - 64 - e);
+  }
+  return sm ? -v : v;
+}
+
+}  // namespace

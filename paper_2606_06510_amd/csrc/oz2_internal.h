@@ -90,6 +90,12 @@ hipError_t oz2_launch_fallback(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws
 hipError_t oz2_launch_integers(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
                                uint8_t* ws, uint32_t* out, hipStream_t s);
 hipError_t oz2_launch_fill(double* C, int m, int n, int ldc, hipStream_t s);
+// all of Alg. 1 for `batch` problems of m, n, k <= 64 in one launch; tab = the
+// residue -> plane-byte tables (oz2_launch_tables)
+hipError_t oz2_launch_batched(const Oz2Const& c, int m, int n, int k, int batch, const double* A,
+                              int lda, long long sA, const double* B, int ldb, long long sB,
+                              double* C, int ldc, long long sC, const uint32_t* tab,
+                              hipStream_t s);
 
 // ---------------------------------------------------------------- device helpers
 #ifdef __HIPCC__

@@ -15,171 +15,9 @@
 // The limbs are normalised to five 32-bit words (two's complement), and
 // rounded once to binary64 with the exponent shift -(s_i + t_j), including
 // gradual underflow and overflow.
-#include "oz2_internal.h"
+#include "oz2_device.h"
 
 namespace {
-
-constexpr int NL = OZ2_NLIMB;
-
-// 32-bit words of the two's complement integer in [-M/2, M/2) for r moduli
-// (log2 M = 76.0, 85.0, 94.0, 102.9, 111.8, 120.8, 129.7, 138.5, 147.4 for
-// r = 8..16; the host checks the same rule).
-template <int R>
-struct NWords {
-  static constexpr int value = R <= 10 ? 3 : (R <= 13 ? 4 : 5);
-};
-
-// Residue I of the 8 a thread holds for one modulus (int16 I of the uint4).
-template <int I>
-__device__ __forceinline__ double res_at(const uint4& v) {
-  constexpr int wi = I >> 1;
-  const uint32_t wd = wi == 0 ? v.x : wi == 1 ? v.y : wi == 2 ? v.z : v.w;
-  return (double)((I & 1) ? ((int32_t)wd >> 16) : (int32_t)(int16_t)(wd & 0xFFFFu));
-}
-
-// limbs j < NW-1 into [0, 2^32) with carries upward (every step exact:
-// integers below 2^48)
-template <int NW>
-__device__ __forceinline__ void normalise(double (&S)[NW]) {
-#pragma unroll
-  for (int j = 0; j < NW - 1; ++j) {
-    const double cy = floor(S[j] * 0x1p-32);
-    S[j] = fma(-cy, 0x1p32, S[j]);
-    S[j + 1] += cy;
-  }
-}
-
-// Exact integer of output I of a thread from its R centred residues:
-// NW words, two's complement, little endian.
-template <int R, int NW, int I>
-__device__ __forceinline__ void crt_words(const Oz2Const& c, const uint4 (&x)[R],
-                                          uint32_t (&w)[NW]) {
-  double S[NW];
-#pragma unroll
-  for (int j = 0; j < NW; ++j) S[j] = 0.0;
-#pragma unroll
-  for (int i = 0; i < R; ++i) {
-    const double xi = res_at<I>(x[i]);
-#pragma unroll
-    for (int j = 0; j < NW; ++j) S[j] = fma(xi, c.W[i][j], S[j]);
-  }
-  // quotient estimate q = rint(X / M) from the three top (unnormalised)
-  // limbs: |S_j| < 2^45, |X/M| <= sum |x_i| < 2^13, so the estimate of X/M
-  // is within 2^-36 of the true value; only within that of +-1/2 can q be
-  // off by one, and an exact range check below settles those.
-  double f = fma(S[NW - 2], 0x1p-32, S[NW - 1]);
-  f = fma(S[NW - 3], 0x1p-64, f);
-  f *= c.mtop;
-  const double q = rint(f);
-#pragma unroll
-  for (int j = 0; j < NW; ++j) S[j] = fma(-q, c.Ml[j], S[j]);
-  normalise<NW>(S);
-  if (fabs(f - q) > 0.49999) {
-    // exact range check, X in [-floor(M/2), ceil(M/2) - 1]:
-    //   P = X - M + floor(M/2) >= 0  <=>  X >= ceil(M/2)   -> X -= M
-    //   N = X + floor(M/2) < 0       <=>  X < -floor(M/2)  -> X += M
-    // (the sign of a normalised limb vector is the sign of its top limb)
-    double P[NW], N[NW];
-#pragma unroll
-    for (int j = 0; j < NW; ++j) {
-      P[j] = S[j] - c.Ml[j] + c.Mhalf[j];
-      N[j] = S[j] + c.Mhalf[j];
-    }
-    normalise<NW>(P);
-    normalise<NW>(N);
-    const double adj = (P[NW - 1] >= 0.0) ? -1.0 : ((N[NW - 1] < 0.0) ? 1.0 : 0.0);
-#pragma unroll
-    for (int j = 0; j < NW; ++j) S[j] = fma(adj, c.Ml[j], S[j]);
-    normalise<NW>(S);
-  }
-#pragma unroll
-  for (int j = 0; j < NW - 1; ++j) w[j] = (uint32_t)S[j];
-  w[NW - 1] = (uint32_t)(int32_t)S[NW - 1];
-}
-
-template <int NW>
-__device__ __forceinline__ uint32_t word_at(const uint32_t (&w)[NW], int i) {
-  uint32_t r = 0;
-#pragma unroll
-  for (int j = 0; j < NW; ++j) r = (i == j) ? w[j] : r;
-  return r;
-}
-
-// RN-even value of |X| 2^-e for a nonzero magnitude whose result is
-// subnormal or zero (the rare path): explicit round and sticky bits at the
-// reduced precision of the subnormal range.
-template <int NW>
-__device__ __forceinline__ double round_subnormal(const uint32_t (&w)[NW], int tb, int e) {
-  const int E = tb - 1 - e;
-  const int p = 53 - (-1022 - E);   // bits kept, < 53
-  if (p < 0) return 0.0;            // below half the smallest subnormal
-  const int sh = tb - p;            // bits below position sh are rounded off (sh > 0)
-  const int wi = sh >> 5, bo = sh & 31;
-  const unsigned long long lo = ((unsigned long long)word_at(w, wi + 1) << 32) | word_at(w, wi);
-  const unsigned long long top = word_at(w, wi + 2);
-  unsigned long long mant = (lo >> bo) | (bo ? (top << (64 - bo)) : 0ull);
-  const int rb = sh - 1;
-  const int rwi = rb >> 5, rbo = rb & 31;
-  const uint32_t rw = word_at(w, rwi);
-  const bool round = (rw >> rbo) & 1u;
-  bool sticky = (rw & ((1u << rbo) - 1u)) != 0u;
-#pragma unroll
-  for (int j = 0; j < NW; ++j) sticky |= (j < rwi) && (w[j] != 0u);
-  if (round && (sticky || (mant & 1ull))) mant += 1ull;
-  return ldexp((double)mant, sh - e);
-}
-
-// RN-even binary64 value of X 2^-e for the NW-word two's complement X.
-// The top 64 bits of |X| (leading bit at bit 63) with a sticky bit OR-ed
-// into bit 0 round to the same 53-bit value as |X| itself (64 > 53 + 2), and
-// one fma of the two 32-bit halves performs that rounding; the power-of-two
-// scaling is exact (or overflows to infinity, the correctly rounded result)
-// unless the result is subnormal, which takes the explicit path.
-template <int NW>
-__device__ __forceinline__ double round_scaled(const uint32_t (&x)[NW], int e) {
-  const uint32_t sm = (uint32_t)((int32_t)x[NW - 1] >> 31);   // all ones if X < 0
-  uint32_t w[NW];
-  uint32_t cy = sm & 1u;
-#pragma unroll
-  for (int j = 0; j < NW; ++j) {   // |X| = (X ^ sm) + (sm & 1)
-    const uint32_t v = (x[j] ^ sm) + cy;
-    cy = (v < cy) ? 1u : 0u;
-    w[j] = v;
-  }
-  uint32_t P[NW];                  // prefix ORs for the sticky bit
-  P[0] = w[0];
-#pragma unroll
-  for (int j = 1; j < NW; ++j) P[j] = P[j - 1] | w[j];
-  // a, b, c: the top nonzero word and the two below it; st: OR of the rest
-  uint32_t a = w[NW - 1], b = w[NW - 2], c = w[NW - 3];
-  uint32_t st = NW >= 4 ? P[NW >= 4 ? NW - 4 : 0] : 0u;
-  int top = NW - 1;
-#pragma unroll
-  for (int s = 0; s < NW - 1; ++s) {
-    const bool z = (a == 0u);
-    const int ni = NW - 4 - s;     // word that enters below c on a shift
-    const uint32_t nxt = ni >= 0 ? w[ni >= 0 ? ni : 0] : 0u;
-    const uint32_t nst = ni >= 1 ? P[ni >= 1 ? ni - 1 : 0] : 0u;
-    a = z ? b : a;
-    b = z ? c : b;
-    c = z ? nxt : c;
-    st = z ? nst : st;
-    top -= z ? 1 : 0;
-  }
-  if (a == 0u) return 0.0;         // exact zero is +0.0
-  const int lz = __clz((int)a);
-  const int tb = 32 * top + 32 - lz;                  // |X| in [2^(tb-1), 2^tb)
-  double v;
-  if (tb - 1 - e < -1022) {
-    v = round_subnormal<NW>(w, tb, e);
-  } else {
-    const uint32_t hi = lz ? __builtin_amdgcn_alignbit(a, b, 32 - lz) : a;
-    const uint32_t lo = lz ? __builtin_amdgcn_alignbit(b, c, 32 - lz) : b;
-    const uint32_t stk = ((st | (c << lz)) != 0u) ? 1u : 0u;
-    v = ldexp(fma((double)hi, 0x1p32, (double)(lo | stk)), tb - 64 - e);
-  }
-  return sm ? -v : v;
-}
 
 // Thread mapping shared by the reconstruction kernels.  The residue GEMM
 // leaves, per modulus, each 32x32 output block (wave w of a 256x256 tile,

@@ -142,3 +142,60 @@ def test_plain_entry_point_and_batched():
     for b in range(5):
         rb = oracle.dgemm(Ab[b], Bb[b], 12)
         assert np.array_equal(bits(Cb[b]), bits(rb.C))
+
+
+def _batched_run(Ab, Bb, r):
+    import paper_2606_06510_amd as oz
+    import torch
+    dev = device()
+    nb, m, k = Ab.shape
+    n = Bb.shape[2]
+    Ad = torch.from_numpy(np.ascontiguousarray(Ab.transpose(0, 2, 1))).to(dev)
+    Bd = torch.from_numpy(np.ascontiguousarray(Bb.transpose(0, 2, 1))).to(dev)
+    Cd = torch.full((nb, n, m), float("nan"), dtype=torch.float64, device=dev)
+    oz.ozaki2_dgemm_strided_batched(m, n, k, Ad, m, m * k, Bd, k, k * n, Cd, m, m * n, nb, r)
+    torch.cuda.synchronize()
+    return Cd.cpu().numpy().transpose(0, 2, 1)
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 1), (17, 33, 5), (64, 64, 64), (40, 64, 63), (64, 7, 64)])
+def test_batched_single_launch_shapes(shape):
+    m, n, k = shape
+    Ab, Bb = synth.batched(6, max(m, k), max(n, k), max(k, 1), seed=m * 7 + n + k)
+    Ab = np.ascontiguousarray(Ab[:, :m, :k])
+    Bb = np.ascontiguousarray(Bb[:, :k, :n])
+    C = _batched_run(Ab, Bb, 12)
+    for b in range(Ab.shape[0]):
+        rb = oracle.dgemm(Ab[b], Bb[b], 12)
+        assert np.array_equal(bits(C[b]), bits(rb.C)), (shape, b)
+
+
+@pytest.mark.parametrize("r", [8, 10, 13, 16])
+def test_batched_single_launch_moduli(r):
+    Ab, Bb = synth.batched(4, 64, 64, 64, seed=40 + r)
+    C = _batched_run(Ab, Bb, r)
+    for b in range(4):
+        assert np.array_equal(bits(C[b]), bits(oracle.dgemm(Ab[b], Bb[b], r).C)), (r, b)
+
+
+def test_batched_single_launch_fallback_and_zeros():
+    from tests.gpu_util import fallback_ok
+    Ab, Bb = synth.batched(4, 64, 64, 64, seed=77)
+    Ab = Ab.copy()
+    Bb = Bb.copy()
+    Ab[0, 3, 5] = np.nan                 # T1 row of A
+    Bb[1, 7, 9] = np.inf                 # T1 column of B
+    Ab[2, 10, :32] *= 1e200              # T2: half a row far above the other half
+    Ab[3] = 0.0                          # all-zero problem
+    C = _batched_run(Ab, Bb, 12)
+    for b in range(4):
+        rb = oracle.dgemm(Ab[b], Bb[b], 12)
+        fr = set(rb.fallback_rows.tolist())
+        fc = set(rb.fallback_cols.tolist())
+        for i in range(64):
+            for j in range(64):
+                if i in fr or j in fc:
+                    assert fallback_ok(C[b], Ab[b], Bb[b], i, j), (b, i, j)
+                else:
+                    assert bits(C[b][i, j]) == bits(rb.C[i, j]), (b, i, j)
+    assert np.all(bits(C[3]) == 0)       # exact zero is +0.0
