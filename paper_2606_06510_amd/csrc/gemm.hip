@@ -149,6 +149,16 @@ __device__ __forceinline__ int tile_of(int b, int ntm, int ntn) {
   return (gm * 4 + (in & 3)) + (gn * 8 + (in >> 2)) * ntm;
 }
 
+// Centred residue in [-floor(m/2), ceil(m/2) - 1] of an integer-valued x with
+// |x| <= m: x * RN(1/m) is within 2^-23 of x / m, which is either a
+// half-integer (even m, x = +-m/2) or at least 1/(2m) away from one, so rint
+// picks the exact nearest quotient; of the two ties, +m/2 (hm; 0.5 for odd m,
+// never hit) is mapped to -m/2.
+__device__ __forceinline__ float centre_small(float x, float fm, float inv, float hm) {
+  const float r = __builtin_fmaf(-rintf(x * inv), fm, x);
+  return r == hm ? -hm : r;
+}
+
 // Main loop over stages [it0, it0 + n) of the stage sequence.
 __device__ __forceinline__ void run_stages(const Ctx& x, Dma& dm, uint8_t* LB, uint32_t lds0, int it0,
                                            int n, v16f (&acc)[4][2]) {
@@ -297,8 +307,14 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
   }
   wait_vm<0>();
 
-  // final epilogue: centred residue of fin * acc (+ the previous slab's)
-  const int fin = c.fin[mi];
+  // final epilogue: centred residue of fin * acc (+ the previous slab's),
+  // in fp32 throughout.  acc is an integer with |acc| <= 2^24 and fin is 1 or
+  // 16, so v = fin * acc is exact.  v * RN(1/m) is within 2 * 2^-24 |v| / m
+  // <= 32 / m of v / m (the relative errors of RN(1/m) and of the product),
+  // so v - m rint(.) is an exact integer of magnitude <= m/2 + 32 < m (every
+  // modulus exceeds 64); centre_small then rounds once more, now exactly.
+  const float ffin = (float)c.fin[mi];
+  const float hm = (m & 1) ? 0.5f : 0.5f * fm;   // even m: +m/2 is not canonical
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int16_t* dst = res + (size_t)mi * mp * np + (size_t)tile * (TILE * TILE) + (size_t)w * 8192 +
                  lane * 16;
@@ -306,12 +322,11 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      int r16[16];
+      float r16[16];
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        float v = acc[i][j][e];
-        if (fin != 1) v = __builtin_fmaf(-rintf(v * inv), fm, v) * (float)fin;
-        r16[e] = oz2_centre((int)v, m, inv);
+        const float v = acc[i][j][e] * ffin;
+        r16[e] = centre_small(__builtin_fmaf(-rintf(v * inv), fm, v), fm, inv, hm);
       }
       uint4* p = reinterpret_cast<uint4*>(dst + (i * 2 + j) * 1024);
       if (accumulate) {
@@ -320,13 +335,14 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int old = (int)(int16_t)((ow[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
-          r16[e] = oz2_centre(r16[e] + old, m, inv);
+          r16[e] = centre_small(r16[e] + (float)old, fm, inv, hm);
         }
       }
       uint32_t pk[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        pk[e] = ((uint32_t)r16[2 * e] & 0xFFFFu) | ((uint32_t)r16[2 * e + 1] << 16);
+        pk[e] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pk_i16((int)r16[2 * e],
+                                                                         (int)r16[2 * e + 1]));
       p[0] = make_uint4(pk[0], pk[1], pk[2], pk[3]);
       p[1] = make_uint4(pk[4], pk[5], pk[6], pk[7]);
     }
