@@ -163,8 +163,11 @@ def main():
     peaks = None
     if not args.no_probes:
         peaks = {"fp8_mfma_tflops": round(oz.ozaki2_probe_mfma_peak(2000), 1),
+                 "fp8_mfma_digits_tflops": round(oz.ozaki2_probe_mfma_digits(20000), 1),
                  "hbm_copy_gbs": round(oz.ozaki2_probe_copy_peak(1 << 30, 5), 1),
-                 "how": "gfx950 probes: independent 32x32x64 FP8 MFMAs on every SIMD; "
+                 "how": "gfx950 probes: independent 32x32x64 FP8 MFMAs on every SIMD "
+                        "(near-constant operands; and digit-plane operands read from LDS "
+                        "each step, the residue GEMM's inner loop); "
                         "1 GiB device copy (read + write bytes)"}
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -218,6 +221,7 @@ def main():
     if peaks:
         out["frac_of_measured_peak"] = {
             "residue_gemm_fp8": round(achieved / peaks["fp8_mfma_tflops"], 4),
+            "residue_gemm_fp8_digits": round(achieved / peaks["fp8_mfma_digits_tflops"], 4),
             "deconstruct_hbm": round(dec_gbs / peaks["hbm_copy_gbs"], 4),
             "reconstruct_hbm": round(rec_gbs / peaks["hbm_copy_gbs"], 4)}
     print(json.dumps(out))

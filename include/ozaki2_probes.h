@@ -41,6 +41,16 @@ int ozaki2_probe_copy(const void* src, void* dst, size_t bytes, void* stream);
  * synchronous.  iters >= 1.  *tflops = FP8 TFLOP/s. */
 int ozaki2_probe_mfma_peak(int iters, double* tflops);
 
+/* Sustained FP8 MFMA rate of the residue GEMM's inner loop on plane-like
+ * data: each workgroup (one per CU, 8 waves) holds 64 KiB of E4M3 bytes of
+ * digits uniform in [-11, 11] in LDS; per step every wave reads its next 4 + 2
+ * operand fragments from LDS while 8 MFMAs consume the current ones.  With
+ * operand values toggling like the real planes the chip settles at a lower
+ * clock than with the near-constant operands of ozaki2_probe_mfma_peak; the
+ * residue GEMM's fractions are also quoted against this rate.  Synchronous;
+ * iters >= 2 and even.  *tflops = FP8 TFLOP/s. */
+int ozaki2_probe_mfma_digits(int iters, double* tflops);
+
 /* Measured HBM copy bandwidth: copies `bytes` (>= 16 MiB) between two
  * internally allocated buffers `reps` times; synchronous; frees the buffers.
  * *gbs = (read + write bytes) / s / 1e9. */

@@ -49,7 +49,7 @@ EXPORTS = [
 # include/ozaki2_probes.h
 PROBE_EXPORTS = [
     "ozaki2_probe_e4m3", "ozaki2_probe_accum", "ozaki2_probe_copy", "ozaki2_probe_mfma_peak",
-    "ozaki2_probe_copy_peak",
+    "ozaki2_probe_mfma_digits", "ozaki2_probe_copy_peak",
 ]
 
 
@@ -91,6 +91,7 @@ def load():
         "ozaki2_probe_accum": (i, [p, p, i, p, p]),
         "ozaki2_probe_copy": (i, [p, p, sz, p]),
         "ozaki2_probe_mfma_peak": (i, [i, ctypes.POINTER(ctypes.c_double)]),
+        "ozaki2_probe_mfma_digits": (i, [i, ctypes.POINTER(ctypes.c_double)]),
         "ozaki2_probe_copy_peak": (i, [sz, i, ctypes.POINTER(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
@@ -237,6 +238,14 @@ def ozaki2_probe_mfma_peak(iters):
     """Measured dense FP8 MFMA TFLOP/s (synchronous)."""
     v = ctypes.c_double(0.0)
     _check("ozaki2_probe_mfma_peak", load().ozaki2_probe_mfma_peak(iters, ctypes.byref(v)))
+    return v.value
+
+
+def ozaki2_probe_mfma_digits(iters):
+    """Sustained FP8 MFMA TFLOP/s of the residue GEMM's inner loop on
+    plane-like digit operands read from LDS (synchronous)."""
+    v = ctypes.c_double(0.0)
+    _check("ozaki2_probe_mfma_digits", load().ozaki2_probe_mfma_digits(iters, ctypes.byref(v)))
     return v.value
 
 

@@ -250,15 +250,22 @@ namespace {
 
 int run_deconstruct(ozaki2_plan_s& p, hipStream_t s) {
   const Oz2Dims& d = p.d;
+  // Each operand's second read follows its first directly, and B's planes are
+  // split before A's, so that the re-reads find A or B still in the 256 MiB
+  // memory-side cache where they fit.
+  const bool codes = !(d.flags & OZ2_SCALE_FIXED);
   hipError_t e = oz2_launch_init(d, p.L, p.ws, s);
-  if (e == hipSuccess) e = oz2_launch_scan(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, s);
-  if (!(d.flags & OZ2_SCALE_FIXED)) {
-    if (e == hipSuccess) e = oz2_launch_codes(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, s);
-    if (e == hipSuccess) e = oz2_launch_codegemm(d, p.L, p.ws, s);
+  for (int side : {OZ2_SIDE_A, OZ2_SIDE_B}) {
+    if (e == hipSuccess) e = oz2_launch_scan(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, side, s);
+    if (codes && e == hipSuccess)
+      e = oz2_launch_codes(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, side, s);
   }
+  if (codes && e == hipSuccess) e = oz2_launch_codegemm(d, p.L, p.ws, s);
   if (e == hipSuccess) e = oz2_launch_scales(d, p.L, p.c, p.ws, s);
   if (e == hipSuccess) e = oz2_launch_tables(p.L, p.c, p.ws, s);
-  if (e == hipSuccess) e = oz2_launch_split(d, p.L, p.c, p.ws, p.A, p.lda, p.B, p.ldb, s);
+  for (int side : {OZ2_SIDE_B, OZ2_SIDE_A})
+    if (e == hipSuccess)
+      e = oz2_launch_split(d, p.L, p.c, p.ws, p.A, p.lda, p.B, p.ldb, side, s);
   return hip_status(e);
 }
 

@@ -350,32 +350,40 @@ hipError_t oz2_launch_init(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, hi
 }
 
 hipError_t oz2_launch_scan(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, const double* A,
-                           int lda, const double* B, int ldb, hipStream_t s) {
-  // rows: 512 per workgroup; k chunks sized for >= ~2048 workgroups when k allows
-  const int gx = (d.m + 511) / 512;
-  int kchunk = 32;
-  while ((long long)gx * ((d.k + kchunk - 1) / kchunk) > 4096 && kchunk < 4096) kchunk *= 2;
-  while ((d.k + kchunk - 1) / kchunk > 65535) kchunk *= 2;
-  const unsigned vecA = ((uintptr_t)A % 16 == 0 && lda % 2 == 0) ? 1u : 0u;
-  dim3 ga(gx, (d.k + kchunk - 1) / kchunk);
-  hipLaunchKernelGGL(k_scan_rows, ga, dim3(256), 0, s, A, lda, d.m, d.k, kchunk, vecA,
-                     (unsigned long long*)(ws + L.rowbits));
-  dim3 gb((d.n + 3) / 4);
-  const unsigned vecB = ((uintptr_t)B % 16 == 0 && ldb % 2 == 0) ? 1u : 0u;
-  hipLaunchKernelGGL(k_scan_cols, gb, dim3(256), 0, s, B, ldb, d.n, d.k, vecB,
-                     (unsigned long long*)(ws + L.colbits));
+                           int lda, const double* B, int ldb, int side, hipStream_t s) {
+  if (side & OZ2_SIDE_A) {
+    // rows: 512 per workgroup; k chunks sized for >= ~2048 workgroups when k allows
+    const int gx = (d.m + 511) / 512;
+    int kchunk = 32;
+    while ((long long)gx * ((d.k + kchunk - 1) / kchunk) > 4096 && kchunk < 4096) kchunk *= 2;
+    while ((d.k + kchunk - 1) / kchunk > 65535) kchunk *= 2;
+    const unsigned vecA = ((uintptr_t)A % 16 == 0 && lda % 2 == 0) ? 1u : 0u;
+    dim3 ga(gx, (d.k + kchunk - 1) / kchunk);
+    hipLaunchKernelGGL(k_scan_rows, ga, dim3(256), 0, s, A, lda, d.m, d.k, kchunk, vecA,
+                       (unsigned long long*)(ws + L.rowbits));
+  }
+  if (side & OZ2_SIDE_B) {
+    dim3 gb((d.n + 3) / 4);
+    const unsigned vecB = ((uintptr_t)B % 16 == 0 && ldb % 2 == 0) ? 1u : 0u;
+    hipLaunchKernelGGL(k_scan_cols, gb, dim3(256), 0, s, B, ldb, d.n, d.k, vecB,
+                       (unsigned long long*)(ws + L.colbits));
+  }
   return hipGetLastError();
 }
 
 hipError_t oz2_launch_codes(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, const double* A,
-                            int lda, const double* B, int ldb, hipStream_t s) {
-  dim3 ga((d.mp / 64) * (d.kp / 64));
-  hipLaunchKernelGGL(k_codes<true>, ga, dim3(256), 0, s, A, lda, d.m, d.mp / 64, d.k, d.kp,
-                     (const unsigned long long*)(ws + L.rowbits), ws + L.codesA, 0u);
-  dim3 gb((d.np / 64) * (d.kp / 64));
-  const unsigned vecB = ((uintptr_t)B % 16 == 0 && ldb % 2 == 0) ? 1u : 0u;
-  hipLaunchKernelGGL(k_codes<false>, gb, dim3(256), 0, s, B, ldb, d.n, d.np / 64, d.k, d.kp,
-                     (const unsigned long long*)(ws + L.colbits), ws + L.codesB, vecB);
+                            int lda, const double* B, int ldb, int side, hipStream_t s) {
+  if (side & OZ2_SIDE_A) {
+    dim3 ga((d.mp / 64) * (d.kp / 64));
+    hipLaunchKernelGGL(k_codes<true>, ga, dim3(256), 0, s, A, lda, d.m, d.mp / 64, d.k, d.kp,
+                       (const unsigned long long*)(ws + L.rowbits), ws + L.codesA, 0u);
+  }
+  if (side & OZ2_SIDE_B) {
+    dim3 gb((d.np / 64) * (d.kp / 64));
+    const unsigned vecB = ((uintptr_t)B % 16 == 0 && ldb % 2 == 0) ? 1u : 0u;
+    hipLaunchKernelGGL(k_codes<false>, gb, dim3(256), 0, s, B, ldb, d.n, d.np / 64, d.k, d.kp,
+                       (const unsigned long long*)(ws + L.colbits), ws + L.codesB, vecB);
+  }
   return hipGetLastError();
 }
 
@@ -426,20 +434,25 @@ static int split_resident(size_t lds) {
 }
 
 hipError_t oz2_launch_split(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
-                            const double* A, int lda, const double* B, int ldb, hipStream_t s) {
+                            const double* A, int lda, const double* B, int ldb, int side,
+                            hipStream_t s) {
   unsigned tz = (d.flags & 4u) ? 1u : 0u;   // OZ2_QUANT_TZ
   const size_t lds = (size_t)c.tabsz * 4;
-  const int tA = (d.mp / 64) * (d.kp / 64), tB = (d.np / 64) * (d.kp / 64);
   // persistent-style grids: one resident round of workgroups walks the tiles
-  const int capA = split_resident<true>(lds), capB = split_resident<false>(lds);
-  const unsigned vecB = ((uintptr_t)B % 16 == 0 && ldb % 2 == 0) ? 1u : 0u;
-  hipLaunchKernelGGL(k_split<true>, dim3(tA < capA ? tA : capA), dim3(256), lds, s, c, A, lda, d.m,
-                     d.mp, d.mp / 64, tA, d.k, d.kp, (const int32_t*)(ws + L.sA),
-                     (uint32_t*)(ws + L.flagsA), (const uint32_t*)(ws + L.tabs), ws + L.planesA, tz,
-                     0u);
-  hipLaunchKernelGGL(k_split<false>, dim3(tB < capB ? tB : capB), dim3(256), lds, s, c, B, ldb, d.n,
-                     d.np, d.np / 64, tB, d.k, d.kp, (const int32_t*)(ws + L.tB),
-                     (uint32_t*)(ws + L.flagsB), (const uint32_t*)(ws + L.tabs), ws + L.planesB, tz,
-                     vecB);
+  if (side & OZ2_SIDE_A) {
+    const int tA = (d.mp / 64) * (d.kp / 64), capA = split_resident<true>(lds);
+    hipLaunchKernelGGL(k_split<true>, dim3(tA < capA ? tA : capA), dim3(256), lds, s, c, A, lda,
+                       d.m, d.mp, d.mp / 64, tA, d.k, d.kp, (const int32_t*)(ws + L.sA),
+                       (uint32_t*)(ws + L.flagsA), (const uint32_t*)(ws + L.tabs), ws + L.planesA,
+                       tz, 0u);
+  }
+  if (side & OZ2_SIDE_B) {
+    const int tB = (d.np / 64) * (d.kp / 64), capB = split_resident<false>(lds);
+    const unsigned vecB = ((uintptr_t)B % 16 == 0 && ldb % 2 == 0) ? 1u : 0u;
+    hipLaunchKernelGGL(k_split<false>, dim3(tB < capB ? tB : capB), dim3(256), lds, s, c, B, ldb,
+                       d.n, d.np, d.np / 64, tB, d.k, d.kp, (const int32_t*)(ws + L.tB),
+                       (uint32_t*)(ws + L.flagsB), (const uint32_t*)(ws + L.tabs), ws + L.planesB,
+                       tz, vecB);
+  }
   return hipGetLastError();
 }

@@ -23,6 +23,8 @@
 // sequential "chains" on ONE accumulator set: where the coefficient changes,
 // the exact integer accumulator is reduced mod m and multiplied by
 // c_this / c_next (mod m), so the next product continues the same residue.
+#include <algorithm>
+
 #include "oz2_internal.h"
 
 namespace {
@@ -56,10 +58,11 @@ __device__ __forceinline__ void dma16(const uint8_t* sbase, uint32_t voff, uint3
                : "memory");
 }
 
-// Per-wave DMA stream: operand base pointers of the three plane products (the
-// tile's first row, k-block kbeg), the next stage's block pointers, and how
-// many stages remain in the current product.  All of it is uniform (SGPRs),
-// so a stage costs four DMA instructions and a few scalar adds.
+// Per-wave DMA stream over a sequence of plane products.  The code GEMM is a
+// single product; a residue-GEMM workgroup walks moduli mi0 .. mi1-1 of its
+// tile, three products each, as one continuous stream (the next modulus's
+// first stages load while the previous one's epilogue runs).  All of it is
+// uniform (SGPRs): a stage costs four DMA instructions and a few scalar adds.
 // planes of product q: square  (1,0) (0,1) | (0,0);  nonsquare (1,1) | (0,0) | (2,2)
 __device__ __forceinline__ int planeA(int s, int q) {
   return s ? (q == 0 ? 1 : 0) : (q == 0 ? 1 : (q == 1 ? 0 : 2));
@@ -69,19 +72,28 @@ __device__ __forceinline__ int planeB(int s, int q) {
 }
 
 struct Ctx {
-  const uint8_t* aq[3];   // A: plane of product q at k-block kbeg, tile row 0
-  const uint8_t* bq[3];   // B: same
+  const uint8_t* a0;      // plane 0 (the codes) at the tile's first row, k-block kbeg
+  const uint8_t* b0;
+  size_t psA, psB;        // plane strides
   size_t kbA, kbB;        // k-block strides (padded rows * 64)
   int nk, T;              // stages per product, total stages
+  int mi1;                // residue GEMM: one past the workgroup's last modulus
 };
 
 struct Dma {
   const uint8_t* pa;
   const uint8_t* pb;
-  int left, q;
+  int left, q, mi;        // stages left in product q of modulus mi
   uint32_t vo0, vo1;      // lane offsets of blocks w and w + 8 (VGPR)
   uint32_t mw;            // w * 1 KiB (uniform)
 };
+
+// operand blocks of product q of modulus mi at k-block kbeg
+__device__ __forceinline__ void product_ptrs(const Oz2Const* c, const Ctx& x, int mi, int q, Dma& d) {
+  const int s = c->sq[mi], p0 = c->pbase[mi];
+  d.pa = x.a0 + (size_t)(p0 + planeA(s, q)) * x.psA;
+  d.pb = x.b0 + (size_t)(p0 + planeB(s, q)) * x.psB;
+}
 
 // One stage = A tile (16 x 1 KiB blocks of 16 rows) + B tile (16 blocks);
 // wave w moves blocks w and w + 8 of each.  Lane L writes row 16 blk + L/4,
@@ -95,25 +107,32 @@ __device__ __forceinline__ Dma dma_init(const Ctx& x) {
   d.vo0 = lo + (uint32_t)w * 1024u;
   d.vo1 = d.vo0 + 8u * 1024u;
   d.mw = (uint32_t)w * 1024u;
-  d.pa = x.aq[0];
-  d.pb = x.bq[0];
+  d.pa = x.a0;
+  d.pb = x.b0;
   d.left = x.nk;
   d.q = 0;
+  d.mi = 0;
   return d;
 }
 
-__device__ __forceinline__ void issue_stage(const Ctx& x, Dma& d, uint32_t lbase) {
+// RES: advance through the residue products up to modulus Ctx::mi1 (c = the
+// plan constants); otherwise the stream is the single code product (c unused).
+template <bool RES>
+__device__ __forceinline__ void issue_stage(const Oz2Const* c, const Ctx& x, Dma& d,
+                                            uint32_t lbase) {
   dma16(d.pa, d.vo0, lbase + d.mw);
   dma16(d.pa, d.vo1, lbase + d.mw + 8u * 1024u);
   dma16(d.pb, d.vo0, lbase + OPB + d.mw);
   dma16(d.pb, d.vo1, lbase + OPB + d.mw + 8u * 1024u);
   d.pa += x.kbA;
   d.pb += x.kbB;
-  if (--d.left == 0) {
-    ++d.q;
+  if (RES && --d.left == 0) {
     d.left = x.nk;
-    d.pa = d.q == 1 ? x.aq[1] : x.aq[2];
-    d.pb = d.q == 1 ? x.bq[1] : x.bq[2];
+    if (++d.q == 3) {
+      d.q = 0;
+      ++d.mi;
+    }
+    if (d.mi < x.mi1) product_ptrs(c, x, d.mi, d.q, d);
   }
 }
 
@@ -159,20 +178,25 @@ __device__ __forceinline__ float centre_small(float x, float fm, float inv, floa
   return r == hm ? -hm : r;
 }
 
-// Main loop over stages [it0, it0 + n) of the stage sequence.
-__device__ __forceinline__ void run_stages(const Ctx& x, Dma& dm, uint8_t* LB, uint32_t lds0, int it0,
-                                           int n, v16f (&acc)[4][2]) {
+// Main loop over stages [it0, it0 + n) of the stage sequence.  drain: the
+// first of them follows an epilogue whose stores share this wave's vmcnt with
+// the DMAs, so it waits for everything outstanding.
+template <bool RES>
+__device__ __forceinline__ void run_stages(const Oz2Const* c, const Ctx& x, Dma& dm, uint8_t* LB,
+                                           uint32_t lds0, int it0, int n, bool drain,
+                                           v16f (&acc)[4][2]) {
   const int T = x.T;
   for (int it = it0; it < it0 + n; ++it) {
     // this wave's DMA share is 4 instructions per stage; stages it+1, it+2
     // may still be in flight
-    if (it + 2 < T) wait_vm<8>();
+    if (drain && it == it0) wait_vm<0>();
+    else if (it + 2 < T) wait_vm<8>();
     else if (it + 1 < T) wait_vm<4>();
     else wait_vm<0>();
     bar();
     v8i fa[4], fb[2];
     frags(LB + (it & 3) * STB, fa, fb);
-    if (it + 3 < T) issue_stage(x, dm, lds0 + ((it + 3) & 3) * STB);
+    if (it + 3 < T) issue_stage<RES>(c, x, dm, lds0 + ((it + 3) & 3) * STB);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -182,10 +206,11 @@ __device__ __forceinline__ void run_stages(const Ctx& x, Dma& dm, uint8_t* LB, u
   }
 }
 
-__device__ __forceinline__ void prologue(const Ctx& x, Dma& dm, uint32_t lds0) {
+template <bool RES>
+__device__ __forceinline__ void prologue(const Oz2Const* c, const Ctx& x, Dma& dm, uint32_t lds0) {
 #pragma unroll
   for (int t = 0; t < NB - 1; ++t)
-    if (t < x.T) issue_stage(x, dm, lds0 + t * STB);
+    if (t < x.T) issue_stage<RES>(c, x, dm, lds0 + t * STB);
 }
 
 // ------------------------------------------------------------- code GEMM
@@ -202,18 +227,20 @@ k_codegemm(const uint8_t* __restrict__ cA, const uint8_t* __restrict__ cB, int m
   Ctx x;
   x.kbA = (size_t)mp * KS;
   x.kbB = (size_t)np * KS;
-  x.aq[0] = x.aq[1] = x.aq[2] = cA + (size_t)tm * TILE * KS + (size_t)(kbeg / KS) * x.kbA;
-  x.bq[0] = x.bq[1] = x.bq[2] = cB + (size_t)tn * TILE * KS + (size_t)(kbeg / KS) * x.kbB;
+  x.a0 = cA + (size_t)tm * TILE * KS + (size_t)(kbeg / KS) * x.kbA;
+  x.b0 = cB + (size_t)tn * TILE * KS + (size_t)(kbeg / KS) * x.kbB;
+  x.psA = x.psB = 0;
   x.nk = (kend - kbeg) / KS;
   x.T = x.nk;
+  x.mi1 = 0;
   Dma dm = dma_init(x);
   v16f acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = v16f{0.f};
-  prologue(x, dm, lds0);
-  run_stages(x, dm, LB, lds0, 0, x.T, acc);
+  prologue<false>(nullptr, x, dm, lds0);
+  run_stages<false>(nullptr, x, dm, LB, lds0, 0, x.T, false, acc);
 
   // lane holds rows 32x + 8(e/4) + 4(lane/32) + e%4 of column 32y + lane%32
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -245,107 +272,118 @@ k_codegemm(const uint8_t* __restrict__ cA, const uint8_t* __restrict__ cB, int m
 }
 
 // ------------------------------------------------------------- residue GEMM
-// grid: (tiles, r).  One modulus per workgroup over k in [kbeg, kend).
+// grid: (tiles, ceil(r / mpw)).  Workgroup (t, g) computes moduli
+// g*mpw .. min(r, (g+1)*mpw) - 1 of tile t over k in [kbeg, kend), one after
+// the other on one accumulator set, as one continuous DMA stream.
 __global__ void __launch_bounds__(NT, 1)
 k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, int mp,
-          int np, int kp, int kbeg, int kend, int accumulate, int16_t* __restrict__ res) {
+          int np, int kp, int kbeg, int kend, int accumulate, int mpw, int16_t* __restrict__ res) {
   __shared__ __attribute__((aligned(16))) uint8_t LB[NB * STB];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)LB;
   const int ntm = mp / TILE, ntn = np / TILE;
-  const int tile = tile_of(blockIdx.x, ntm, ntn), mi = blockIdx.y;
+  const int tile = tile_of(blockIdx.x, ntm, ntn);
+  const int mi0 = blockIdx.y * mpw, mi1 = min(c.r, mi0 + mpw);
   const int tm = tile % ntm, tn = tile / ntm;
-  const int m = c.m[mi], s = c.sq[mi], pb = c.pbase[mi];
-  const float fm = (float)m, inv = c.finv[mi];
   Ctx x;
-  const size_t psA = (size_t)mp * kp, psB = (size_t)np * kp;
+  x.psA = (size_t)mp * kp;
+  x.psB = (size_t)np * kp;
   x.kbA = (size_t)mp * KS;
   x.kbB = (size_t)np * KS;
-  const uint8_t* a0 = PA + (size_t)pb * psA + (size_t)tm * TILE * KS + (size_t)(kbeg / KS) * x.kbA;
-  const uint8_t* b0 = PB + (size_t)pb * psB + (size_t)tn * TILE * KS + (size_t)(kbeg / KS) * x.kbB;
-#pragma unroll
-  for (int q = 0; q < 3; ++q) {
-    x.aq[q] = a0 + (size_t)planeA(s, q) * psA;
-    x.bq[q] = b0 + (size_t)planeB(s, q) * psB;
-  }
+  x.a0 = PA + (size_t)tm * TILE * KS + (size_t)(kbeg / KS) * x.kbA;
+  x.b0 = PB + (size_t)tn * TILE * KS + (size_t)(kbeg / KS) * x.kbB;
   x.nk = (kend - kbeg) / KS;
-  x.T = 3 * x.nk;
+  x.T = 3 * x.nk * (mi1 - mi0);
+  x.mi1 = mi1;
+  const int nk = x.nk;
   Dma dm = dma_init(x);
-  v16f acc[4][2];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = v16f{0.f};
+  dm.mi = mi0;
+  product_ptrs(&c, x, mi0, 0, dm);
+  prologue<true>(&c, x, dm, lds0);
 
-  // chain transitions: acc <- (acc - m rint(acc/m)) * rho.  The reduced value
-  // has magnitude <= m/2 + 3 (the fp32 quotient estimate is within 1 of the
-  // exact one), so |acc * rho| < 2^18 and the next pair keeps every partial
-  // sum below 2^24.  Square moduli: the two cross products share one chain
-  // (their sum is at most 512 k_slab = 2^24), then x s before d0e0.
-  // Nonsquare: d1e1, x rho0 = 240/(-15), d0e0, x rho1 = -15/16, (d0+d1)(e0+e1).
-  auto transition = [&](const float rho) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int it = 0;
+  for (int mi = mi0; mi < mi1; ++mi) {
+    const int m = c.m[mi], s = c.sq[mi];
+    const float fm = (float)m, inv = c.finv[mi];
+    v16f acc[4][2];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < 2; ++j) acc[i][j] = v16f{0.f};
+
+    // chain transitions: acc <- (acc - m rint(acc/m)) * rho.  The reduced
+    // value has magnitude <= m/2 + 3 (the fp32 quotient estimate is within 1
+    // of the exact one), so |acc * rho| < 2^18 and the next pair keeps every
+    // partial sum below 2^24.  Square moduli: the two cross products share
+    // one chain (their sum is at most 512 k_slab = 2^24), then x s before
+    // d0e0.  Nonsquare: d1e1, x rho0 = 240/(-15), d0e0, x rho1 = -15/16,
+    // (d0+d1)(e0+e1).
+    auto transition = [&](const float rho) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const float v = acc[i][j][e];
+            acc[i][j][e] = __builtin_fmaf(-rintf(v * inv), fm, v) * rho;
+          }
+    };
+    const bool drain = mi > mi0;
+    if (s) {
+      run_stages<true>(&c, x, dm, LB, lds0, it, 2 * nk, drain, acc);
+      transition((float)s);
+      run_stages<true>(&c, x, dm, LB, lds0, it + 2 * nk, nk, false, acc);
+    } else {
+      run_stages<true>(&c, x, dm, LB, lds0, it, nk, drain, acc);
+      transition((float)c.rho0[mi]);
+      run_stages<true>(&c, x, dm, LB, lds0, it + nk, nk, false, acc);
+      transition((float)c.rho1[mi]);
+      run_stages<true>(&c, x, dm, LB, lds0, it + 2 * nk, nk, false, acc);
+    }
+    it += 3 * nk;
+
+    // epilogue: centred residue of fin * acc (+ the previous slab's), in
+    // fp32 throughout.  acc is an integer with |acc| <= 2^24 and fin is 1 or
+    // 16, so v = fin * acc is exact.  v * RN(1/m) is within
+    // 2 * 2^-24 |v| / m <= 32 / m of v / m (the relative errors of RN(1/m)
+    // and of the product), so v - m rint(.) is an exact integer of magnitude
+    // <= m/2 + 32 < m (every modulus exceeds 64); centre_small then rounds
+    // once more, now exactly.
+    const float ffin = (float)c.fin[mi];
+    const float hm = (m & 1) ? 0.5f : 0.5f * fm;   // even m: +m/2 is not canonical
+    int16_t* dst = res + (size_t)mi * mp * np + (size_t)tile * (TILE * TILE) + (size_t)w * 8192 +
+                   lane * 16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        float r16[16];
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const float v = acc[i][j][e];
-          acc[i][j][e] = __builtin_fmaf(-rintf(v * inv), fm, v) * rho;
+          const float v = acc[i][j][e] * ffin;
+          r16[e] = centre_small(__builtin_fmaf(-rintf(v * inv), fm, v), fm, inv, hm);
         }
-  };
-  prologue(x, dm, lds0);
-  if (s) {
-    run_stages(x, dm, LB, lds0, 0, 2 * x.nk, acc);
-    transition((float)s);
-    run_stages(x, dm, LB, lds0, 2 * x.nk, x.nk, acc);
-  } else {
-    run_stages(x, dm, LB, lds0, 0, x.nk, acc);
-    transition((float)c.rho0[mi]);
-    run_stages(x, dm, LB, lds0, x.nk, x.nk, acc);
-    transition((float)c.rho1[mi]);
-    run_stages(x, dm, LB, lds0, 2 * x.nk, x.nk, acc);
+        uint4* p = reinterpret_cast<uint4*>(dst + (i * 2 + j) * 1024);
+        if (accumulate) {
+          const uint4 o0 = p[0], o1 = p[1];
+          const uint32_t ow[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int old = (int)(int16_t)((ow[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
+            r16[e] = centre_small(r16[e] + (float)old, fm, inv, hm);
+          }
+        }
+        uint32_t pk[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          pk[e] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pk_i16((int)r16[2 * e],
+                                                                           (int)r16[2 * e + 1]));
+        p[0] = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+        p[1] = make_uint4(pk[4], pk[5], pk[6], pk[7]);
+      }
   }
   wait_vm<0>();
-
-  // final epilogue: centred residue of fin * acc (+ the previous slab's),
-  // in fp32 throughout.  acc is an integer with |acc| <= 2^24 and fin is 1 or
-  // 16, so v = fin * acc is exact.  v * RN(1/m) is within 2 * 2^-24 |v| / m
-  // <= 32 / m of v / m (the relative errors of RN(1/m) and of the product),
-  // so v - m rint(.) is an exact integer of magnitude <= m/2 + 32 < m (every
-  // modulus exceeds 64); centre_small then rounds once more, now exactly.
-  const float ffin = (float)c.fin[mi];
-  const float hm = (m & 1) ? 0.5f : 0.5f * fm;   // even m: +m/2 is not canonical
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int16_t* dst = res + (size_t)mi * mp * np + (size_t)tile * (TILE * TILE) + (size_t)w * 8192 +
-                 lane * 16;
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      float r16[16];
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float v = acc[i][j][e] * ffin;
-        r16[e] = centre_small(__builtin_fmaf(-rintf(v * inv), fm, v), fm, inv, hm);
-      }
-      uint4* p = reinterpret_cast<uint4*>(dst + (i * 2 + j) * 1024);
-      if (accumulate) {
-        const uint4 o0 = p[0], o1 = p[1];
-        const uint32_t ow[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int old = (int)(int16_t)((ow[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
-          r16[e] = centre_small(r16[e] + (float)old, fm, inv, hm);
-        }
-      }
-      uint32_t pk[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        pk[e] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pk_i16((int)r16[2 * e],
-                                                                         (int)r16[2 * e + 1]));
-      p[0] = make_uint4(pk[0], pk[1], pk[2], pk[3]);
-      p[1] = make_uint4(pk[4], pk[5], pk[6], pk[7]);
-    }
 }
 
 }  // namespace
@@ -359,11 +397,24 @@ hipError_t oz2_launch_codegemm(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws
 
 hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
                               uint8_t* ws, hipStream_t s) {
-  dim3 grid((d.mp / TILE) * (d.np / TILE), c.r);
+  // moduli per workgroup: all r when the tiles alone fill the device (one
+  // resident workgroup per CU), else split so tiles x groups still covers it
+  static int cus = 0;
+  if (!cus) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      cus = 256;
+  }
+  const int tiles = (d.mp / TILE) * (d.np / TILE);
+  const int groups = std::min(c.r, (cus + tiles - 1) / tiles);
+  const int mpw = (c.r + groups - 1) / groups;
+  dim3 grid(tiles, (c.r + mpw - 1) / mpw);
   for (int kb = 0, sl = 0; kb < d.kp; kb += OZ2_KSLAB, ++sl) {
     const int ke = kb + OZ2_KSLAB < d.kp ? kb + OZ2_KSLAB : d.kp;
     hipLaunchKernelGGL(k_resgemm, grid, dim3(NT), 0, s, c, ws + L.planesA, ws + L.planesB, d.mp,
-                       d.np, d.kp, kb, ke, sl > 0 ? 1 : 0, (int16_t*)(ws + L.res));
+                       d.np, d.kp, kb, ke, sl > 0 ? 1 : 0, mpw, (int16_t*)(ws + L.res));
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -26,7 +26,7 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, n), n
     assert sorted(_lib.EXPORTS) == names
     probes = _declared("ozaki2_probes.h")
-    assert len(probes) == 5
+    assert len(probes) == 6
     for n in probes:
         assert hasattr(L, n), n
     assert sorted(_lib.PROBE_EXPORTS) == probes
@@ -43,6 +43,8 @@ def test_probe_argument_checks():
         oz.ozaki2_probe_copy(16, 32, 15, 0)           # size not a multiple of 16
     with pytest.raises(oz.Ozaki2Error):
         oz.ozaki2_probe_mfma_peak(0)
+    with pytest.raises(oz.Ozaki2Error):
+        oz.ozaki2_probe_mfma_digits(3)                # odd iteration count
     with pytest.raises(oz.Ozaki2Error):
         oz.ozaki2_probe_copy_peak(1 << 20, 1)         # below 16 MiB
 

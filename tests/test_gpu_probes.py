@@ -100,5 +100,7 @@ def test_copy_probe_and_peaks(torch_cuda):
     assert torch.equal(src, dst)
     gbs = oz.ozaki2_probe_copy_peak(256 << 20, 3)
     tf = oz.ozaki2_probe_mfma_peak(200)
+    td = oz.ozaki2_probe_mfma_digits(2000)
     assert 500 < gbs < 8200          # at most the 8 TB/s datasheet figure
     assert 500 < tf < 5100           # at most the 5 PF dense FP8 figure
+    assert 500 < td < 5100
