@@ -269,6 +269,14 @@ __global__ void k_plane_tables(Oz2Const c, uint32_t* tab) {
   tab[idx] = ((uint32_t)lo & 0xFFFFu) | (((uint32_t)hi & 0xFFu) << 16);
 }
 
+// Plane bytes are written once and read back only by the residue GEMMs, after
+// the other operand's split: non-temporal stores keep them from displacing
+// that operand's FP64 input in the caches while it waits to be re-read.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void store_stream(uint8_t* p, uint4 v) {
+  __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, reinterpret_cast<u32x4*>(p));
+}
+
 // Quantise (Eq. (scale)) and split into E4M3 digit planes.  A persistent-style
 // grid walks the 64x64 tiles; each workgroup first copies the residue->bytes
 // tables (sum of the moduli entries, <= 42 KiB) into LDS.
@@ -321,15 +329,15 @@ __global__ void __launch_bounds__(256) k_split(Oz2Const c, const double* __restr
       v1.y = gather_byte(e[4], e[5], e[6], e[7], 0x05010501u);
       v1.z = gather_byte(e[8], e[9], e[10], e[11], 0x05010501u);
       v1.w = gather_byte(e[12], e[13], e[14], e[15], 0x05010501u);
-      *reinterpret_cast<uint4*>(dst) = v0;
-      *reinterpret_cast<uint4*>(dst + pstride) = v1;
+      store_stream(dst, v0);
+      store_stream(dst + pstride, v1);
       if (!c.sq[i]) {
         uint4 v2;
         v2.x = gather_byte(e[0], e[1], e[2], e[3], 0x05010602u);
         v2.y = gather_byte(e[4], e[5], e[6], e[7], 0x05010602u);
         v2.z = gather_byte(e[8], e[9], e[10], e[11], 0x05010602u);
         v2.w = gather_byte(e[12], e[13], e[14], e[15], 0x05010602u);
-        *reinterpret_cast<uint4*>(dst + 2 * pstride) = v2;
+        store_stream(dst + 2 * pstride, v2);
       }
     }
   }

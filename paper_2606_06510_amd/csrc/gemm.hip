@@ -178,19 +178,19 @@ __device__ __forceinline__ float centre_small(float x, float fm, float inv, floa
   return r == hm ? -hm : r;
 }
 
-// Main loop over stages [it0, it0 + n) of the stage sequence.  drain: the
-// first of them follows an epilogue whose stores share this wave's vmcnt with
-// the DMAs, so it waits for everything outstanding.
+// Main loop over stages [it0, it0 + n) of the stage sequence.  Stages below
+// `landed` are known to be in LDS already (this wave waited for all its DMAs
+// before the epilogue stores that now share its vmcnt), so they skip the wait.
 template <bool RES>
 __device__ __forceinline__ void run_stages(const Oz2Const* c, const Ctx& x, Dma& dm, uint8_t* LB,
-                                           uint32_t lds0, int it0, int n, bool drain,
+                                           uint32_t lds0, int it0, int n, int landed,
                                            v16f (&acc)[4][2]) {
   const int T = x.T;
   for (int it = it0; it < it0 + n; ++it) {
     // this wave's DMA share is 4 instructions per stage; stages it+1, it+2
     // may still be in flight
-    if (drain && it == it0) wait_vm<0>();
-    else if (it + 2 < T) wait_vm<8>();
+    if (it < landed) {
+    } else if (it + 2 < T) wait_vm<8>();
     else if (it + 1 < T) wait_vm<4>();
     else wait_vm<0>();
     bar();
@@ -240,7 +240,7 @@ k_codegemm(const uint8_t* __restrict__ cA, const uint8_t* __restrict__ cB, int m
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = v16f{0.f};
   prologue<false>(nullptr, x, dm, lds0);
-  run_stages<false>(nullptr, x, dm, LB, lds0, 0, x.T, false, acc);
+  run_stages<false>(nullptr, x, dm, LB, lds0, 0, x.T, 0, acc);
 
   // lane holds rows 32x + 8(e/4) + 4(lane/32) + e%4 of column 32y + lane%32
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -301,7 +301,7 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
   prologue<true>(&c, x, dm, lds0);
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int it = 0;
+  int it = 0, landed = 0;
   for (int mi = mi0; mi < mi1; ++mi) {
     const int m = c.m[mi], s = c.sq[mi];
     const float fm = (float)m, inv = c.finv[mi];
@@ -329,17 +329,16 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
             acc[i][j][e] = __builtin_fmaf(-rintf(v * inv), fm, v) * rho;
           }
     };
-    const bool drain = mi > mi0;
     if (s) {
-      run_stages<true>(&c, x, dm, LB, lds0, it, 2 * nk, drain, acc);
+      run_stages<true>(&c, x, dm, LB, lds0, it, 2 * nk, landed, acc);
       transition((float)s);
-      run_stages<true>(&c, x, dm, LB, lds0, it + 2 * nk, nk, false, acc);
+      run_stages<true>(&c, x, dm, LB, lds0, it + 2 * nk, nk, landed, acc);
     } else {
-      run_stages<true>(&c, x, dm, LB, lds0, it, nk, drain, acc);
+      run_stages<true>(&c, x, dm, LB, lds0, it, nk, landed, acc);
       transition((float)c.rho0[mi]);
-      run_stages<true>(&c, x, dm, LB, lds0, it + nk, nk, false, acc);
+      run_stages<true>(&c, x, dm, LB, lds0, it + nk, nk, landed, acc);
       transition((float)c.rho1[mi]);
-      run_stages<true>(&c, x, dm, LB, lds0, it + 2 * nk, nk, false, acc);
+      run_stages<true>(&c, x, dm, LB, lds0, it + 2 * nk, nk, landed, acc);
     }
     it += 3 * nk;
 
@@ -354,6 +353,7 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
     const float hm = (m & 1) ? 0.5f : 0.5f * fm;   // even m: +m/2 is not canonical
     int16_t* dst = res + (size_t)mi * mp * np + (size_t)tile * (TILE * TILE) + (size_t)w * 8192 +
                    lane * 16;
+    uint32_t pk[4][2][8];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -364,8 +364,8 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
           const float v = acc[i][j][e] * ffin;
           r16[e] = centre_small(__builtin_fmaf(-rintf(v * inv), fm, v), fm, inv, hm);
         }
-        uint4* p = reinterpret_cast<uint4*>(dst + (i * 2 + j) * 1024);
         if (accumulate) {
+          const uint4* p = reinterpret_cast<const uint4*>(dst + (i * 2 + j) * 1024);
           const uint4 o0 = p[0], o1 = p[1];
           const uint32_t ow[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
 #pragma unroll
@@ -374,13 +374,23 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
             r16[e] = centre_small(r16[e] + (float)old, fm, inv, hm);
           }
         }
-        uint32_t pk[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-          pk[e] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pk_i16((int)r16[2 * e],
-                                                                           (int)r16[2 * e + 1]));
-        p[0] = make_uint4(pk[0], pk[1], pk[2], pk[3]);
-        p[1] = make_uint4(pk[4], pk[5], pk[6], pk[7]);
+          pk[i][j][e] = __builtin_bit_cast(
+              uint32_t, __builtin_amdgcn_cvt_pk_i16((int)r16[2 * e], (int)r16[2 * e + 1]));
+      }
+    // Every DMA issued so far (the next modulus's first stages, up to three)
+    // has landed before the stores go out; those stages then skip their wait,
+    // and the wait of the stage after them also covers the stores.
+    wait_vm<0>();
+    landed = it + 3;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        uint4* p = reinterpret_cast<uint4*>(dst + (i * 2 + j) * 1024);
+        p[0] = make_uint4(pk[i][j][0], pk[i][j][1], pk[i][j][2], pk[i][j][3]);
+        p[1] = make_uint4(pk[i][j][4], pk[i][j][5], pk[i][j][6], pk[i][j][7]);
       }
   }
   wait_vm<0>();
