@@ -213,6 +213,20 @@ __device__ __forceinline__ void prologue(const Oz2Const* c, const Ctx& x, Dma& d
     if (t < x.T) issue_stage<RES>(c, x, dm, lds0 + t * STB);
 }
 
+// One step of a halving max-butterfly across lanes L and L^B: of the first N
+// entries of u, lane L keeps the half selected by bit B of L (upper when set),
+// maximised with the partner's copy of that half, in u[0 .. N/2).
+template <int N, int B>
+__device__ __forceinline__ void halve(float (&u)[64], int lane) {
+  const bool up = (lane & B) != 0;
+#pragma unroll
+  for (int k = 0; k < N / 2; ++k) {
+    const float keep = up ? u[k + N / 2] : u[k];
+    const float send = up ? u[k] : u[k + N / 2];
+    u[k] = fmaxf(keep, __shfl_xor(send, B));
+  }
+}
+
 // ------------------------------------------------------------- code GEMM
 // grid: (tiles, code slabs).  G'[i][j] <= 256 * 65536 = 2^24: exact in FP32.
 __global__ void __launch_bounds__(NT, 1)
@@ -242,23 +256,22 @@ k_codegemm(const uint8_t* __restrict__ cA, const uint8_t* __restrict__ cB, int m
   prologue<false>(nullptr, x, dm, lds0);
   run_stages<false>(nullptr, x, dm, LB, lds0, 0, x.T, 0, acc);
 
-  // lane holds rows 32x + 8(e/4) + 4(lane/32) + e%4 of column 32y + lane%32
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int row0 = tm * TILE + (w >> 2) * 128, col0 = tn * TILE + (w & 3) * 64;
+  // Row and column maxima of G'.  Lane L holds rows 32i + 8(e/4) + 4(L/32) +
+  // e%4 (of the wave's 128) in column 32j + L%32 (of its 64).
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wr = w >> 2, wc = w & 3;
+  float u[64];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      float v = fmaxf(acc[i][0][e], acc[i][1][e]);
-      v = fmaxf(v, __shfl_xor(v, 1));
-      v = fmaxf(v, __shfl_xor(v, 2));
-      v = fmaxf(v, __shfl_xor(v, 4));
-      v = fmaxf(v, __shfl_xor(v, 8));
-      v = fmaxf(v, __shfl_xor(v, 16));
-      if ((lane & 31) == 0)
-        atomicMax(Rmax + (size_t)slab * mp + row0 + 32 * i + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3),
-                  (uint32_t)v);
-    }
+    for (int e = 0; e < 16; ++e) u[16 * i + e] = fmaxf(acc[i][0][e], acc[i][1][e]);
+  // halving butterfly over the 32 lanes of each half: lane L keeps entries
+  // 2(L%32) and 2(L%32) + 1 of u, maximised over its half
+  halve<64, 16>(u, lane);
+  halve<32, 8>(u, lane);
+  halve<16, 4>(u, lane);
+  halve<8, 2>(u, lane);
+  halve<4, 1>(u, lane);
+  float cmax[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     float v = acc[0][j][0];
@@ -266,8 +279,35 @@ k_codegemm(const uint8_t* __restrict__ cA, const uint8_t* __restrict__ cB, int m
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int e = 0; e < 16; ++e) v = fmaxf(v, acc[i][j][e]);
-    v = fmaxf(v, __shfl_xor(v, 32));
-    if (lane < 32) atomicMax(Kmax + (size_t)slab * np + col0 + 32 * j + lane, (uint32_t)v);
+    cmax[j] = fmaxf(v, __shfl_xor(v, 32));   // column 32j + L%32 over the wave's rows
+  }
+  // combine the 4 waves sharing rows and the 2 sharing columns in LDS (the
+  // ring is free once every wave is past its last stage), then one atomic per
+  // row and per column of the tile
+  float* red = reinterpret_cast<float*>(LB);   // [wr][wc][128] row maxima
+  float* cred = red + 1024;                    // [wr][wc][64] column maxima
+  bar();
+  const int h = lane >> 5, q = lane & 31;
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int ie = 2 * q + t, i = ie >> 4, e = ie & 15;
+    red[(wr * 4 + wc) * 128 + 32 * i + 8 * (e >> 2) + 4 * h + (e & 3)] = u[t];
+  }
+  if (lane < 32) {
+    cred[(wr * 4 + wc) * 64 + lane] = cmax[0];
+    cred[(wr * 4 + wc) * 64 + 32 + lane] = cmax[1];
+  }
+  __syncthreads();
+  const int t = threadIdx.x;
+  if (t < 256) {
+    const int r = t >> 7, row = t & 127;
+    const float* p = red + r * 512 + row;
+    const float v = fmaxf(fmaxf(p[0], p[128]), fmaxf(p[256], p[384]));
+    atomicMax(Rmax + (size_t)slab * mp + tm * TILE + t, (uint32_t)v);
+  } else {
+    const int col = t - 256, c4 = col >> 6, cc = col & 63;
+    const float v = fmaxf(cred[c4 * 64 + cc], cred[(4 + c4) * 64 + cc]);
+    atomicMax(Kmax + (size_t)slab * np + tn * TILE + col, (uint32_t)v);
   }
 }
 
