@@ -232,3 +232,22 @@ def test_moduli_per_workgroup_grids(shape, r):
     del plan, Ad, Bd, Cd
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+
+
+def test_subnormal_and_overflowing_results():
+    """Rows and columns scaled so that one block of C lies in the subnormal
+    range and another overflows: the GPU's gradual-underflow rounding path and
+    the overflow to infinity are bit-exact against the oracle."""
+    m, n, k = 96, 80, 200
+    A, B = synth.lognormal(m, n, k, seed=321)
+    A = A.copy()
+    B = B.copy()
+    A[:32] *= 2.0 ** -560
+    A[64:] *= 2.0 ** 520
+    B[:, :24] *= 2.0 ** -500
+    B[:, 56:] *= 2.0 ** 520
+    res = oracle.dgemm(A, B, 12)
+    assert ((res.C != 0) & (np.abs(res.C) < 2.0 ** -1022)).sum() == 32 * 24
+    assert np.isinf(res.C).sum() == 32 * 24
+    plan, C = run_staged(A, B, 12)
+    compare_all(plan, C, A, B, 12, res)
