@@ -171,12 +171,62 @@ __device__ __forceinline__ void take_cols(const double* tile, bool zero, double 
   }
 }
 
-template <bool TRANS>
-__global__ void __launch_bounds__(256) k_codes(const double* __restrict__ X, int ld, int rows,
-                                               int nrb, int k, int kp,
-                                               const unsigned long long* __restrict__ bits,
-                                               uint8_t* __restrict__ codes, unsigned vec) {
-  __shared__ __attribute__((aligned(16))) double tile[TRANS ? 2 : 64 * TPITCH];
+// Codes of A (rows contiguous in memory).  A tile of 64 rows x 64 k per
+// workgroup: thread t reads rows 2(t%32), 2(t%32)+1 of columns t/32 + 8j with
+// 16-byte loads (each wave instruction covers 512 contiguous bytes of two
+// columns), converts them to code bytes, and the 64 x 64 bytes are transposed
+// through LDS so that each thread stores 16 consecutive k of one row.
+__global__ void __launch_bounds__(256) k_codes_rows(const double* __restrict__ X, int ld, int rows,
+                                                    int nrb, int k, int kp,
+                                                    const unsigned long long* __restrict__ bits,
+                                                    uint8_t* __restrict__ codes, unsigned vec) {
+  __shared__ __attribute__((aligned(16))) uint8_t T[64][80];
+  const int rows_pad = nrb * 64;
+  const int t = threadIdx.x;
+  const int bx = (int)(blockIdx.x % (unsigned)nrb), by = (int)(blockIdx.x / (unsigned)nrb);
+  const int p = t & 31, g = t >> 5;
+  const int r0 = bx * 64 + 2 * p, lbase = by * 64;
+  const unsigned long long b0 = r0 < rows ? bits[r0] : 0ull;
+  const unsigned long long b1 = r0 + 1 < rows ? bits[r0 + 1] : 0ull;
+  const bool z0 = b0 >= kInfBits, z1 = b1 >= kInfBits;   // T1 rows: codes 0
+  const int E0 = (b0 == 0 || z0) ? 0 : exp_of_bits(b0);
+  const int E1 = (b1 == 0 || z1) ? 0 : exp_of_bits(b1);
+  double2 v[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int l = lbase + g + 8 * j;
+    v[j] = make_double2(0.0, 0.0);
+    if (l < k) {
+      const double* q = X + (size_t)l * ld + r0;
+      if (vec && r0 + 1 < rows) {
+        v[j] = *reinterpret_cast<const double2*>(q);
+      } else {
+        if (r0 < rows) v[j].x = q[0];
+        if (r0 + 1 < rows) v[j].y = q[1];
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int c = g + 8 * j;
+    const float c0 = z0 ? 0.0f : code_of(v[j].x, E0);
+    const float c1 = z1 ? 0.0f : code_of(v[j].y, E1);
+    const uint32_t w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c0, c1, 0, false);
+    T[2 * p][c] = (uint8_t)(w & 0xFFu);
+    T[2 * p + 1][c] = (uint8_t)((w >> 8) & 0xFFu);
+  }
+  __syncthreads();
+  const int row = bx * 64 + (t >> 2), l0 = lbase + (t & 3) * 16;
+  const uint4 o = *reinterpret_cast<const uint4*>(&T[t >> 2][(t & 3) * 16]);
+  *reinterpret_cast<uint4*>(codes + kblocked(row, l0, rows_pad)) = o;
+}
+
+// Codes of B (columns contiguous): 64 columns x 64 k staged through LDS.
+__global__ void __launch_bounds__(256) k_codes_cols(const double* __restrict__ X, int ld, int rows,
+                                                    int nrb, int k, int kp,
+                                                    const unsigned long long* __restrict__ bits,
+                                                    uint8_t* __restrict__ codes, unsigned vec) {
+  __shared__ __attribute__((aligned(16))) double tile[64 * TPITCH];
   const int rows_pad = nrb * 64;
   int row, l0;
   seg_coords(blockIdx.x, nrb, row, l0);
@@ -184,14 +234,10 @@ __global__ void __launch_bounds__(256) k_codes(const double* __restrict__ X, int
   bool t1 = b >= kInfBits;
   int E = (b == 0 || t1) ? 0 : exp_of_bits(b);
   double x[16];
-  if (TRANS) {
-    load_seg<TRANS>(X, ld, rows, k, row, l0, t1, x);
-  } else {
-    const int bx = (int)(blockIdx.x % (unsigned)nrb), by = (int)(blockIdx.x / (unsigned)nrb);
-    stage_cols(X, ld, rows, k, bx * 64, by * 64, vec != 0, tile);
-    __syncthreads();
-    take_cols(tile, t1, x);
-  }
+  const int bx = (int)(blockIdx.x % (unsigned)nrb), by = (int)(blockIdx.x / (unsigned)nrb);
+  stage_cols(X, ld, rows, k, bx * 64, by * 64, vec != 0, tile);
+  __syncthreads();
+  take_cols(tile, t1, x);
   uint32_t w[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q)
@@ -383,13 +429,14 @@ hipError_t oz2_launch_codes(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, c
                             int lda, const double* B, int ldb, int side, hipStream_t s) {
   if (side & OZ2_SIDE_A) {
     dim3 ga((d.mp / 64) * (d.kp / 64));
-    hipLaunchKernelGGL(k_codes<true>, ga, dim3(256), 0, s, A, lda, d.m, d.mp / 64, d.k, d.kp,
-                       (const unsigned long long*)(ws + L.rowbits), ws + L.codesA, 0u);
+    const unsigned vecA = ((uintptr_t)A % 16 == 0 && lda % 2 == 0) ? 1u : 0u;
+    hipLaunchKernelGGL(k_codes_rows, ga, dim3(256), 0, s, A, lda, d.m, d.mp / 64, d.k, d.kp,
+                       (const unsigned long long*)(ws + L.rowbits), ws + L.codesA, vecA);
   }
   if (side & OZ2_SIDE_B) {
     dim3 gb((d.np / 64) * (d.kp / 64));
     const unsigned vecB = ((uintptr_t)B % 16 == 0 && ldb % 2 == 0) ? 1u : 0u;
-    hipLaunchKernelGGL(k_codes<false>, gb, dim3(256), 0, s, B, ldb, d.n, d.np / 64, d.k, d.kp,
+    hipLaunchKernelGGL(k_codes_cols, gb, dim3(256), 0, s, B, ldb, d.n, d.np / 64, d.k, d.kp,
                        (const unsigned long long*)(ws + L.colbits), ws + L.codesB, vecB);
   }
   return hipGetLastError();
