@@ -221,30 +221,44 @@ __global__ void __launch_bounds__(256) k_codes_rows(const double* __restrict__ X
   *reinterpret_cast<uint4*>(codes + kblocked(row, l0, rows_pad)) = o;
 }
 
-// Codes of B (columns contiguous): 64 columns x 64 k staged through LDS.
+// Codes of B (columns contiguous).  A tile of 64 columns x 64 k per
+// workgroup: thread t reads k 2(t%32), 2(t%32)+1 of columns t/32 + 8j with
+// 16-byte loads (512 contiguous bytes of one column per half-wave
+// instruction); the code bytes are transposed through LDS as for A.
 __global__ void __launch_bounds__(256) k_codes_cols(const double* __restrict__ X, int ld, int rows,
                                                     int nrb, int k, int kp,
                                                     const unsigned long long* __restrict__ bits,
                                                     uint8_t* __restrict__ codes, unsigned vec) {
-  __shared__ __attribute__((aligned(16))) double tile[64 * TPITCH];
+  __shared__ __attribute__((aligned(16))) uint8_t T[64][80];
   const int rows_pad = nrb * 64;
-  int row, l0;
-  seg_coords(blockIdx.x, nrb, row, l0);
-  unsigned long long b = row < rows ? bits[row] : 0ull;
-  bool t1 = b >= kInfBits;
-  int E = (b == 0 || t1) ? 0 : exp_of_bits(b);
-  double x[16];
+  const int t = threadIdx.x;
   const int bx = (int)(blockIdx.x % (unsigned)nrb), by = (int)(blockIdx.x / (unsigned)nrb);
-  stage_cols(X, ld, rows, k, bx * 64, by * 64, vec != 0, tile);
-  __syncthreads();
-  take_cols(tile, t1, x);
-  uint32_t w[4];
+  const int kk = 2 * (t & 31), g = t >> 5;
+  const int l = by * 64 + kk;
 #pragma unroll
-  for (int q = 0; q < 4; ++q)
-    w[q] = pack4_fp8(code_of(x[4 * q], E), code_of(x[4 * q + 1], E), code_of(x[4 * q + 2], E),
-                     code_of(x[4 * q + 3], E));
-  uint4 v = make_uint4(w[0], w[1], w[2], w[3]);
-  *reinterpret_cast<uint4*>(codes + kblocked(row, l0, rows_pad)) = v;
+  for (int j = 0; j < 8; ++j) {
+    const int cc = g + 8 * j, col = bx * 64 + cc;
+    const unsigned long long b = col < rows ? bits[col] : 0ull;
+    const bool z = b >= kInfBits;   // T1 columns: codes 0
+    const int E = (b == 0 || z) ? 0 : exp_of_bits(b);
+    double2 v = make_double2(0.0, 0.0);
+    if (col < rows && !z) {
+      const double* q = X + (size_t)col * ld + l;
+      if (vec && l + 1 < k) {
+        v = *reinterpret_cast<const double2*>(q);
+      } else {
+        if (l < k) v.x = q[0];
+        if (l + 1 < k) v.y = q[1];
+      }
+    }
+    const uint32_t w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(code_of(v.x, E), code_of(v.y, E), 0,
+                                                                 false);
+    *reinterpret_cast<uint16_t*>(&T[cc][kk]) = (uint16_t)(w & 0xFFFFu);
+  }
+  __syncthreads();
+  const int row = bx * 64 + (t >> 2), l0 = by * 64 + (t & 3) * 16;
+  const uint4 o = *reinterpret_cast<const uint4*>(&T[t >> 2][(t & 3) * 16]);
+  *reinterpret_cast<uint4*>(codes + kblocked(row, l0, rows_pad)) = o;
 }
 
 __global__ void k_scales(Oz2Dims d, const unsigned long long* __restrict__ rowbits,
