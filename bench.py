@@ -41,6 +41,10 @@ def parse():
     ap.add_argument("--no-probes", action="store_true", help="skip the measured-peak probes")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB copy kernel (rocprofv3 counter calibration)")
+    ap.add_argument("--stationary", action="store_true",
+                    help="operand-stationary use (Mode P): A deconstructed once under fixed "
+                         "scaling, each step deconstructs a new B and runs the residue GEMMs "
+                         "and the reconstruction")
     ap.add_argument("--accuracy-sweep", action="store_true",
                     help="instead of the bench line: max componentwise error of a sampled set "
                          "of outputs against the exact product for r = 8..16")
@@ -97,6 +101,9 @@ def main():
     n = B.shape[1]
     if args.accuracy_sweep:
         accuracy_sweep(A, B, dev)
+        return
+    if args.stationary:
+        stationary_line(args, cfg, r, dev, A, B)
         return
     Ad = oz.to_device_colmajor(A, dev)
     Bd = oz.to_device_colmajor(B, dev)
@@ -227,6 +234,74 @@ def main():
     print(json.dumps(out))
 
 
+def stationary_line(args, cfg, r, dev, A, B):
+    """Operand-stationary workload (the paper's Mode P for a dense operand):
+    a fixed-scale plan keeps A's planes; each timed step deconstructs a new B
+    (two B matrices alternate), then runs the residue GEMMs and the
+    reconstruction."""
+    import torch
+    import paper_2606_06510_amd as oz
+    m, k = A.shape
+    n = B.shape[1]
+    B2 = np.ascontiguousarray(B[:, ::-1])
+    Ad = oz.to_device_colmajor(A, dev)
+    Bds = [oz.to_device_colmajor(B, dev), oz.to_device_colmajor(B2, dev)]
+    Cd = oz.colmajor_empty(m, n, device=dev)
+    plan = oz.Plan(m, n, k, r, oz.OZ2_SCALE_FIXED, device=dev)
+    plan.deconstruct(Ad, Bds[0])
+    stream = torch.cuda.current_stream()
+
+    def step(i, ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        plan.deconstruct_b(Bds[i & 1])
+        if ev is not None:
+            ev[1].record(stream)
+        plan.residue_gemm()
+        if ev is not None:
+            ev[2].record(stream)
+        plan.reconstruct(Cd)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, events[i])
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    dec = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
+    gem = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
+    rec = float(np.mean([e[2].elapsed_time(e[3]) for e in events]))
+    flop = 2.0 * m * n * k
+    fp8_flop = 3 * r * flop
+    achieved = fp8_flop / (gem * 1e-3) / 1e12
+    Blast = B if ((args.warmup + args.steps - 1) & 1) == 0 else B2
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(A, Blast, r, Cd, min(args.cpu_sample, 256), mode="fixed")
+    print(json.dumps({
+        "metric": "effective FP64 TFLOPS of emulated DGEMM, operand-stationary "
+                  "(A's planes kept, fixed scaling)",
+        "value": round(flop / (ms_step * 1e-3) / 1e12, 3), "unit": "TFLOPS", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "fp8-e4m3 MFMA -> exact int -> f64", "data": "synthetic (seeded numpy PCG64)",
+        "config": {"workload": f"{args.config} operand-stationary: C = A B_t, m={m} n={n} k={k}, "
+                               f"r={r} moduli (alpha={3 * r}), new B each step",
+                   "m": m, "n": n, "k": k, "num_moduli": r},
+        "roofline": {"bound": "mfma", "kernel": "k_resgemm (residue GEMMs, 3r FP8 products)",
+                     "achieved": round(achieved, 2), "peak": FP8_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
+                     "traffic": None},
+        "stages_ms": {"deconstruct_b": round(dec, 4), "residue_gemm": round(gem, 4),
+                      "reconstruct": round(rec, 4)},
+        "cpu_baseline": cpu}))
+
+
 def accuracy_sweep(A, B, dev):
     """Max componentwise error |C - AB| / (|A||B|) over 256 sampled outputs
     (exact error by compensated summation) for every moduli count."""
@@ -307,7 +382,7 @@ def plan_pstore(r):
     return sum(2 if int(round(x ** 0.5)) ** 2 == x else 3 for x in ms)
 
 
-def cpu_baseline(A, B, r, Cd, nsamp):
+def cpu_baseline(A, B, r, Cd, nsamp, mode="bound"):
     """The oracle, as it stands, on a bounded sample: nsamp sampled rows x nsamp
     sampled columns of the same workload (the scales of a sampled row need its
     code product against all of B, as the method does)."""
@@ -325,7 +400,7 @@ def cpu_baseline(A, B, r, Cd, nsamp):
     rows = np.sort(rng.choice(m, size=min(nsamp, m), replace=False))
     cols = np.sort(rng.choice(n, size=min(nsamp, n), replace=False))
     t = time.perf_counter()
-    res = oracle.dgemm(A, B, r, rows=rows, cols=cols)
+    res = oracle.dgemm(A, B, r, rows=rows, cols=cols, mode=mode)
     dt = time.perf_counter() - t
     C = oz.from_device_colmajor(Cd)[np.ix_(rows, cols)]
     same = int(np.sum(C.view(np.uint64) == res.C.view(np.uint64)))

@@ -113,6 +113,21 @@ int ozaki2_plan_destroy(ozaki2_plan_t plan);
 int ozaki2_deconstruct(ozaki2_plan_t plan, const double* A, int lda,
                        const double* B, int ldb, void* stream);
 
+/* Operand-stationary use (the paper's Mode P, deferred deconstruction of a
+ * fixed operand, here for a dense one): re-run phase 1 for one operand only
+ * and keep the other operand's planes, scales and flags from an earlier
+ * ozaki2_deconstruct / ozaki2_deconstruct_a / ozaki2_deconstruct_b of this
+ * plan.  Only for plans created with OZ2_SCALE_FIXED, where the scale of a row
+ * of A depends on A alone and that of a column of B on B alone (no
+ * max-magnitude pass); the results are then those of ozaki2_deconstruct on
+ * the same pair.  Returns OZ2_E_INVALID for a plan without OZ2_SCALE_FIXED, a
+ * null pointer or lda < max(1, m) / ldb < max(1, k).  ozaki2_residue_gemm
+ * needs both operands deconstructed; the kept operand's device memory must
+ * stay unchanged while the plan uses it (the native-FP64 fallback of
+ * ozaki2_reconstruct reads it). */
+int ozaki2_deconstruct_a(ozaki2_plan_t plan, const double* A, int lda, void* stream);
+int ozaki2_deconstruct_b(ozaki2_plan_t plan, const double* B, int ldb, void* stream);
+
 /* Phase 2: the 3r FP8 plane products and their exact modular accumulation;
  * writes the r centred residues of every output entry into the workspace. */
 int ozaki2_residue_gemm(ozaki2_plan_t plan, void* stream);

@@ -41,7 +41,8 @@ OZ2_Q_FALLBACK_COUNT = 9
 EXPORTS = [
     "ozaki2_dgemm", "ozaki2_dgemm_ex", "ozaki2_dgemm_strided_batched",
     "ozaki2_workspace_bytes", "ozaki2_moduli", "ozaki2_plan_create",
-    "ozaki2_plan_destroy", "ozaki2_deconstruct", "ozaki2_residue_gemm",
+    "ozaki2_plan_destroy", "ozaki2_deconstruct", "ozaki2_deconstruct_a", "ozaki2_deconstruct_b",
+    "ozaki2_residue_gemm",
     "ozaki2_reconstruct", "ozaki2_plan_query_bytes", "ozaki2_plan_query",
     "ozaki2_status_string", "ozaki2_finalize",
 ]
@@ -81,6 +82,8 @@ def load():
         "ozaki2_plan_create": (i, [ctypes.POINTER(p), i, i, i, i, u, p, sz]),
         "ozaki2_plan_destroy": (i, [p]),
         "ozaki2_deconstruct": (i, [p, p, i, p, i, p]),
+        "ozaki2_deconstruct_a": (i, [p, p, i, p]),
+        "ozaki2_deconstruct_b": (i, [p, p, i, p]),
         "ozaki2_residue_gemm": (i, [p, p]),
         "ozaki2_reconstruct": (i, [p, p, i, p]),
         "ozaki2_plan_query_bytes": (sz, [p, i]),
@@ -181,6 +184,16 @@ def ozaki2_plan_destroy(plan):
 def ozaki2_deconstruct(plan, A, lda, B, ldb, stream=None):
     return _check("ozaki2_deconstruct", load().ozaki2_deconstruct(
         plan, _ptr(A), lda, _ptr(B), ldb, _stream(stream)))
+
+
+def ozaki2_deconstruct_a(plan, A, lda, stream=None):
+    return _check("ozaki2_deconstruct_a", load().ozaki2_deconstruct_a(plan, _ptr(A), lda,
+                                                                      _stream(stream)))
+
+
+def ozaki2_deconstruct_b(plan, B, ldb, stream=None):
+    return _check("ozaki2_deconstruct_b", load().ozaki2_deconstruct_b(plan, _ptr(B), ldb,
+                                                                      _stream(stream)))
 
 
 def ozaki2_residue_gemm(plan, stream=None):

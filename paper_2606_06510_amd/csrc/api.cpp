@@ -244,28 +244,33 @@ struct ozaki2_plan_s {
   const double* B = nullptr;
   int lda = 0, ldb = 0;
   int stage = 0;      // 0 created, 1 deconstructed, 2 residues ready, 3 reconstructed
+  int sides = 0;      // operands whose planes are in the workspace (OZ2_SIDE_A | OZ2_SIDE_B)
 };
 
 namespace {
 
-int run_deconstruct(ozaki2_plan_s& p, hipStream_t s) {
+// Phase 1 for the operands in `side` (OZ2_SIDE_A, OZ2_SIDE_B or both).  One
+// operand alone only under OZ2_SCALE_FIXED, where its scales do not depend on
+// the other operand (no max-magnitude pass).
+int run_deconstruct(ozaki2_plan_s& p, int side, hipStream_t s) {
   const Oz2Dims& d = p.d;
   // Each operand's second read follows its first directly, and B's planes are
   // split before A's, so that the re-reads find A or B still in the 256 MiB
   // memory-side cache where they fit.
   const bool codes = !(d.flags & OZ2_SCALE_FIXED);
-  hipError_t e = oz2_launch_init(d, p.L, p.ws, s);
-  for (int side : {OZ2_SIDE_A, OZ2_SIDE_B}) {
-    if (e == hipSuccess) e = oz2_launch_scan(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, side, s);
+  hipError_t e = oz2_launch_init(d, p.L, p.ws, side, s);
+  for (int one : {OZ2_SIDE_A, OZ2_SIDE_B}) {
+    if (!(side & one)) continue;
+    if (e == hipSuccess) e = oz2_launch_scan(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, one, s);
     if (codes && e == hipSuccess)
-      e = oz2_launch_codes(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, side, s);
+      e = oz2_launch_codes(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, one, s);
   }
   if (codes && e == hipSuccess) e = oz2_launch_codegemm(d, p.L, p.ws, s);
-  if (e == hipSuccess) e = oz2_launch_scales(d, p.L, p.c, p.ws, s);
+  if (e == hipSuccess) e = oz2_launch_scales(d, p.L, p.c, p.ws, side, s);
   if (e == hipSuccess) e = oz2_launch_tables(p.L, p.c, p.ws, s);
-  for (int side : {OZ2_SIDE_B, OZ2_SIDE_A})
-    if (e == hipSuccess)
-      e = oz2_launch_split(d, p.L, p.c, p.ws, p.A, p.lda, p.B, p.ldb, side, s);
+  for (int one : {OZ2_SIDE_B, OZ2_SIDE_A})
+    if ((side & one) && e == hipSuccess)
+      e = oz2_launch_split(d, p.L, p.c, p.ws, p.A, p.lda, p.B, p.ldb, one, s);
   return hip_status(e);
 }
 
@@ -379,9 +384,38 @@ int ozaki2_deconstruct(ozaki2_plan_t p, const double* A, int lda, const double* 
   p->B = B;
   p->lda = lda;
   p->ldb = ldb;
-  int st = run_deconstruct(*p, (hipStream_t)stream);
+  int st = run_deconstruct(*p, OZ2_SIDE_A | OZ2_SIDE_B, (hipStream_t)stream);
+  p->sides = st == OZ2_OK ? (OZ2_SIDE_A | OZ2_SIDE_B) : 0;
   p->stage = st == OZ2_OK ? 1 : 0;
   return st;
+}
+
+namespace {
+// Operand-stationary use: re-deconstruct one operand, keep the other's planes.
+int deconstruct_one(ozaki2_plan_t p, int side, const double* X, int ld, void* stream) {
+  if (!p || !X || !(p->d.flags & OZ2_SCALE_FIXED)) return OZ2_E_INVALID;
+  if (ld < std::max(1, side == OZ2_SIDE_A ? p->d.m : p->d.k)) return OZ2_E_INVALID;
+  if (side == OZ2_SIDE_A) {
+    p->A = X;
+    p->lda = ld;
+  } else {
+    p->B = X;
+    p->ldb = ld;
+  }
+  p->sides &= ~side;
+  int st = run_deconstruct(*p, side, (hipStream_t)stream);
+  if (st == OZ2_OK) p->sides |= side;
+  p->stage = (st == OZ2_OK && p->sides == (OZ2_SIDE_A | OZ2_SIDE_B)) ? 1 : 0;
+  return st;
+}
+}  // namespace
+
+int ozaki2_deconstruct_a(ozaki2_plan_t p, const double* A, int lda, void* stream) {
+  return deconstruct_one(p, OZ2_SIDE_A, A, lda, stream);
+}
+
+int ozaki2_deconstruct_b(ozaki2_plan_t p, const double* B, int ldb, void* stream) {
+  return deconstruct_one(p, OZ2_SIDE_B, B, ldb, stream);
 }
 
 int ozaki2_residue_gemm(ozaki2_plan_t p, void* stream) {
@@ -424,7 +458,7 @@ int ozaki2_dgemm_ex(int m, int n, int k, const double* A, int lda, const double*
   p.B = B;
   p.lda = lda;
   p.ldb = ldb;
-  st = run_deconstruct(p, s);
+  st = run_deconstruct(p, OZ2_SIDE_A | OZ2_SIDE_B, s);
   if (st != OZ2_OK) return st;
   st = hip_status(oz2_launch_resgemm(p.d, p.L, p.c, p.ws, s));
   if (st != OZ2_OK) return st;

@@ -13,14 +13,20 @@
 
 namespace {
 
+// zero the row (side A) / column (side B) maxima the scans and the code GEMM
+// accumulate with atomics
 __global__ void k_init(unsigned long long* rowbits, int mp, unsigned long long* colbits, int np,
-                       uint32_t* Rmax, uint32_t* Kmax, int cslabs) {
+                       uint32_t* Rmax, uint32_t* Kmax, int cslabs, int side) {
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   size_t nR = (size_t)cslabs * mp, nK = (size_t)cslabs * np;
-  if (i < (size_t)mp) rowbits[i] = 0;
-  if (i < (size_t)np) colbits[i] = 0;
-  if (i < nR) Rmax[i] = 0;
-  if (i < nK) Kmax[i] = 0;
+  if (side & OZ2_SIDE_A) {
+    if (i < (size_t)mp) rowbits[i] = 0;
+    if (i < nR) Rmax[i] = 0;
+  }
+  if (side & OZ2_SIDE_B) {
+    if (i < (size_t)np) colbits[i] = 0;
+    if (i < nK) Kmax[i] = 0;
+  }
 }
 
 // rows of a column-major matrix: lanes along the (contiguous) row index, two
@@ -265,12 +271,13 @@ __global__ void k_scales(Oz2Dims d, const unsigned long long* __restrict__ rowbi
                          const unsigned long long* __restrict__ colbits,
                          const uint32_t* __restrict__ Rmax, const uint32_t* __restrict__ Kmax,
                          int32_t* sA, int32_t* tB, uint32_t* fA, uint32_t* fB, int cA, int cB,
-                         int* counters) {
+                         int* counters, int side) {
   int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx == 0) { counters[0] = 0; counters[1] = 0; counters[2] = 0; counters[3] = 0; }
   bool fixed = (d.flags & 2u) != 0;   // OZ2_SCALE_FIXED
   unsigned long long fixedR = 256ull * (unsigned long long)d.k;
   if (idx < d.mp) {
+    if (!(side & OZ2_SIDE_A)) return;
     int i = idx;
     unsigned long long b = rowbits[i];
     int s = 0;
@@ -291,6 +298,7 @@ __global__ void k_scales(Oz2Dims d, const unsigned long long* __restrict__ rowbi
     sA[i] = s;
     fA[i] = f;
   } else if (idx < d.mp + d.np) {
+    if (!(side & OZ2_SIDE_B)) return;
     int j = idx - d.mp;
     unsigned long long b = colbits[j];
     int t = 0;
@@ -405,7 +413,8 @@ __global__ void __launch_bounds__(256) k_split(Oz2Const c, const double* __restr
 
 }  // namespace
 
-hipError_t oz2_launch_init(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, hipStream_t s) {
+hipError_t oz2_launch_init(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, int side,
+                           hipStream_t s) {
   size_t n = (size_t)d.cslabs * (size_t)(d.mp > d.np ? d.mp : d.np);
   if ((size_t)d.mp > n) n = d.mp;
   if ((size_t)d.np > n) n = d.np;
@@ -413,7 +422,7 @@ hipError_t oz2_launch_init(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, hi
   hipLaunchKernelGGL(k_init, dim3(blocks), dim3(256), 0, s,
                      (unsigned long long*)(ws + L.rowbits), d.mp,
                      (unsigned long long*)(ws + L.colbits), d.np, (uint32_t*)(ws + L.Rmax),
-                     (uint32_t*)(ws + L.Kmax), d.cslabs);
+                     (uint32_t*)(ws + L.Kmax), d.cslabs, side);
   return hipGetLastError();
 }
 
@@ -457,14 +466,14 @@ hipError_t oz2_launch_codes(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, c
 }
 
 hipError_t oz2_launch_scales(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
-                             uint8_t* ws, hipStream_t s) {
+                             uint8_t* ws, int side, hipStream_t s) {
   unsigned blocks = (unsigned)((d.mp + d.np + 255) / 256);
   hipLaunchKernelGGL(k_scales, dim3(blocks), dim3(256), 0, s, d,
                      (const unsigned long long*)(ws + L.rowbits),
                      (const unsigned long long*)(ws + L.colbits), (const uint32_t*)(ws + L.Rmax),
                      (const uint32_t*)(ws + L.Kmax), (int32_t*)(ws + L.sA), (int32_t*)(ws + L.tB),
                      (uint32_t*)(ws + L.flagsA), (uint32_t*)(ws + L.flagsB), c.cA, c.cB,
-                     (int*)(ws + L.counters));
+                     (int*)(ws + L.counters), side);
   return hipGetLastError();
 }
 

@@ -72,7 +72,8 @@ struct Oz2Layout {
 // deconstruct launchers: OZ2_SIDE_A, OZ2_SIDE_B or both.
 #define OZ2_SIDE_A 1
 #define OZ2_SIDE_B 2
-hipError_t oz2_launch_init(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, hipStream_t s);
+hipError_t oz2_launch_init(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, int side,
+                           hipStream_t s);
 hipError_t oz2_launch_scan(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
                            const double* A, int lda, const double* B, int ldb, int side,
                            hipStream_t s);
@@ -81,7 +82,7 @@ hipError_t oz2_launch_codes(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
                             hipStream_t s);
 hipError_t oz2_launch_codegemm(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, hipStream_t s);
 hipError_t oz2_launch_scales(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
-                             uint8_t* ws, hipStream_t s);
+                             uint8_t* ws, int side, hipStream_t s);
 hipError_t oz2_launch_tables(const Oz2Layout& L, const Oz2Const& c, uint8_t* ws, hipStream_t s);
 hipError_t oz2_launch_split(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
                             const double* A, int lda, const double* B, int ldb, int side,

@@ -91,8 +91,13 @@ template <int R>
 __global__ void __launch_bounds__(256)
 k_reconstruct(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res,
               const int32_t* __restrict__ sA, const int32_t* __restrict__ tB,
-              const uint32_t* __restrict__ fA, const uint32_t* __restrict__ fB, double* C, int ldc) {
+              const uint32_t* __restrict__ fA, const uint32_t* __restrict__ fB, double* C, int ldc,
+              int* counters) {
   __shared__ double tr[2][32][33];
+  // the fallback lists of this reconstruction start empty (they are filled
+  // by the next kernel on the stream, so a repeated reconstruction of the
+  // same residues rebuilds them instead of appending)
+  if (blockIdx.x == 0 && threadIdx.x < 4) counters[threadIdx.x] = 0;
   const BlockMap b = block_map(d.mp);
   {
     uint4 x[R];
@@ -281,7 +286,7 @@ void launch_reconstruct_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& 
   hipLaunchKernelGGL(k_reconstruct<R>, dim3((unsigned)blocks), dim3(256), 0, s, c, d,
                      (const int16_t*)(ws + L.res), (const int32_t*)(ws + L.sA),
                      (const int32_t*)(ws + L.tB), (const uint32_t*)(ws + L.flagsA),
-                     (const uint32_t*)(ws + L.flagsB), C, ldc);
+                     (const uint32_t*)(ws + L.flagsB), C, ldc, (int*)(ws + L.counters));
 }
 
 template <int R>

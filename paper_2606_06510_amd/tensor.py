@@ -75,6 +75,16 @@ class Plan:
         self._A, self._B = A, B      # borrowed by the plan until reconstruct
         _lib.ozaki2_deconstruct(self.handle, A, _ld(A), B, _ld(B), stream)
 
+    def deconstruct_a(self, A, stream=None):
+        """Operand-stationary use (OZ2_SCALE_FIXED plans): new A, B's planes kept."""
+        self._A = A
+        _lib.ozaki2_deconstruct_a(self.handle, A, _ld(A), stream)
+
+    def deconstruct_b(self, B, stream=None):
+        """Operand-stationary use (OZ2_SCALE_FIXED plans): new B, A's planes kept."""
+        self._B = B
+        _lib.ozaki2_deconstruct_b(self.handle, B, _ld(B), stream)
+
     def residue_gemm(self, stream=None):
         _lib.ozaki2_residue_gemm(self.handle, stream)
 

@@ -251,3 +251,64 @@ def test_subnormal_and_overflowing_results():
     assert np.isinf(res.C).sum() == 32 * 24
     plan, C = run_staged(A, B, 12)
     compare_all(plan, C, A, B, 12, res)
+
+
+def test_repeated_reconstruct_rebuilds_fallback_lists():
+    """A plan may reconstruct its residues more than once; each time the
+    flagged-row lists are rebuilt from empty (more than half the rows are
+    flagged here, so lists that kept growing would overrun their m entries)."""
+    import paper_2606_06510_amd as oz
+    import torch
+    m, n, k = 200, 150, 100
+    A, B = synth.uniform(m, n, k, seed=77)
+    A = A.copy()
+    A[:140, ::2] *= 1e200                     # T2: intra-row span ~2^664 on 140 rows
+    res = oracle.dgemm(A, B, 12)
+    assert len(res.fallback_rows) == 140 and len(res.fallback_cols) == 0
+    plan, C = run_staged(A, B, 12)
+    compare_C(C, A, B, res)
+    assert plan.query(oz.OZ2_Q_FALLBACK_COUNT) == (140, 0)
+    C2d = oz.to_device_colmajor(np.full((m, n), np.nan), device())
+    plan.reconstruct(C2d)
+    torch.cuda.synchronize()
+    C2 = oz.from_device_colmajor(C2d)
+    assert np.array_equal(bits(C2), bits(C))
+    assert plan.query(oz.OZ2_Q_FALLBACK_COUNT) == (140, 0)
+
+
+def test_operand_stationary_planes():
+    """Mode P on a fixed-scale plan: A's planes are kept across a product with a
+    new B, then B's across a new A; every product equals the oracle's
+    fixed-scale result on its pair, bit for bit.  One-operand deconstruction
+    is refused without OZ2_SCALE_FIXED and before both operands exist."""
+    import paper_2606_06510_amd as oz
+    import torch
+    m, n, k = 300, 260, 200
+    A, B1 = synth.lognormal(m, n, k, seed=41)
+    A2, B2 = synth.lognormal(m, n, k, seed=43)
+    dev = device()
+    Ad, B1d, A2d, B2d = (oz.to_device_colmajor(X, dev) for X in (A, B1, A2, B2))
+    plan = oz.Plan(m, n, k, 12, oz.OZ2_SCALE_FIXED, device=dev)
+    with pytest.raises(oz.Ozaki2Error):
+        plan.deconstruct_a(Ad)
+        plan.residue_gemm()                   # B was never deconstructed
+
+    def product():
+        Cd = oz.colmajor_empty(m, n, device=dev)
+        plan.residue_gemm()
+        plan.reconstruct(Cd)
+        torch.cuda.synchronize()
+        return oz.from_device_colmajor(Cd)
+
+    plan.deconstruct(Ad, B1d)
+    C1 = product()
+    plan.deconstruct_b(B2d)
+    C2 = product()
+    plan.deconstruct_a(A2d)
+    C3 = product()
+    for C, X, Y in ((C1, A, B1), (C2, A, B2), (C3, A2, B2)):
+        compare_C(C, X, Y, oracle.dgemm(X, Y, 12, mode="fixed"))
+    adaptive = oz.Plan(m, n, k, 12, 0, device=dev)
+    adaptive.deconstruct(Ad, B1d)
+    with pytest.raises(oz.Ozaki2Error):
+        adaptive.deconstruct_b(B2d)
