@@ -62,6 +62,15 @@ struct Big {
     return 32 * top + (32 - __builtin_clz(w[top]));
   }
   uint32_t word(int i) const { return i < (int)w.size() ? w[i] : 0u; }
+  // bits lo .. lo+cnt-1 (cnt <= 52) as an integer
+  uint64_t bits(int lo, int cnt) const {
+    uint64_t v = 0;
+    for (int b = cnt - 1; b >= 0; --b) {
+      const int pos = lo + b;
+      v = (v << 1) | ((word(pos >> 5) >> (pos & 31)) & 1u);
+    }
+    return v;
+  }
 };
 
 int64_t inv_mod(int64_t a, int64_t m) {  // a^-1 mod m, gcd(a, m) = 1
@@ -112,6 +121,7 @@ bool make_const(int r, Oz2Const& c) {
     Big Wi = Mi;
     Wi.mul_small((uint32_t)inv);
     for (int j = 0; j < OZ2_NLIMB; ++j) c.W[i][j] = (double)Wi.word(j);
+    for (int j = 0; j < 3; ++j) c.W38[i][j] = (double)Wi.bits(38 * j, 38);
     c.wfrac[i] = (double)inv / (double)m;   // W_i / M exactly = inv_i / m_i
   }
   c.P = pb;
@@ -127,6 +137,10 @@ bool make_const(int r, Oz2Const& c) {
     c.Ml[j] = (double)M.word(j);
     c.Mhalf[j] = (double)Mh.word(j);
   }
+  for (int j = 0; j < 3; ++j) {
+    c.M38[j] = (double)M.bits(38 * j, 38);
+    c.Mhalf38[j] = (double)Mh.bits(38 * j, 38);
+  }
   // the reconstruction kernels are specialised on r with nw = 3 (r <= 10),
   // 4 (r <= 13), 5 words: [-M/2, M/2) must fit nw words of two's complement
   c.nw = r <= 10 ? 3 : (r <= 13 ? 4 : 5);
@@ -134,6 +148,10 @@ bool make_const(int r, Oz2Const& c) {
   double Md = 0.0;
   for (int j = OZ2_NLIMB - 1; j >= 0; --j) Md = Md * 4294967296.0 + (double)M.word(j);
   c.mtop = std::ldexp(1.0, 32 * (c.nw - 1)) / Md;
+  // radix-2^38 limbs (the reconstruction of r <= 12): [-M/2, M/2) must fit
+  // 114 bits, and with |x_i| <= 545 every limb sum stays below 2^52
+  if (r <= 12 && M.bitlen() + 1 > 114) return false;
+  c.mtop38 = std::ldexp(1.0, 76) / Md;
   const int cc = (M.bitlen() - 1) + 6;     // floor(log2 M) + 6
   c.cA = cc / 2;
   c.cB = cc - c.cA;

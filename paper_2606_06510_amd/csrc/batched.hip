@@ -167,6 +167,8 @@ struct Emit {
         double sacc = 0.0;   // native FP64, one FMA per k in ascending k
         for (int l = 0; l < k; ++l) sacc = fma(A[row + (size_t)l * lda], B[l + (size_t)col * ldb], sacc);
         v = sacc;
+      } else if constexpr (R <= 12) {
+        v = crt38_rounded<R, I>(c, x, S.sS[row] + S.sT[col]);
       } else {
         uint32_t w[NW];
         crt_words<R, NW, I>(c, x, w);

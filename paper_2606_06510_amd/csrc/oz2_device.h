@@ -251,4 +251,90 @@ __device__ __forceinline__ double round_scaled(const uint32_t (&x)[NW], int e) {
   return sm ? -v : v;
 }
 
+// ---- r <= 12: the exact integer in three radix-2^38 fp64 limbs ----------
+// X = S2 2^76 + S1 2^38 + S0 with S0, S1 in [0, 2^38) after normalisation
+// and S2 signed; [-M/2, M/2) fits (log2 M < 113).  Every limb sum is an
+// integer below 2^52 (|x_i| <= 545, limbs of W_i and M below 2^38, at most
+// 12 terms plus the q M correction), so the fp64 arithmetic is exact.
+__device__ __forceinline__ void normalise38(double& S0, double& S1, double& S2) {
+  double cy = floor(S0 * 0x1p-38);
+  S0 = fma(-cy, 0x1p38, S0);
+  S1 += cy;
+  cy = floor(S1 * 0x1p-38);
+  S1 = fma(-cy, 0x1p38, S1);
+  S2 += cy;
+}
+
+// RN-even binary64 value of X 2^-e from normalised limbs.  If S2 is in
+// [-2^15, 2^15), H = S2 2^38 + S1 is exact (|H| <= 2^53) and one fma rounds
+// H 2^38 + S0 once.  Otherwise |S2 2^38 + S1| >= 2^53, where binary64
+// rounding boundaries fall on integers, so S0 / 2^38 (in [0, 1)) can stand
+// in as a sticky half: S2 2^38 + S1 + 0.5 [S0 != 0] rounds like X / 2^38.
+// The power-of-two scaling is exact unless the result overflows (to
+// infinity, the correct rounding) or is subnormal, which takes the 32-bit
+// word routine above.
+__device__ __forceinline__ double round38(double S0, double S1, double S2, int e) {
+  double v;
+  int sh;
+  if (S2 >= -0x1p15 && S2 < 0x1p15) {
+    v = fma(fma(S2, 0x1p38, S1), 0x1p38, S0);
+    sh = 0;
+  } else {
+    v = fma(S2, 0x1p38, S1 + (S0 != 0.0 ? 0.5 : 0.0));
+    sh = 38;
+  }
+  if (v == 0.0) return 0.0;        // exact zero is +0.0
+  const int ev = (int)((__double_as_longlong(v) >> 52) & 0x7ff) - 1023;   // |v| >= 1
+  if (ev + sh - e < -1022) {
+    // subnormal result: X as four 32-bit words, X = b1 2^64 + b0
+    const unsigned long long u0 = (unsigned long long)S0, u1 = (unsigned long long)S1;
+    const unsigned long long b0 = u0 | (u1 << 38);
+    const long long b1 = (long long)S2 * 4096 + (long long)(u1 >> 26);
+    const uint32_t w[4] = {(uint32_t)b0, (uint32_t)(b0 >> 32), (uint32_t)b1,
+                           (uint32_t)((unsigned long long)b1 >> 32)};
+    return round_scaled<4>(w, e);
+  }
+  return ldexp(v, sh - e);
+}
+
+// C~ of output I of a thread (R <= 12 centred residues) rounded with the
+// exponent shift -e: the direct CRT sum in radix-2^38 limbs, the quotient
+// q = rint(X/M) from the top limbs (within 2^-36 of X/M), the exact range
+// check for the ambiguous case, then round38.
+template <int R, int I>
+__device__ __forceinline__ double crt38_rounded(const Oz2Const& c, const uint4 (&x)[R], int e) {
+  static_assert(R <= 12, "three radix-2^38 limbs hold [-M/2, M/2) only for r <= 12");
+  double S0 = 0.0, S1 = 0.0, S2 = 0.0;
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const double xi = res_at<I>(x[i]);
+    S0 = fma(xi, c.W38[i][0], S0);
+    S1 = fma(xi, c.W38[i][1], S1);
+    S2 = fma(xi, c.W38[i][2], S2);
+  }
+  const double f = fma(S1, 0x1p-38, S2) * c.mtop38;
+  const double q = rint(f);
+  S0 = fma(-q, c.M38[0], S0);
+  S1 = fma(-q, c.M38[1], S1);
+  S2 = fma(-q, c.M38[2], S2);
+  normalise38(S0, S1, S2);
+  if (fabs(f - q) > 0.49999) {
+    // X in [-floor(M/2), ceil(M/2) - 1]: P = X - M + floor(M/2) >= 0 means
+    // X >= ceil(M/2) (subtract M); N = X + floor(M/2) < 0 means X <
+    // -floor(M/2) (add M); the sign of a normalised limb vector is that of
+    // its top limb
+    double P0 = S0 - c.M38[0] + c.Mhalf38[0], P1 = S1 - c.M38[1] + c.Mhalf38[1],
+           P2 = S2 - c.M38[2] + c.Mhalf38[2];
+    double N0 = S0 + c.Mhalf38[0], N1 = S1 + c.Mhalf38[1], N2 = S2 + c.Mhalf38[2];
+    normalise38(P0, P1, P2);
+    normalise38(N0, N1, N2);
+    const double adj = (P2 >= 0.0) ? -1.0 : ((N2 < 0.0) ? 1.0 : 0.0);
+    S0 = fma(adj, c.M38[0], S0);
+    S1 = fma(adj, c.M38[1], S1);
+    S2 = fma(adj, c.M38[2], S2);
+    normalise38(S0, S1, S2);
+  }
+  return round38(S0, S1, S2, e);
+}
+
 }  // namespace

@@ -38,6 +38,10 @@ struct Oz2Const {
   double Mhalf[OZ2_NLIMB];        // 32-bit words of floor(M/2)
   int nw;                         // words of the two's complement integer in [-M/2, M/2)
   double mtop;                    // 2^(32 (nw - 1)) / M, rounded
+  // the same in three radix-2^38 limbs (used for r <= 12, 114 bits)
+  double W38[OZ2_MAXR][3];
+  double M38[3], Mhalf38[3];
+  double mtop38;                  // 2^76 / M, rounded
   int cA, cB;                     // width budgets of the scaling rule
   // residue -> plane-bytes tables: entry toff[i] + d for the centred residue d
   int toff[OZ2_MAXR];             // (sum of the earlier moduli) + floor(m_i/2)

@@ -71,9 +71,13 @@ struct Outputs {
     const int rr = b.rb + 8 * (I >> 2) + (I & 3);
     const int row = b.row0 + rr;
     const int si = row < d.m ? sA[row] : 0;
-    uint32_t w[NW];
-    crt_words<R, NW, I>(c, x, w);
-    tr[b.cl][rr] = round_scaled<NW>(w, si + tj);
+    if constexpr (R <= 12) {
+      tr[b.cl][rr] = crt38_rounded<R, I>(c, x, si + tj);
+    } else {
+      uint32_t w[NW];
+      crt_words<R, NW, I>(c, x, w);
+      tr[b.cl][rr] = round_scaled<NW>(w, si + tj);
+    }
     Outputs<R, I + 1>::run(c, d, x, b, tj, sA, tr);
   }
 };
