@@ -83,7 +83,7 @@ int64_t inv_mod(int64_t a, int64_t m) {  // a^-1 mod m, gcd(a, m) = 1
   return t < 0 ? t + m : t;
 }
 
-bool make_const(int r, Oz2Const& c) {
+bool build_const(int r, Oz2Const& c) {
   if (r < 8 || r > OZ2_MAXR) return false;
   std::memset(&c, 0, sizeof(c));
   std::vector<int> ms(kPool, kPool + r);
@@ -155,6 +155,22 @@ bool make_const(int r, Oz2Const& c) {
   const int cc = (M.bitlen() - 1) + 6;     // floor(log2 M) + 6
   c.cA = cc / 2;
   c.cB = cc - c.cA;
+  return true;
+}
+
+// The constants depend only on r: built once per r (bigint products and
+// inverses), then copied.
+bool make_const(int r, Oz2Const& c) {
+  static std::mutex mu;
+  static Oz2Const cache[OZ2_MAXR + 1];
+  static bool ready[OZ2_MAXR + 1] = {false};
+  if (r < 8 || r > OZ2_MAXR) return false;
+  std::lock_guard<std::mutex> g(mu);
+  if (!ready[r]) {
+    if (!build_const(r, cache[r])) return false;
+    ready[r] = true;
+  }
+  c = cache[r];
   return true;
 }
 
