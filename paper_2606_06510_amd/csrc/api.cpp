@@ -125,6 +125,24 @@ bool build_const(int r, Oz2Const& c) {
     c.wfrac[i] = (double)inv / (double)m;   // W_i / M exactly = inv_i / m_i
   }
   c.P = pb;
+  // kcheap: with digit maxima D0, D1 of the planes (both operands share the
+  // digit rule), a k-term chain has |d1 e0 + d0 e1| <= 2 D0 D1 per term and
+  // |d0 e0| <= D0^2 (square m: x s between them), or |d1 e1| <= D1^2 and
+  // |d0 e0| <= D0^2 (nonsquare m: x -16 between them); an integer multiply
+  // keeps the chain exact while k times the bound stays <= 2^24
+  for (int i = 0; i < r; ++i) {
+    const int m = c.m[i], sq = c.sq[i];
+    int D0 = 0, D1 = 0;
+    for (int d = -(m / 2); d <= (m + 1) / 2 - 1; ++d) {
+      int d0, d1;
+      oz2_digits(d, m, sq, d0, d1);
+      D0 = std::max(D0, std::abs(d0));
+      D1 = std::max(D1, std::abs(d1));
+    }
+    const long long per = sq ? 2LL * D0 * D1 * sq + (long long)D0 * D0
+                             : 16LL * D1 * D1 + (long long)D0 * D0;
+    c.kcheap[i] = (int)((1LL << 24) / per);
+  }
   int off = 0;
   for (int i = 0; i < r; ++i) {
     c.toff[i] = off + ms[i] / 2;

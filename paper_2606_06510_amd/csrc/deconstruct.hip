@@ -331,7 +331,7 @@ __global__ void k_plane_tables(Oz2Const c, uint32_t* tab) {
   const int m = c.m[i];
   const int d = idx - c.toff[i];
   int d0, d1;
-  digits(d, m, c.sq[i], d0, d1);
+  oz2_digits(d, m, c.sq[i], d0, d1);
   const int lo = __builtin_amdgcn_cvt_pk_fp8_f32((float)d0, (float)d1, 0, false);
   const int hi = __builtin_amdgcn_cvt_pk_fp8_f32((float)(d0 + d1), 0.0f, 0, false);
   tab[idx] = ((uint32_t)lo & 0xFFFFu) | (((uint32_t)hi & 0xFFu) << 16);

@@ -311,10 +311,40 @@ k_codegemm(const uint8_t* __restrict__ cA, const uint8_t* __restrict__ cB, int m
   }
 }
 
+// Chain transitions: acc <- (acc - m rint(acc/m)) * rho.  The reduced value
+// has magnitude <= m/2 + 3 (the fp32 quotient estimate is within 1 of the
+// exact one), so |acc * rho| < 2^18 and the next product keeps every partial
+// sum below 2^24.  Square moduli: the two cross products share one chain
+// (their sum is at most 512 k_slab = 2^24), then x s before d0e0.
+// Nonsquare: d1e1, x rho0 = 240/(-15), d0e0, x rho1 = -15/16,
+// (d0+d1)(e0+e1).
+__device__ __forceinline__ void chain_reduce(v16f (&acc)[4][2], float inv, float fm, float rho) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float v = acc[i][j][e];
+        acc[i][j][e] = __builtin_fmaf(-rintf(v * inv), fm, v) * rho;
+      }
+}
+// the same transition without the reduction, for chains short enough that
+// the unreduced product stays exact (k <= kcheap)
+__device__ __forceinline__ void chain_scale(v16f (&acc)[4][2], float f) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] *= f;
+}
+
 // ------------------------------------------------------------- residue GEMM
 // grid: (tiles, ceil(r / mpw)).  Workgroup (t, g) computes moduli
 // g*mpw .. min(r, (g+1)*mpw) - 1 of tile t over k in [kbeg, kend), one after
 // the other on one accumulator set, as one continuous DMA stream.
+// CH bit 0: square moduli, bit 1: nonsquare moduli take the first chain
+// transition as a plain multiply (every modulus of that kind has k <= kcheap)
+template <int CH>
 __global__ void __launch_bounds__(NT, 1)
 k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, int mp,
           int np, int kp, int kbeg, int kend, int accumulate, int mpw, int16_t* __restrict__ res) {
@@ -358,26 +388,19 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
     // one chain (their sum is at most 512 k_slab = 2^24), then x s before
     // d0e0.  Nonsquare: d1e1, x rho0 = 240/(-15), d0e0, x rho1 = -15/16,
     // (d0+d1)(e0+e1).
-    auto transition = [&](const float rho) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const float v = acc[i][j][e];
-            acc[i][j][e] = __builtin_fmaf(-rintf(v * inv), fm, v) * rho;
-          }
-    };
+    // short chains (k <= kcheap) need no reduction at the first transition:
+    // a plain multiply by the integer coefficient ratio keeps them exact
     if (s) {
       run_stages<true>(&c, x, dm, LB, lds0, it, 2 * nk, landed, acc);
-      transition((float)s);
+      if (CH & 1) chain_scale(acc, (float)s);
+      else chain_reduce(acc, inv, fm, (float)s);
       run_stages<true>(&c, x, dm, LB, lds0, it + 2 * nk, nk, landed, acc);
     } else {
       run_stages<true>(&c, x, dm, LB, lds0, it, nk, landed, acc);
-      transition((float)c.rho0[mi]);
+      if (CH & 2) chain_scale(acc, -16.0f);
+      else chain_reduce(acc, inv, fm, (float)c.rho0[mi]);
       run_stages<true>(&c, x, dm, LB, lds0, it + nk, nk, landed, acc);
-      transition((float)c.rho1[mi]);
+      chain_reduce(acc, inv, fm, (float)c.rho1[mi]);
       run_stages<true>(&c, x, dm, LB, lds0, it + 2 * nk, nk, landed, acc);
     }
     it += 3 * nk;
@@ -463,8 +486,20 @@ hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Con
   dim3 grid(tiles, (c.r + mpw - 1) / mpw);
   for (int kb = 0, sl = 0; kb < d.kp; kb += OZ2_KSLAB, ++sl) {
     const int ke = kb + OZ2_KSLAB < d.kp ? kb + OZ2_KSLAB : d.kp;
-    hipLaunchKernelGGL(k_resgemm, grid, dim3(NT), 0, s, c, ws + L.planesA, ws + L.planesB, d.mp,
-                       d.np, d.kp, kb, ke, sl > 0 ? 1 : 0, mpw, (int16_t*)(ws + L.res));
+    // the first chain transition may skip its reduction when every modulus of
+    // a kind has k <= kcheap for this slab
+    bool sq_cheap = true, ns_cheap = true;
+    for (int i = 0; i < c.r; ++i) {
+      const bool ok = ke - kb <= c.kcheap[i];
+      if (c.sq[i]) sq_cheap = sq_cheap && ok;
+      else ns_cheap = ns_cheap && ok;
+    }
+    const int ch = (sq_cheap ? 1 : 0) | (ns_cheap ? 2 : 0);
+    void (*kern)(Oz2Const, const uint8_t*, const uint8_t*, int, int, int, int, int, int, int,
+                 int16_t*) = ch == 3 ? k_resgemm<3> : ch == 2 ? k_resgemm<2>
+                                                    : ch == 1 ? k_resgemm<1> : k_resgemm<0>;
+    hipLaunchKernelGGL(kern, grid, dim3(NT), 0, s, c, ws + L.planesA, ws + L.planesB, d.mp, d.np,
+                       d.kp, kb, ke, sl > 0 ? 1 : 0, mpw, (int16_t*)(ws + L.res));
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

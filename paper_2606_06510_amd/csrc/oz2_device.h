@@ -56,33 +56,6 @@ __device__ __forceinline__ int centred_residue(double ah, double al, double m, d
   return (int)fma(-q, m, t);
 }
 
-// Digit planes of a centred residue d of m (the E4M3-exact layouts of the
-// "frozen plane kernel" section):
-//  * square m = s^2, Eq. (sq-shortcut): balanced base-s digits
-//    d0 = ((d + floor(s/2)) mod s) - floor(s/2), d1 = (d - d0)/s;
-//  * nonsquare, Eq. (kar) with b = 4: balanced base-16 digits with the carry
-//    correction of the "e4m3 layout envelope" paragraph (if d0+d1 is not
-//    E4M3-exact -- odd and above 16 in magnitude -- move one unit of base
-//    weight: (d0 - 16 sgn(d0), d1 + sgn(d0))), plus the sum plane d0+d1.
-__device__ __forceinline__ void digits(int d, int m, int s, int& d0, int& d1) {
-  if (s) {
-    const int h = s >> 1;
-    int u = (d + h) % s;
-    u += (u < 0) ? s : 0;
-    d0 = u - h;
-    d1 = (d - d0) / s;
-  } else {
-    d0 = ((d + 8) & 15) - 8;
-    d1 = (d - d0) >> 4;
-    const int sm = d0 + d1, am = sm < 0 ? -sm : sm;
-    if (am > 16 && (am & 1)) {
-      const int sg = d0 > 0 ? 1 : -1;
-      d0 -= 16 * sg;
-      d1 += sg;
-    }
-  }
-}
-
 // bytes p of four table entries, packed (element j in byte j)
 __device__ __forceinline__ uint32_t gather_byte(uint32_t e0, uint32_t e1, uint32_t e2, uint32_t e3,
                                                 uint32_t sel) {

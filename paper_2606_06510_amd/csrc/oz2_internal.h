@@ -46,6 +46,10 @@ struct Oz2Const {
   // residue -> plane-bytes tables: entry toff[i] + d for the centred residue d
   int toff[OZ2_MAXR];             // (sum of the earlier moduli) + floor(m_i/2)
   int tabsz;                      // sum of the moduli (entries)
+  // largest k per exact FP32 chain for which the first chain transition of
+  // modulus i may be a plain multiply (x s for square m, x -16 = 240/-15 for
+  // nonsquare m) without a reduction: every partial sum stays below 2^24
+  int kcheap[OZ2_MAXR];
 };
 
 struct Oz2Dims {
@@ -107,6 +111,34 @@ hipError_t oz2_launch_batched(const Oz2Const& c, int m, int n, int k, int batch,
                               int lda, long long sA, const double* B, int ldb, long long sB,
                               double* C, int ldc, long long sC, const uint32_t* tab,
                               hipStream_t s);
+
+// ---------------------------------------------------------------- digit rule
+// Digit planes of a centred residue d of m (the E4M3-exact layouts of the
+// "frozen plane kernel" section):
+//  * square m = s^2, Eq. (sq-shortcut): balanced base-s digits
+//    d0 = ((d + floor(s/2)) mod s) - floor(s/2), d1 = (d - d0)/s;
+//  * nonsquare, Eq. (kar) with b = 4: balanced base-16 digits with the carry
+//    correction of the "e4m3 layout envelope" paragraph (if d0+d1 is not
+//    E4M3-exact -- odd and above 16 in magnitude -- move one unit of base
+//    weight: (d0 - 16 sgn(d0), d1 + sgn(d0))), plus the sum plane d0+d1.
+__host__ __device__ inline void oz2_digits(int d, int m, int s, int& d0, int& d1) {
+  if (s) {
+    const int h = s >> 1;
+    int u = (d + h) % s;
+    u += (u < 0) ? s : 0;
+    d0 = u - h;
+    d1 = (d - d0) / s;
+  } else {
+    d0 = ((d + 8) & 15) - 8;
+    d1 = (d - d0) >> 4;
+    const int sm = d0 + d1, am = sm < 0 ? -sm : sm;
+    if (am > 16 && (am & 1)) {
+      const int sg = d0 > 0 ? 1 : -1;
+      d0 -= 16 * sg;
+      d1 += sg;
+    }
+  }
+}
 
 // ---------------------------------------------------------------- device helpers
 #ifdef __HIPCC__
