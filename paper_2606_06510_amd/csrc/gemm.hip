@@ -40,7 +40,14 @@ constexpr int STB = 2 * OPB;     // 32 KiB per stage
 constexpr int NB = 4;            // ring depth
 constexpr int NT = 512;          // threads per workgroup
 
-__device__ __forceinline__ void bar() { asm volatile("s_barrier" ::: "memory"); }
+// s_barrier pinned in the instruction stream: the scheduler moves nothing
+// (not even register-only MFMAs) across it, so the phases below stay phases
+__device__ __forceinline__ void bar() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+__device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 template <int N>
 __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
@@ -178,39 +185,67 @@ __device__ __forceinline__ float centre_small(float x, float fm, float inv, floa
   return r == hm ? -hm : r;
 }
 
-// Main loop over stages [it0, it0 + n) of the stage sequence.  Stages below
-// `landed` are known to be in LDS already (this wave waited for all its DMAs
-// before the epilogue stores that now share its vmcnt), so they skip the wait.
+// Wait until this wave's DMA share of stage s has landed.  When it waits
+// for stage s the wave has issued its shares up to stage min(s + 2, T - 1)
+// (four DMA instructions each, returning in order); stages below `landed`
+// are known to be in LDS already (the wave drained its loads before the
+// epilogue stores that now share its vmcnt).
+__device__ __forceinline__ void wait_stage(int s, int T, int landed) {
+  if (s >= T || s < landed) return;
+  if (s + 2 < T) wait_vm<8>();
+  else if (s + 1 < T) wait_vm<4>();
+  else wait_vm<0>();
+}
+
+// Main loop over stages [it0, it0 + n) of the stage sequence, in two phases
+// per stage separated by workgroup barriers:
+//   L(t): issue this wave's DMA share of stage t + 3 (ring slot (t+3)%4, last
+//         read in L(t-1)), read the fragments of stage t from LDS and wait
+//         for them;
+//   C(t): the 8 MFMAs of stage t.
+// The two waves sharing a SIMD (w and w + 4) run the same sequence one phase
+// apart (group g = w / 4; group 1 passes one extra barrier first, group 0 one
+// extra barrier last), so while one issues its LDS reads, DMAs, waits and
+// chain transitions the other keeps the SIMD's matrix unit busy.  Barrier b
+// sees C(t) of group 0 end with L(t) of group 1 (b = 2t + 1) and L(t+1) of
+// group 0 end with C(t) of group 1 (b = 2t + 2); stage t + 1 must have landed
+// by barrier 2t + 1, the first one before anyone reads it, and the
+// fragment reads of slot t%4 are complete by barrier 2t + 1 as well, before
+// any wave's L(t+1) may issue the DMA that overwrites it.
 template <bool RES>
 __device__ __forceinline__ void run_stages(const Oz2Const* c, const Ctx& x, Dma& dm, uint8_t* LB,
-                                           uint32_t lds0, int it0, int n, int landed,
+                                           uint32_t lds0, int it0, int n, int landed, int g,
                                            v16f (&acc)[4][2]) {
   const int T = x.T;
   for (int it = it0; it < it0 + n; ++it) {
-    // this wave's DMA share is 4 instructions per stage; stages it+1, it+2
-    // may still be in flight
-    if (it < landed) {
-    } else if (it + 2 < T) wait_vm<8>();
-    else if (it + 1 < T) wait_vm<4>();
-    else wait_vm<0>();
-    bar();
+    if (it + 3 < T) issue_stage<RES>(c, x, dm, lds0 + ((it + 3) & 3) * STB);
     v8i fa[4], fb[2];
     frags(LB + (it & 3) * STB, fa, fb);
-    if (it + 3 < T) issue_stage<RES>(c, x, dm, lds0 + ((it + 3) & 3) * STB);
+    wait_lgkm0();
+    if (g) wait_stage(it + 1, T, landed);
+    bar();
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[i], fb[j], acc[i][j], 0, 0,
                                                                    0, 0, 0, 0);
+    if (!g) wait_stage(it + 1, T, landed);
+    bar();
   }
 }
 
+// Before the loop: every wave issues its shares of stages 0..2, stage 0 is
+// waited for by all, then group 1 takes its one-phase offset.
 template <bool RES>
-__device__ __forceinline__ void prologue(const Oz2Const* c, const Ctx& x, Dma& dm, uint32_t lds0) {
+__device__ __forceinline__ void prologue(const Oz2Const* c, const Ctx& x, Dma& dm, uint32_t lds0,
+                                         int g) {
 #pragma unroll
   for (int t = 0; t < NB - 1; ++t)
     if (t < x.T) issue_stage<RES>(c, x, dm, lds0 + t * STB);
+  wait_stage(0, x.T, 0);
+  bar();
+  if (g) bar();
 }
 
 // One step of a halving max-butterfly across lanes L and L^B: of the first N
@@ -253,8 +288,10 @@ k_codegemm(const uint8_t* __restrict__ cA, const uint8_t* __restrict__ cB, int m
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = v16f{0.f};
-  prologue<false>(nullptr, x, dm, lds0);
-  run_stages<false>(nullptr, x, dm, LB, lds0, 0, x.T, 0, acc);
+  const int g = __builtin_amdgcn_readfirstlane(threadIdx.x >> 8);
+  prologue<false>(nullptr, x, dm, lds0, g);
+  run_stages<false>(nullptr, x, dm, LB, lds0, 0, x.T, 0, g, acc);
+  if (!g) bar();
 
   // Row and column maxima of G'.  Lane L holds rows 32i + 8(e/4) + 4(L/32) +
   // e%4 (of the wave's 128) in column 32j + L%32 (of its 64).
@@ -368,7 +405,8 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
   Dma dm = dma_init(x);
   dm.mi = mi0;
   product_ptrs(&c, x, mi0, 0, dm);
-  prologue<true>(&c, x, dm, lds0);
+  const int g = __builtin_amdgcn_readfirstlane(threadIdx.x >> 8);
+  prologue<true>(&c, x, dm, lds0, g);
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int it = 0, landed = 0;
@@ -391,17 +429,17 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
     // short chains (k <= kcheap) need no reduction at the first transition:
     // a plain multiply by the integer coefficient ratio keeps them exact
     if (s) {
-      run_stages<true>(&c, x, dm, LB, lds0, it, 2 * nk, landed, acc);
+      run_stages<true>(&c, x, dm, LB, lds0, it, 2 * nk, landed, g, acc);
       if (CH & 1) chain_scale(acc, (float)s);
       else chain_reduce(acc, inv, fm, (float)s);
-      run_stages<true>(&c, x, dm, LB, lds0, it + 2 * nk, nk, landed, acc);
+      run_stages<true>(&c, x, dm, LB, lds0, it + 2 * nk, nk, landed, g, acc);
     } else {
-      run_stages<true>(&c, x, dm, LB, lds0, it, nk, landed, acc);
+      run_stages<true>(&c, x, dm, LB, lds0, it, nk, landed, g, acc);
       if (CH & 2) chain_scale(acc, -16.0f);
       else chain_reduce(acc, inv, fm, (float)c.rho0[mi]);
-      run_stages<true>(&c, x, dm, LB, lds0, it + nk, nk, landed, acc);
+      run_stages<true>(&c, x, dm, LB, lds0, it + nk, nk, landed, g, acc);
       chain_reduce(acc, inv, fm, (float)c.rho1[mi]);
-      run_stages<true>(&c, x, dm, LB, lds0, it + 2 * nk, nk, landed, acc);
+      run_stages<true>(&c, x, dm, LB, lds0, it + 2 * nk, nk, landed, g, acc);
     }
     it += 3 * nk;
 
@@ -456,6 +494,7 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
         p[1] = make_uint4(pk[i][j][4], pk[i][j][5], pk[i][j][6], pk[i][j][7]);
       }
   }
+  if (!g) bar();
   wait_vm<0>();
 }
 
