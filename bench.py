@@ -77,6 +77,24 @@ def pmc_traffic(kernel_src, tag):
         return None
 
 
+def pmc_mfma(kernel_src, tag):
+    """MFMA busy share and clock of the residue GEMM from the committed rocprofv3
+    counter summary; None unless it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{tag}_pmc_mfma.txt")
+    if not os.path.exists(path):
+        return None
+    lines = open(path).read().splitlines()
+    sha = [x.split(":", 1)[1].strip() for x in lines if x.startswith("kernel_source_sha256:")]
+    if not sha or sha[0] != source_sha256(kernel_src):
+        return None
+    for x in lines:
+        cells = [c.strip() for c in x.strip("|").split("|")]
+        if len(cells) == 7 and "k_resgemm" in cells[0]:
+            return {"mfma_busy": cells[5], "clock_ghz": float(cells[6]),
+                    "fp8_ops_per_launch": float(cells[3]), "source": os.path.relpath(path, ROOT)}
+    return None
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -189,6 +207,7 @@ def main():
 
     tag = f"resgemm_{args.config}_r{r}"
     traffic = pmc_traffic("paper_2606_06510_amd/csrc/gemm.hip", tag)
+    mfma_pmc = pmc_mfma("paper_2606_06510_amd/csrc/gemm.hip", tag)
     dec_bytes = (m * k + k * n) * (8 + 1 + plan_pstore(r))    # A, B read once + codes + planes
     rec_bytes = m * n * (2 * r + 8)                              # residues read + C written
     dec_gbs = dec_bytes / (dec * 1e-3) / 1e9
@@ -217,6 +236,7 @@ def main():
         "stages_ms": {"deconstruct": round(dec, 4), "residue_gemm": round(gem, 4),
                       "reconstruct": round(rec, 4)},
         "fp8_mfma_util_residue_gemm": round(achieved / FP8_PEAK_TFLOPS, 4),
+        "fp8_mfma_rocprof_residue_gemm": mfma_pmc,
         "deconstruct_gbs_algorithmic": round(dec_gbs, 1),
         "deconstruct_frac_hbm": round(dec_gbs / HBM_PEAK_GBS, 4),
         "reconstruct_gbs_algorithmic": round(rec_gbs, 1),

@@ -3,6 +3,7 @@
     python -m paper_2606_06510_amd.rocprof_summary stats STATS_CSV OUT_MD TITLE COMMAND
     python -m paper_2606_06510_amd.rocprof_summary traffic FETCH_CSV WRITE_CSV OUT_TXT \\
         KERNEL COPY_BYTES SOURCE CMD_FETCH CMD_WRITE
+    python -m paper_2606_06510_amd.rocprof_summary mfma COUNTER_CSV OUT_TXT SOURCE CMD
 
 ``stats`` turns a ``--kernel-trace --stats`` kernel_stats.csv into a markdown
 table.  ``traffic`` reads two ``--pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE``
@@ -10,6 +11,11 @@ counter_collection.csv files (KiB per dispatch), takes the mean per launch of
 KERNEL and of the plain copy kernel (COPY_BYTES read and written), and scales
 the kernel's figures by copy_bytes / copy_reading; the result carries the
 sha256 of SOURCE so that bench.py uses it only for the kernel it was taken on.
+``mfma`` reads one ``--pmc SQ_INSTS_VALU_MFMA_MOPS_F8 SQ_VALU_MFMA_BUSY_CYCLES
+GRBM_GUI_ACTIVE`` counter_collection.csv and reports, per FP8-MFMA kernel,
+the FP8 operations per launch (MOPS x 512), the share of SIMD cycles the MFMA
+unit was busy and the shader clock the launch ran at (GRBM_GUI_ACTIVE is
+summed over the XCDs: cycles = sum / XCDs, clock = cycles / duration).
 """
 from __future__ import annotations
 
@@ -76,11 +82,45 @@ def traffic(fetch_csv, write_csv, dst, kernel, copy_bytes, source, cmd_fetch, cm
             f.write(f"#   {k}: {fetch[k]:.1f} / {write.get(k, float('nan')):.1f}\n")
 
 
+def mfma(src, dst, source, cmd, xcds=8, simds=1024):
+    per = collections.defaultdict(lambda: collections.defaultdict(float))
+    names, dur = {}, {}
+    for r in csv.DictReader(open(src)):
+        key = r["Dispatch_Id"]
+        per[key][r["Counter_Name"]] += float(r["Counter_Value"])
+        names[key] = _short(r["Kernel_Name"])
+        dur[key] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+    by = collections.defaultdict(list)
+    for key, v in per.items():
+        if v.get("SQ_INSTS_VALU_MFMA_MOPS_F8", 0.0) <= 0.0:
+            continue
+        cycles = v["GRBM_GUI_ACTIVE"] / xcds
+        by[names[key]].append((dur[key], v["SQ_INSTS_VALU_MFMA_MOPS_F8"] * 512.0,
+                               v["SQ_VALU_MFMA_BUSY_CYCLES"] / (cycles * simds), cycles / dur[key]))
+    sha = hashlib.sha256(open(source, "rb").read()).hexdigest()
+    with open(dst, "w") as f:
+        f.write("# FP8 MFMA activity per launch: rocprofv3 SQ_INSTS_VALU_MFMA_MOPS_F8 (x 512 = FP8\n"
+                "# operations), SQ_VALU_MFMA_BUSY_CYCLES over the SIMD cycles, GRBM_GUI_ACTIVE over\n"
+                f"# the {xcds} XCDs for the clock.\n")
+        f.write(f"command: {cmd}\nkernel_source: {source}\nkernel_source_sha256: {sha}\n")
+        f.write("| kernel | launches | avg (us) | FP8 ops per launch | TFLOP/s | MFMA busy | clock (GHz) |\n")
+        f.write("|---|---|---|---|---|---|---|\n")
+        for k in sorted(by):
+            xs = by[k]
+            n = len(xs)
+            d = sum(x[0] for x in xs) / n
+            fl = sum(x[1] for x in xs) / n
+            f.write(f"| {k} | {n} | {d * 1e6:.1f} | {fl:.4g} | {fl / d / 1e12:.0f} | "
+                    f"{100 * sum(x[2] for x in xs) / n:.1f}% | {sum(x[3] for x in xs) / n / 1e9:.2f} |\n")
+
+
 def main(argv):
     if argv[0] == "stats":
         stats(*argv[1:5])
     elif argv[0] == "traffic":
         traffic(argv[1], argv[2], argv[3], argv[4], int(argv[5]), argv[6], argv[7], argv[8])
+    elif argv[0] == "mfma":
+        mfma(*argv[1:5])
     else:
         raise SystemExit(__doc__)
 
