@@ -148,7 +148,7 @@ enum {
   OZ2_Q_PLANES = 6,        /* uint8 planes of A [p_store][m][k] then of B [p_store][n][k] */
   OZ2_Q_RESIDUES = 7,      /* int16 [r][n][m] centred residues (after residue_gemm) */
   OZ2_Q_INTEGERS = 8,      /* uint32 [n][m][5]: exact integer, two's complement, 160 bits LE */
-  OZ2_Q_FALLBACK_COUNT = 9 /* int32 [2]: flagged rows of A, flagged columns of B */
+  OZ2_Q_FALLBACK_COUNT = 9 /* int32 [2]: rows of A, columns of B the reconstruction recomputes natively */
 };
 size_t ozaki2_plan_query_bytes(ozaki2_plan_t plan, int what);
 int ozaki2_plan_query(ozaki2_plan_t plan, int what, void* host_out, size_t bytes);

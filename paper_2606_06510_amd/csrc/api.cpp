@@ -297,6 +297,7 @@ struct ozaki2_plan_s {
   int lda = 0, ldb = 0;
   int stage = 0;      // 0 created, 1 deconstructed, 2 residues ready, 3 reconstructed
   int sides = 0;      // operands whose planes are in the workspace (OZ2_SIDE_A | OZ2_SIDE_B)
+  bool tables = false;   // residue -> plane-byte tables built in the workspace (they depend on r only)
 };
 
 namespace {
@@ -306,9 +307,10 @@ namespace {
 // the other operand (no max-magnitude pass).
 int run_deconstruct(ozaki2_plan_s& p, int side, hipStream_t s) {
   const Oz2Dims& d = p.d;
-  // Each operand's second read follows its first directly, and B's planes are
-  // split before A's, so that the re-reads find A or B still in the 256 MiB
-  // memory-side cache where they fit.
+  // Each operand's second read (codes) follows its first (scan) directly, and
+  // both operands are split in one launch, B's tiles first, so that the
+  // re-reads find A or B still in the 256 MiB memory-side cache where they
+  // fit.
   const bool codes = !(d.flags & OZ2_SCALE_FIXED);
   hipError_t e = oz2_launch_init(d, p.L, p.ws, side, s);
   for (int one : {OZ2_SIDE_A, OZ2_SIDE_B}) {
@@ -319,10 +321,11 @@ int run_deconstruct(ozaki2_plan_s& p, int side, hipStream_t s) {
   }
   if (codes && e == hipSuccess) e = oz2_launch_codegemm(d, p.L, p.ws, s);
   if (e == hipSuccess) e = oz2_launch_scales(d, p.L, p.c, p.ws, side, s);
-  if (e == hipSuccess) e = oz2_launch_tables(p.L, p.c, p.ws, s);
-  for (int one : {OZ2_SIDE_B, OZ2_SIDE_A})
-    if ((side & one) && e == hipSuccess)
-      e = oz2_launch_split(d, p.L, p.c, p.ws, p.A, p.lda, p.B, p.ldb, one, s);
+  if (e == hipSuccess && !p.tables) {
+    e = oz2_launch_tables(p.L, p.c, p.ws, s);
+    p.tables = e == hipSuccess;
+  }
+  if (e == hipSuccess) e = oz2_launch_split(d, p.L, p.c, p.ws, p.A, p.lda, p.B, p.ldb, side, s);
   return hip_status(e);
 }
 
@@ -614,9 +617,7 @@ int ozaki2_plan_query(ozaki2_plan_t p, int what, void* host_out, size_t bytes) {
   if (!p || !host_out) return OZ2_E_INVALID;
   const size_t need = ozaki2_plan_query_bytes(p, what);
   if (need == 0 || bytes < need) return OZ2_E_INVALID;
-  const int needs_stage = (what == OZ2_Q_RESIDUES || what == OZ2_Q_INTEGERS) ? 2
-                          : (what == OZ2_Q_FALLBACK_COUNT)                    ? 3
-                                                                              : 1;
+  const int needs_stage = (what == OZ2_Q_RESIDUES || what == OZ2_Q_INTEGERS) ? 2 : 1;
   if (p->stage < needs_stage) return OZ2_E_INVALID;
   if (hipDeviceSynchronize() != hipSuccess) return OZ2_E_DEVICE;
   const Oz2Dims& d = p->d;

@@ -95,13 +95,8 @@ template <int R>
 __global__ void __launch_bounds__(256)
 k_reconstruct(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res,
               const int32_t* __restrict__ sA, const int32_t* __restrict__ tB,
-              const uint32_t* __restrict__ fA, const uint32_t* __restrict__ fB, double* C, int ldc,
-              int* counters) {
+              const uint32_t* __restrict__ fA, const uint32_t* __restrict__ fB, double* C, int ldc) {
   __shared__ double tr[2][32][33];
-  // the fallback lists of this reconstruction start empty (they are filled
-  // by the next kernel on the stream, so a repeated reconstruction of the
-  // same residues rebuilds them instead of appending)
-  if (blockIdx.x == 0 && threadIdx.x < 4) counters[threadIdx.x] = 0;
   const BlockMap b = block_map(d.mp);
   {
     uint4 x[R];
@@ -168,19 +163,6 @@ k_integers(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res, uint32_t* out
 
 // Compaction of flagged rows / columns into index lists (order irrelevant:
 // every flagged entry is computed independently and deterministically).
-__global__ void k_fallback_lists(Oz2Dims d, const uint32_t* __restrict__ fA,
-                                 const uint32_t* __restrict__ fB, int* counters, int* listA,
-                                 int* listB) {
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  const bool force = (d.flags & 16u) != 0;
-  if (idx < d.m) {
-    if (force || (fA[idx] & (OZ2_T1 | OZ2_T2))) listA[atomicAdd(counters + 0, 1)] = idx;
-  } else if (idx < d.m + d.n) {
-    const int j = idx - d.m;
-    if (!force && (fB[j] & (OZ2_T1 | OZ2_T2))) listB[atomicAdd(counters + 1, 1)] = j;
-  }
-}
-
 // Native FP64 for flagged entries: one FMA per k in ascending k for every
 // output (the same order as a plain dot product loop), register-tiled so the
 // flagged rows run at FP64 FMA speed.  Work = (flagged rows of A) x (all
@@ -290,7 +272,7 @@ void launch_reconstruct_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& 
   hipLaunchKernelGGL(k_reconstruct<R>, dim3((unsigned)blocks), dim3(256), 0, s, c, d,
                      (const int16_t*)(ws + L.res), (const int32_t*)(ws + L.sA),
                      (const int32_t*)(ws + L.tB), (const uint32_t*)(ws + L.flagsA),
-                     (const uint32_t*)(ws + L.flagsB), C, ldc, (int*)(ws + L.counters));
+                     (const uint32_t*)(ws + L.flagsB), C, ldc);
 }
 
 template <int R>
@@ -333,12 +315,7 @@ hipError_t oz2_launch_integers(const Oz2Dims& d, const Oz2Layout& L, const Oz2Co
 hipError_t oz2_launch_fallback(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, const double* A,
                                int lda, const double* B, int ldb, double* C, int ldc,
                                hipStream_t s) {
-  const unsigned lb = (unsigned)((d.m + d.n + 255) / 256);
-  hipLaunchKernelGGL(k_fallback_lists, dim3(lb), dim3(256), 0, s, d,
-                     (const uint32_t*)(ws + L.flagsA), (const uint32_t*)(ws + L.flagsB),
-                     (int*)(ws + L.counters), (int*)(ws + L.listA), (int*)(ws + L.listB));
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  // the lists were filled by the deconstruction (k_scales: T1, k_split: T2)
   hipLaunchKernelGGL(k_fallback, dim3(1024), dim3(256), 0, s, d, A, lda, B, ldb, C, ldc,
                      (const int*)(ws + L.counters), (const int*)(ws + L.listA),
                      (const int*)(ws + L.listB), (const uint32_t*)(ws + L.flagsA));

@@ -253,10 +253,11 @@ def test_subnormal_and_overflowing_results():
     compare_all(plan, C, A, B, 12, res)
 
 
-def test_repeated_reconstruct_rebuilds_fallback_lists():
-    """A plan may reconstruct its residues more than once; each time the
-    flagged-row lists are rebuilt from empty (more than half the rows are
-    flagged here, so lists that kept growing would overrun their m entries)."""
+def test_repeated_reconstruct_keeps_fallback_lists():
+    """A plan may reconstruct its residues more than once; the flagged-row
+    lists the deconstruction built stay as they are (more than half the rows
+    are flagged here, so lists that grew per reconstruction would overrun
+    their m entries)."""
     import paper_2606_06510_amd as oz
     import torch
     m, n, k = 200, 150, 100
