@@ -710,9 +710,15 @@ int ozaki2_plan_query(ozaki2_plan_t p, int what, void* host_out, size_t bytes) {
           if (col >= d.n) continue;
           for (int e = 0; e < 16; ++e) {
             const int rr = row + 8 * (e >> 2) + (e & 3);
-            if (rr < d.m)
-              o[((size_t)i * d.n + col) * d.m + rr] =
-                  raw[(size_t)i * plane + tile * (OZ2_TILE * OZ2_TILE) + (size_t)q * 16 + e];
+            if (rr < d.m) {
+              // the workspace holds a representative of magnitude <= m/2 + 32;
+              // the query returns the centred residue in [-floor(m/2), ceil(m/2) - 1]
+              const int mi = p->c.m[i];
+              int v = raw[(size_t)i * plane + tile * (OZ2_TILE * OZ2_TILE) + (size_t)q * 16 + e];
+              v = ((v % mi) + mi) % mi;
+              if (v >= (mi + 1) / 2) v -= mi;
+              o[((size_t)i * d.n + col) * d.m + rr] = (int16_t)v;
+            }
           }
         }
       return OZ2_OK;

@@ -8,7 +8,8 @@
 //    d0e0 with coefficient 1) or Eq. (kar) with b = 4 (nonsquare: d1e1 with
 //    240, d0e0 with -15, (d0+d1)(e0+e1) with 16), accumulated exactly in FP32
 //    (Eq. (accum-exact): every partial sum is an integer of magnitude
-//    <= 2^24 for k <= 32768), then reduced to the centred residue.
+//    <= 2^24 for k <= 32768), then reduced mod m (to a representative of
+//    magnitude <= m/2 + 32; see the epilogue).
 //
 // Design.  One workgroup (8 waves, 2 per SIMD) owns a 256x256 output tile;
 // wave w owns 128x64 of it (4x2 MFMA tiles of 32x32, 128 FP32 accumulators
@@ -173,16 +174,6 @@ __device__ __forceinline__ int tile_of(int b, int ntm, int ntn) {
   const int gid = grp * 8 + xcd, ngx = ntm / 4;
   const int gm = gid % ngx, gn = gid / ngx;
   return (gm * 4 + (in & 3)) + (gn * 8 + (in >> 2)) * ntm;
-}
-
-// Centred residue in [-floor(m/2), ceil(m/2) - 1] of an integer-valued x with
-// |x| <= m: x * RN(1/m) is within 2^-23 of x / m, which is either a
-// half-integer (even m, x = +-m/2) or at least 1/(2m) away from one, so rint
-// picks the exact nearest quotient; of the two ties, +m/2 (hm; 0.5 for odd m,
-// never hit) is mapped to -m/2.
-__device__ __forceinline__ float centre_small(float x, float fm, float inv, float hm) {
-  const float r = __builtin_fmaf(-rintf(x * inv), fm, x);
-  return r == hm ? -hm : r;
 }
 
 // Wait until this wave's DMA share of stage s has landed.  When it waits
@@ -443,15 +434,18 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
     }
     it += 3 * nk;
 
-    // epilogue: centred residue of fin * acc (+ the previous slab's), in
-    // fp32 throughout.  acc is an integer with |acc| <= 2^24 and fin is 1 or
-    // 16, so v = fin * acc is exact.  v * RN(1/m) is within
+    // epilogue: a representative of fin * acc (+ the previous slab's) mod m,
+    // in fp32 throughout.  acc is an integer with |acc| <= 2^24 and fin is 1
+    // or 16, so v = fin * acc is exact.  v * RN(1/m) is within
     // 2 * 2^-24 |v| / m <= 32 / m of v / m (the relative errors of RN(1/m)
     // and of the product), so v - m rint(.) is an exact integer of magnitude
-    // <= m/2 + 32 < m (every modulus exceeds 64); centre_small then rounds
-    // once more, now exactly.
+    // <= m/2 + 32: stored as it is.  The reconstruction's exact CRT sum takes
+    // any representative of that size (its limb sums stay below 2^53 for
+    // |x| <= 1365), so the canonical centring (one more rounding per output)
+    // is left to the diagnostic residue query.  With a previous slab, the sum
+    // (|.| <= m + 64) is reduced once more: its quotient estimate is then
+    // within 2^-22 of the exact one, so the result lies in [-m/2, m/2].
     const float ffin = (float)c.fin[mi];
-    const float hm = (m & 1) ? 0.5f : 0.5f * fm;   // even m: +m/2 is not canonical
     int16_t* dst = res + (size_t)mi * mp * np + (size_t)tile * (TILE * TILE) + (size_t)w * 8192 +
                    lane * 16;
     uint32_t pk[4][2][8];
@@ -463,7 +457,7 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const float v = acc[i][j][e] * ffin;
-          r16[e] = centre_small(__builtin_fmaf(-rintf(v * inv), fm, v), fm, inv, hm);
+          r16[e] = __builtin_fmaf(-rintf(v * inv), fm, v);
         }
         if (accumulate) {
           const uint4* p = reinterpret_cast<const uint4*>(dst + (i * 2 + j) * 1024);
@@ -472,7 +466,8 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
             const int old = (int)(int16_t)((ow[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
-            r16[e] = centre_small(r16[e] + (float)old, fm, inv, hm);
+            const float t = r16[e] + (float)old;
+            r16[e] = __builtin_fmaf(-rintf(t * inv), fm, t);
           }
         }
 #pragma unroll

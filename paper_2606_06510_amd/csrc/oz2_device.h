@@ -92,7 +92,8 @@ __device__ __forceinline__ void normalise(double (&S)[NW]) {
   }
 }
 
-// Exact integer of output I of a thread from its R centred residues:
+// Exact integer of output I of a thread from its R residues (any
+// representatives of magnitude <= 577):
 // NW words, two's complement, little endian.
 template <int R, int NW, int I>
 __device__ __forceinline__ void crt_words(const Oz2Const& c, const uint4 (&x)[R],
@@ -107,7 +108,7 @@ __device__ __forceinline__ void crt_words(const Oz2Const& c, const uint4 (&x)[R]
     for (int j = 0; j < NW; ++j) S[j] = fma(xi, c.W[i][j], S[j]);
   }
   // quotient estimate q = rint(X / M) from the three top (unnormalised)
-  // limbs: |S_j| < 2^45, |X/M| <= sum |x_i| < 2^13, so the estimate of X/M
+  // limbs: |S_j| < 2^46, |X/M| <= sum |x_i| < 2^14, so the estimate of X/M
   // is within 2^-36 of the true value; only within that of +-1/2 can q be
   // off by one, and an exact range check below settles those.
   double f = fma(S[NW - 2], 0x1p-32, S[NW - 1]);
@@ -227,8 +228,9 @@ __device__ __forceinline__ double round_scaled(const uint32_t (&x)[NW], int e) {
 // ---- r <= 12: the exact integer in three radix-2^38 fp64 limbs ----------
 // X = S2 2^76 + S1 2^38 + S0 with S0, S1 in [0, 2^38) after normalisation
 // and S2 signed; [-M/2, M/2) fits (log2 M < 113).  Every limb sum is an
-// integer below 2^52 (|x_i| <= 545, limbs of W_i and M below 2^38, at most
-// 12 terms plus the q M correction), so the fp64 arithmetic is exact.
+// integer below 2^52 (|x_i| <= 577, limbs of W_i and M below 2^38, at most
+// 12 terms plus the q M correction with |q| <= sum |x_i|), so the fp64
+// arithmetic is exact.
 __device__ __forceinline__ void normalise38(double& S0, double& S1, double& S2) {
   double cy = floor(S0 * 0x1p-38);
   S0 = fma(-cy, 0x1p38, S0);
@@ -270,7 +272,7 @@ __device__ __forceinline__ double round38(double S0, double S1, double S2, int e
   return ldexp(v, sh - e);
 }
 
-// C~ of output I of a thread (R <= 12 centred residues) rounded with the
+// C~ of output I of a thread (R <= 12 residues, |x_i| <= 577) rounded with the
 // exponent shift -e: the direct CRT sum in radix-2^38 limbs, the quotient
 // q = rint(X/M) from the top limbs (within 2^-36 of X/M), the exact range
 // check for the ambiguous case, then round38.

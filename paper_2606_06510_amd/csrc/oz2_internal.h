@@ -68,7 +68,8 @@ struct Oz2Layout {
   size_t codesA, codesB;      // uint8 [kp/64][mp][64] / [kp/64][np][64] (K-blocked)
   size_t planesA, planesB;    // uint8 [P][kp/64][mp][64] / [P][kp/64][np][64] (K-blocked)
   size_t tabs;                // uint32 [tabsz]: E4M3 plane bytes of every centred residue
-  size_t res;                 // int16 [r][tile][wave 8][x 4][y 2][lane 64][16]
+  size_t res;                 // int16 [r][tile][wave 8][x 4][y 2][lane 64][16]: per modulus a
+                              //   representative of C~ mod m_i of magnitude <= m_i/2 + 32
                               //   (the GEMM's accumulator order, see gemm.hip)
   size_t counters;            // int32 [4]: fallback row / column counts
   size_t listA, listB;        // int32 [mp] / [np]: flagged row / column indices
