@@ -228,6 +228,8 @@ Oz2Layout make_layout(const Oz2Dims& d, const Oz2Const& c) {
   L.listB = take((size_t)d.np * 4);
   L.codesA = take((size_t)d.mp * d.kp);
   L.codesB = take((size_t)d.np * d.kp);
+  L.etA = take((size_t)d.mp * (d.kp / 64) * 2);
+  L.etB = take((size_t)d.np * (d.kp / 64) * 2);
   L.planesA = take((size_t)c.P * d.mp * d.kp);
   L.planesB = take((size_t)c.P * d.np * d.kp);
   L.tabs = take((size_t)c.tabsz * 4);
@@ -307,18 +309,17 @@ namespace {
 // the other operand (no max-magnitude pass).
 int run_deconstruct(ozaki2_plan_s& p, int side, hipStream_t s) {
   const Oz2Dims& d = p.d;
-  // Each operand's second read (codes) follows its first (scan) directly, and
+  // Each operand is read once for its scan and code bytes (one kernel), and
   // both operands are split in one launch, B's tiles first, so that the
-  // re-reads find A or B still in the 256 MiB memory-side cache where they
-  // fit.
+  // second read finds B (read last) still in the 256 MiB memory-side cache.
   const bool codes = !(d.flags & OZ2_SCALE_FIXED);
   hipError_t e = oz2_launch_init(d, p.L, p.ws, side, s);
   for (int one : {OZ2_SIDE_A, OZ2_SIDE_B}) {
-    if (!(side & one)) continue;
-    if (e == hipSuccess) e = oz2_launch_scan(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, one, s);
-    if (codes && e == hipSuccess)
-      e = oz2_launch_codes(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, one, s);
+    if (!(side & one) || e != hipSuccess) continue;
+    e = codes ? oz2_launch_scan_codes(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, one, s)
+              : oz2_launch_scan(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, one, s);
   }
+  if (codes && e == hipSuccess) e = oz2_launch_rebase(d, p.L, p.ws, side, s);
   if (codes && e == hipSuccess) e = oz2_launch_codegemm(d, p.L, p.ws, s);
   if (e == hipSuccess) e = oz2_launch_scales(d, p.L, p.c, p.ws, side, s);
   if (e == hipSuccess && !p.tables) {

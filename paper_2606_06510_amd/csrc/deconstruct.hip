@@ -180,26 +180,53 @@ __device__ __forceinline__ void take_cols(const double* tile, bool zero, double 
   }
 }
 
-// Codes of A (rows contiguous in memory).  A tile of 64 rows x 64 k per
-// workgroup: thread t reads rows 2(t%32), 2(t%32)+1 of columns t/32 + 8j with
-// 16-byte loads (each wave instruction covers 512 contiguous bytes of two
-// columns), converts them to code bytes, and the 64 x 64 bytes are transposed
-// through LDS so that each thread stores 16 consecutive k of one row.
-__global__ void __launch_bounds__(256) k_codes_rows(const double* __restrict__ X, int ld, int rows,
-                                                    int nrb, int k, int kp,
-                                                    const unsigned long long* __restrict__ bits,
-                                                    uint8_t* __restrict__ codes, unsigned vec) {
+// Codes for the max-magnitude pass, in two steps so that each operand's FP64
+// input is read once here (the scan and the codes share the read):
+//
+// 1. k_scan_codes_rows / _cols (one 64x64 tile of 64 rows or columns x 64 k
+//    per workgroup): the tile-row maxima of |x| (folded into the row maxima
+//    with atomicMax), their frexp exponents Et (int16 [k/64][rows]), and per
+//    element a byte relative to Et, stored in the K-blocked codes layout:
+//      bit 7: x != 0;  bits 4..6: min(Et - e, 4);  bit 3: sticky;
+//      bits 0..2: floor(16 f) - 8,   where |x| = f 2^e, f in [1/2, 1),
+//    the sticky bit telling whether 16 f has bits below its integer part.
+// 2. k_rebase (both operands, one launch, in place): with E the exponent of
+//    the whole row's maximum and d = min(E - Et + (E_t - e), 4) = min(E - e, 4),
+//    the code ceil(16 |x| 2^-E) = ceil((q + rho) 2^-d), q = floor(16 f) in
+//    [8, 15], rho in [0, 1), is q + sticky for d = 0, 1 for d >= 4 (x != 0),
+//    else floor(q / 2^d) + 1 if q mod 2^d or sticky is nonzero, q / 2^d if not:
+//    exactly the code of code_of(), from the byte alone (the three cases are
+//    (q + 2^d - 1 + sticky) >> d).  T1 rows (a NaN or Inf entry) get codes 0,
+//    as before.
+__device__ __forceinline__ uint32_t local_code(unsigned long long b, int Et) {
+  if (b == 0) return 0u;
+  const int e = exp_of_bits(b);
+  // mantissa of |x| normalised to the implicit-one position (subnormals shifted up)
+  const unsigned long long mb =
+      (b >> 52) ? b : (b << (__clzll((long long)b) - 11));
+  const unsigned long long man = mb & 0xFFFFFFFFFFFFFull;
+  const uint32_t q3 = (uint32_t)(man >> 49);                   // floor(16 f) - 8
+  const uint32_t st = (man & 0x1FFFFFFFFFFFFull) ? 8u : 0u;     // bits of 16 f below 1
+  const int dt = min(Et - e, 4);
+  return 0x80u | ((uint32_t)dt << 4) | st | q3;
+}
+
+// Rows of A (contiguous along the row index): thread t reads rows 2(t%32),
+// 2(t%32)+1 of k = t/32 + 8j (j < 8) with 16-byte loads (each wave
+// instruction covers 512 contiguous bytes of two columns); the 64 x 64 bytes
+// are transposed through LDS so that each thread stores 16 consecutive k of
+// one row.
+__global__ void __launch_bounds__(256) k_scan_codes_rows(const double* __restrict__ X, int ld,
+                                                         int rows, int nrb, int k, unsigned vec,
+                                                         unsigned long long* bits, int16_t* et,
+                                                         uint8_t* __restrict__ codes) {
   __shared__ __attribute__((aligned(16))) uint8_t T[64][80];
+  __shared__ unsigned long long mx[8][64];
   const int rows_pad = nrb * 64;
   const int t = threadIdx.x;
   const int bx = (int)(blockIdx.x % (unsigned)nrb), by = (int)(blockIdx.x / (unsigned)nrb);
   const int p = t & 31, g = t >> 5;
   const int r0 = bx * 64 + 2 * p, lbase = by * 64;
-  const unsigned long long b0 = r0 < rows ? bits[r0] : 0ull;
-  const unsigned long long b1 = r0 + 1 < rows ? bits[r0 + 1] : 0ull;
-  const bool z0 = b0 >= kInfBits, z1 = b1 >= kInfBits;   // T1 rows: codes 0
-  const int E0 = (b0 == 0 || z0) ? 0 : exp_of_bits(b0);
-  const int E1 = (b1 == 0 || z1) ? 0 : exp_of_bits(b1);
   double2 v[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
@@ -215,14 +242,32 @@ __global__ void __launch_bounds__(256) k_codes_rows(const double* __restrict__ X
       }
     }
   }
+  unsigned long long m0 = 0, m1 = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    m0 = max(m0, abs_bits(v[j].x));
+    m1 = max(m1, abs_bits(v[j].y));
+  }
+  mx[g][2 * p] = m0;
+  mx[g][2 * p + 1] = m1;
+  __syncthreads();
+  if (t < 64) {
+    unsigned long long m = mx[0][t];
+#pragma unroll
+    for (int u = 1; u < 8; ++u) m = max(m, mx[u][t]);
+    const int row = bx * 64 + t;
+    if (row < rows && m) atomicMax(bits + row, m);
+    et[(size_t)by * rows_pad + row] = (int16_t)(m ? exp_of_bits(m) : 0);
+    mx[0][t] = m;   // only thread t reads column t of mx
+  }
+  __syncthreads();
+  const unsigned long long t0 = mx[0][2 * p], t1 = mx[0][2 * p + 1];
+  const int E0 = t0 ? exp_of_bits(t0) : 0, E1 = t1 ? exp_of_bits(t1) : 0;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int c = g + 8 * j;
-    const float c0 = z0 ? 0.0f : code_of(v[j].x, E0);
-    const float c1 = z1 ? 0.0f : code_of(v[j].y, E1);
-    const uint32_t w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c0, c1, 0, false);
-    T[2 * p][c] = (uint8_t)(w & 0xFFu);
-    T[2 * p + 1][c] = (uint8_t)((w >> 8) & 0xFFu);
+    T[2 * p][c] = (uint8_t)local_code(abs_bits(v[j].x), E0);
+    T[2 * p + 1][c] = (uint8_t)local_code(abs_bits(v[j].y), E1);
   }
   __syncthreads();
   const int row = bx * 64 + (t >> 2), l0 = lbase + (t & 3) * 16;
@@ -230,28 +275,25 @@ __global__ void __launch_bounds__(256) k_codes_rows(const double* __restrict__ X
   *reinterpret_cast<uint4*>(codes + kblocked(row, l0, rows_pad)) = o;
 }
 
-// Codes of B (columns contiguous).  A tile of 64 columns x 64 k per
-// workgroup: thread t reads k 2(t%32), 2(t%32)+1 of columns t/32 + 8j with
-// 16-byte loads (512 contiguous bytes of one column per half-wave
-// instruction); the code bytes are transposed through LDS as for A.
-__global__ void __launch_bounds__(256) k_codes_cols(const double* __restrict__ X, int ld, int rows,
-                                                    int nrb, int k, int kp,
-                                                    const unsigned long long* __restrict__ bits,
-                                                    uint8_t* __restrict__ codes, unsigned vec) {
+// Columns of B (contiguous along k): thread t reads k 2(t%32), 2(t%32)+1 of
+// columns t/32 + 8j with 16-byte loads (512 contiguous bytes of one column per
+// half-wave instruction); a column's tile maximum is a max-reduction over the
+// 32 lanes of a half-wave; the bytes are transposed through LDS as for A.
+__global__ void __launch_bounds__(256) k_scan_codes_cols(const double* __restrict__ X, int ld,
+                                                         int rows, int nrb, int k, unsigned vec,
+                                                         unsigned long long* bits, int16_t* et,
+                                                         uint8_t* __restrict__ codes) {
   __shared__ __attribute__((aligned(16))) uint8_t T[64][80];
   const int rows_pad = nrb * 64;
   const int t = threadIdx.x;
   const int bx = (int)(blockIdx.x % (unsigned)nrb), by = (int)(blockIdx.x / (unsigned)nrb);
-  const int kk = 2 * (t & 31), g = t >> 5;
+  const int p = t & 31, kk = 2 * p, g = t >> 5;
   const int l = by * 64 + kk;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int cc = g + 8 * j, col = bx * 64 + cc;
-    const unsigned long long b = col < rows ? bits[col] : 0ull;
-    const bool z = b >= kInfBits;   // T1 columns: codes 0
-    const int E = (b == 0 || z) ? 0 : exp_of_bits(b);
     double2 v = make_double2(0.0, 0.0);
-    if (col < rows && !z) {
+    if (col < rows) {
       const double* q = X + (size_t)col * ld + l;
       if (vec && l + 1 < k) {
         v = *reinterpret_cast<const double2*>(q);
@@ -260,14 +302,78 @@ __global__ void __launch_bounds__(256) k_codes_cols(const double* __restrict__ X
         if (l + 1 < k) v.y = q[1];
       }
     }
-    const uint32_t w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(code_of(v.x, E), code_of(v.y, E), 0,
-                                                                 false);
-    *reinterpret_cast<uint16_t*>(&T[cc][kk]) = (uint16_t)(w & 0xFFFFu);
+    const unsigned long long a0 = abs_bits(v.x), a1 = abs_bits(v.y);
+    unsigned long long m = max(a0, a1);
+#pragma unroll
+    for (int off = 16; off; off >>= 1)
+      m = max(m, (unsigned long long)__shfl_xor((long long)m, off, 32));
+    if (p == 0) {
+      if (col < rows && m) atomicMax(bits + col, m);
+      et[(size_t)by * rows_pad + col] = (int16_t)(m ? exp_of_bits(m) : 0);
+    }
+    const int E = m ? exp_of_bits(m) : 0;
+    const uint32_t w = local_code(a0, E) | (local_code(a1, E) << 8);
+    *reinterpret_cast<uint16_t*>(&T[cc][kk]) = (uint16_t)w;
   }
   __syncthreads();
   const int row = bx * 64 + (t >> 2), l0 = by * 64 + (t & 3) * 16;
   const uint4 o = *reinterpret_cast<const uint4*>(&T[t >> 2][(t & 3) * 16]);
   *reinterpret_cast<uint4*>(codes + kblocked(row, l0, rows_pad)) = o;
+}
+
+// code of one byte of step 1 given D = E - Et: with d = min(D + dt, 4), the
+// ceiling above is (q + 2^d - 1 + sticky) >> d for every d in [0, 4]
+__device__ __forceinline__ float rebase_code(uint32_t y, int D) {
+  const int d = min(D + (int)((y >> 4) & 7u), 4);
+  const int c = (7 + (int)(y & 7u) + (int)((y >> 3) & 1u) + (1 << d)) >> d;
+  return (y & 0x80u) ? (float)c : 0.0f;
+}
+
+__device__ __forceinline__ uint32_t rebase_word(uint32_t w, int D) {
+  return pack4_fp8(rebase_code(w & 0xFFu, D), rebase_code((w >> 8) & 0xFFu, D),
+                   rebase_code((w >> 16) & 0xFFu, D), rebase_code(w >> 24, D));
+}
+
+// Step 2 for both operands, in place: one thread per 64-byte row segment of
+// one k-block (threads [0, nA) on A, then B), four 16-byte loads in flight.
+__global__ void __launch_bounds__(256) k_rebase(uint8_t* codesA, const int16_t* __restrict__ etA,
+                                                const unsigned long long* __restrict__ bitsA,
+                                                int mp, size_t nA, uint8_t* codesB,
+                                                const int16_t* __restrict__ etB,
+                                                const unsigned long long* __restrict__ bitsB,
+                                                int np, size_t nB) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  uint8_t* codes = codesA;
+  const int16_t* et = etA;
+  const unsigned long long* bits = bitsA;
+  int rp = mp;
+  if (i >= nA) {
+    i -= nA;
+    if (i >= nB) return;
+    codes = codesB;
+    et = etB;
+    bits = bitsB;
+    rp = np;
+  }
+  // segment i = (k-block, row): et is [k/64][rows], the codes [k/64][rows][64]
+  // every load first (one round of latency), then the arithmetic
+  const int row = (int)(i % (size_t)rp);
+  uint4* q = reinterpret_cast<uint4*>(codes) + 4 * i;
+  uint4 y[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) y[u] = q[u];
+  const unsigned long long b = bits[row];
+  const int et_i = (int)et[i];
+  if (b == 0 || b >= kInfBits) {   // all-zero row, or T1: codes 0
+#pragma unroll
+    for (int u = 0; u < 4; ++u) q[u] = make_uint4(0u, 0u, 0u, 0u);
+    return;
+  }
+  const int D = exp_of_bits(b) - et_i;
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+    q[u] = make_uint4(rebase_word(y[u].x, D), rebase_word(y[u].y, D), rebase_word(y[u].z, D),
+                      rebase_word(y[u].w, D));
 }
 
 __global__ void k_scales(Oz2Dims d, const unsigned long long* __restrict__ rowbits,
@@ -481,20 +587,36 @@ hipError_t oz2_launch_scan(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, co
   return hipGetLastError();
 }
 
-hipError_t oz2_launch_codes(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, const double* A,
-                            int lda, const double* B, int ldb, int side, hipStream_t s) {
+hipError_t oz2_launch_scan_codes(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
+                                 const double* A, int lda, const double* B, int ldb, int side,
+                                 hipStream_t s) {
   if (side & OZ2_SIDE_A) {
     dim3 ga((d.mp / 64) * (d.kp / 64));
     const unsigned vecA = ((uintptr_t)A % 16 == 0 && lda % 2 == 0) ? 1u : 0u;
-    hipLaunchKernelGGL(k_codes_rows, ga, dim3(256), 0, s, A, lda, d.m, d.mp / 64, d.k, d.kp,
-                       (const unsigned long long*)(ws + L.rowbits), ws + L.codesA, vecA);
+    hipLaunchKernelGGL(k_scan_codes_rows, ga, dim3(256), 0, s, A, lda, d.m, d.mp / 64, d.k, vecA,
+                       (unsigned long long*)(ws + L.rowbits), (int16_t*)(ws + L.etA),
+                       ws + L.codesA);
   }
   if (side & OZ2_SIDE_B) {
     dim3 gb((d.np / 64) * (d.kp / 64));
     const unsigned vecB = ((uintptr_t)B % 16 == 0 && ldb % 2 == 0) ? 1u : 0u;
-    hipLaunchKernelGGL(k_codes_cols, gb, dim3(256), 0, s, B, ldb, d.n, d.np / 64, d.k, d.kp,
-                       (const unsigned long long*)(ws + L.colbits), ws + L.codesB, vecB);
+    hipLaunchKernelGGL(k_scan_codes_cols, gb, dim3(256), 0, s, B, ldb, d.n, d.np / 64, d.k, vecB,
+                       (unsigned long long*)(ws + L.colbits), (int16_t*)(ws + L.etB),
+                       ws + L.codesB);
   }
+  return hipGetLastError();
+}
+
+hipError_t oz2_launch_rebase(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, int side,
+                             hipStream_t s) {
+  const size_t nA = (side & OZ2_SIDE_A) ? (size_t)d.mp * (d.kp / 64) : 0;
+  const size_t nB = (side & OZ2_SIDE_B) ? (size_t)d.np * (d.kp / 64) : 0;
+  if (nA + nB == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_rebase, dim3((unsigned)((nA + nB + 255) / 256)), dim3(256), 0, s,
+                     ws + L.codesA, (const int16_t*)(ws + L.etA),
+                     (const unsigned long long*)(ws + L.rowbits), d.mp, nA, ws + L.codesB,
+                     (const int16_t*)(ws + L.etB), (const unsigned long long*)(ws + L.colbits),
+                     d.np, nB);
   return hipGetLastError();
 }
 

@@ -66,6 +66,7 @@ struct Oz2Layout {
   size_t Rmax, Kmax;          // uint32 [cslabs][mp] / [cslabs][np]
   size_t sA, tB;              // int32 [mp] / [np]
   size_t codesA, codesB;      // uint8 [kp/64][mp][64] / [kp/64][np][64] (K-blocked)
+  size_t etA, etB;            // int16 [kp/64][mp] / [kp/64][np]: exponents of the tile-row maxima
   size_t planesA, planesB;    // uint8 [P][kp/64][mp][64] / [P][kp/64][np][64] (K-blocked)
   size_t tabs;                // uint32 [tabsz]: E4M3 plane bytes of every centred residue
   size_t res;                 // int16 [r][tile][wave 8][x 4][y 2][lane 64][16]: per modulus a
@@ -86,9 +87,13 @@ hipError_t oz2_launch_init(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, in
 hipError_t oz2_launch_scan(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
                            const double* A, int lda, const double* B, int ldb, int side,
                            hipStream_t s);
-hipError_t oz2_launch_codes(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
-                            const double* A, int lda, const double* B, int ldb, int side,
-                            hipStream_t s);
+// scan + per-tile code bytes in one read of each operand, then the bytes
+// rebased to the row exponents (the codes of the max-magnitude pass)
+hipError_t oz2_launch_scan_codes(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
+                                 const double* A, int lda, const double* B, int ldb, int side,
+                                 hipStream_t s);
+hipError_t oz2_launch_rebase(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, int side,
+                             hipStream_t s);
 hipError_t oz2_launch_codegemm(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, hipStream_t s);
 hipError_t oz2_launch_scales(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
                              uint8_t* ws, int side, hipStream_t s);
