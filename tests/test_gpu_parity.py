@@ -71,6 +71,35 @@ def test_fallback_rows_and_columns():
     assert plan.query(oz.OZ2_Q_FALLBACK_COUNT) == (3, 2)
 
 
+def test_code_bytes_edge_cases():
+    """The max-magnitude codes are built per 64-wide k-block (a byte relative to
+    the block's own exponent) and rebased to the row's: rows whose blocks sit
+    0..6 binary orders below the row maximum, exact powers of two and
+    mantissas with and without bits below the fourth, subnormal rows and
+    entries, a NaN row; codes, scales and C are compared with the oracle."""
+    rng = np.random.default_rng(23)
+    m, n, k = 70, 66, 450                      # 8 k-blocks, the last ragged
+    A, B = synth.uniform(m, n, k, seed=23)
+    A, B = A.copy(), B.copy()
+    for b in range(8):                         # row 0: block b lies b orders down
+        A[0, 64 * b:64 * (b + 1)] *= 2.0 ** -b
+    A[1] = 2.0 ** rng.integers(-30, 3, k)      # exact powers of two (sticky 0)
+    A[2] = (8 + rng.integers(0, 8, k)) / 16.0 * 2.0 ** rng.integers(-6, 6, k)   # 4-bit mantissas
+    A[2, ::3] *= 1.0 + 2.0 ** -40              # and some with low bits set
+    A[3] = rng.integers(1, 2 ** 40, k) * 2.0 ** -1074      # a subnormal row
+    A[4, ::5] = rng.integers(1, 2 ** 20, (k + 4) // 5) * 2.0 ** -1074   # subnormals in a normal row
+    A[5, 10] = np.nan                          # T1 row: codes 0
+    A[6] = 0.0                                 # zero row
+    A[7, 300:] *= 2.0 ** 9                     # row maximum in a late block
+    for b in range(8):                         # column 0 of B: block b lies 2b orders down
+        B[64 * b:64 * (b + 1), 0] *= 2.0 ** (-2 * b)
+    B[:, 1] = 2.0 ** rng.integers(-10, 10, k)
+    B[:, 2] = rng.integers(1, 2 ** 30, k) * 2.0 ** -1074   # a subnormal column
+    res = oracle.dgemm(A, B, 12)
+    plan, C = run_staged(A, B, 12)
+    compare_all(plan, C, A, B, 12, res, check_integers=False)
+
+
 def test_whole_rows_1e200_absorbed():
     A, B, rows = synth.wide(300, 200, 256, seed=3)
     assert len(rows) > 0
