@@ -199,14 +199,20 @@ __device__ __forceinline__ void take_cols(const double* tile, bool zero, double 
 //    (q + 2^d - 1 + sticky) >> d).  T1 rows (a NaN or Inf entry) get codes 0,
 //    as before.
 __device__ __forceinline__ uint32_t local_code(unsigned long long b, int Et) {
-  if (b == 0) return 0u;
-  const int e = exp_of_bits(b);
-  // mantissa of |x| normalised to the implicit-one position (subnormals shifted up)
-  const unsigned long long mb =
-      (b >> 52) ? b : (b << (__clzll((long long)b) - 11));
-  const unsigned long long man = mb & 0xFFFFFFFFFFFFFull;
-  const uint32_t q3 = (uint32_t)(man >> 49);                   // floor(16 f) - 8
-  const uint32_t st = (man & 0x1FFFFFFFFFFFFull) ? 8u : 0u;     // bits of 16 f below 1
+  uint32_t hi = (uint32_t)(b >> 32);
+  const uint32_t lo = (uint32_t)b;
+  // normal x: every field from the high word and one test of the low one
+  uint32_t q3 = (hi >> 17) & 7u;                          // floor(16 f) - 8
+  uint32_t st = ((hi & 0x1FFFFu) | lo) ? 8u : 0u;         // bits of 16 f below 1
+  int e = (int)(hi >> 20) - 1022;
+  if ((hi >> 20) == 0u) {   // zero or subnormal (rare): normalise the mantissa
+    if ((hi | lo) == 0u) return 0u;
+    const int z = __clzll((long long)b);                  // >= 12
+    const unsigned long long man = (b << (z - 11)) & 0xFFFFFFFFFFFFFull;
+    q3 = (uint32_t)(man >> 49);
+    st = (man & 0x1FFFFFFFFFFFFull) ? 8u : 0u;
+    e = (64 - z) - 1074;
+  }
   const int dt = min(Et - e, 4);
   return 0x80u | ((uint32_t)dt << 4) | st | q3;
 }
@@ -228,17 +234,23 @@ __global__ void __launch_bounds__(256) k_scan_codes_rows(const double* __restric
   const int p = t & 31, g = t >> 5;
   const int r0 = bx * 64 + 2 * p, lbase = by * 64;
   double2 v[8];
+  if (vec && bx * 64 + 64 <= rows && lbase + 64 <= k) {   // interior tile (uniform)
+    const double* q = X + (size_t)(lbase + g) * ld + r0;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int l = lbase + g + 8 * j;
-    v[j] = make_double2(0.0, 0.0);
-    if (l < k) {
-      const double* q = X + (size_t)l * ld + r0;
-      if (vec && r0 + 1 < rows) {
-        v[j] = *reinterpret_cast<const double2*>(q);
-      } else {
-        if (r0 < rows) v[j].x = q[0];
-        if (r0 + 1 < rows) v[j].y = q[1];
+    for (int j = 0; j < 8; ++j) v[j] = *reinterpret_cast<const double2*>(q + (size_t)(8 * j) * ld);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int l = lbase + g + 8 * j;
+      v[j] = make_double2(0.0, 0.0);
+      if (l < k) {
+        const double* q = X + (size_t)l * ld + r0;
+        if (vec && r0 + 1 < rows) {
+          v[j] = *reinterpret_cast<const double2*>(q);
+        } else {
+          if (r0 < rows) v[j].x = q[0];
+          if (r0 + 1 < rows) v[j].y = q[1];
+        }
       }
     }
   }
@@ -286,23 +298,37 @@ __global__ void __launch_bounds__(256) k_scan_codes_cols(const double* __restric
   __shared__ __attribute__((aligned(16))) uint8_t T[64][80];
   const int rows_pad = nrb * 64;
   const int t = threadIdx.x;
-  const int bx = (int)(blockIdx.x % (unsigned)nrb), by = (int)(blockIdx.x / (unsigned)nrb);
+  // k-blocks fastest: consecutive workgroups read consecutive 512-byte pieces
+  // of the same 64 columns (DRAM pages are filled in order)
+  const int nkb = (int)(gridDim.x / (unsigned)nrb);
+  const int by = (int)(blockIdx.x % (unsigned)nkb), bx = (int)(blockIdx.x / (unsigned)nkb);
   const int p = t & 31, kk = 2 * p, g = t >> 5;
   const int l = by * 64 + kk;
+  double2 v[8];
+  if (vec && bx * 64 + 64 <= rows && by * 64 + 64 <= k) {   // interior tile (uniform)
+    const double* q = X + (size_t)(bx * 64 + g) * ld + l;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = *reinterpret_cast<const double2*>(q + (size_t)(8 * j) * ld);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int col = bx * 64 + g + 8 * j;
+      v[j] = make_double2(0.0, 0.0);
+      if (col < rows) {
+        const double* q = X + (size_t)col * ld + l;
+        if (vec && l + 1 < k) {
+          v[j] = *reinterpret_cast<const double2*>(q);
+        } else {
+          if (l < k) v[j].x = q[0];
+          if (l + 1 < k) v[j].y = q[1];
+        }
+      }
+    }
+  }
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int cc = g + 8 * j, col = bx * 64 + cc;
-    double2 v = make_double2(0.0, 0.0);
-    if (col < rows) {
-      const double* q = X + (size_t)col * ld + l;
-      if (vec && l + 1 < k) {
-        v = *reinterpret_cast<const double2*>(q);
-      } else {
-        if (l < k) v.x = q[0];
-        if (l + 1 < k) v.y = q[1];
-      }
-    }
-    const unsigned long long a0 = abs_bits(v.x), a1 = abs_bits(v.y);
+    const unsigned long long a0 = abs_bits(v[j].x), a1 = abs_bits(v[j].y);
     unsigned long long m = max(a0, a1);
 #pragma unroll
     for (int off = 16; off; off >>= 1)
