@@ -355,19 +355,22 @@ __device__ __forceinline__ float rebase_code(uint32_t y, int D) {
   return (y & 0x80u) ? (float)c : 0.0f;
 }
 
-__device__ __forceinline__ uint32_t rebase_word(uint32_t w, int D) {
-  return pack4_fp8(rebase_code(w & 0xFFu, D), rebase_code((w >> 8) & 0xFFu, D),
-                   rebase_code((w >> 16) & 0xFFu, D), rebase_code(w >> 24, D));
-}
-
 // Step 2 for both operands, in place: one thread per 64-byte row segment of
 // one k-block (threads [0, nA) on A, then B), four 16-byte loads in flight.
+// Since d = min(D + dt, 4) depends on D only through min(D, 4), the E4M3 code
+// of every byte for every D is a 5 x 256-byte table, built per workgroup in
+// LDS; a byte then costs a shift, an add and one LDS byte read.
 __global__ void __launch_bounds__(256) k_rebase(uint8_t* codesA, const int16_t* __restrict__ etA,
                                                 const unsigned long long* __restrict__ bitsA,
                                                 int mp, size_t nA, uint8_t* codesB,
                                                 const int16_t* __restrict__ etB,
                                                 const unsigned long long* __restrict__ bitsB,
                                                 int np, size_t nB) {
+  __shared__ uint8_t lut[5 * 256];
+  for (int e = threadIdx.x; e < 5 * 256; e += blockDim.x)
+    lut[e] = (uint8_t)(__builtin_amdgcn_cvt_pk_fp8_f32(rebase_code((uint32_t)(e & 255), e >> 8),
+                                                       0.0f, 0, false) & 0xFF);
+  __syncthreads();
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   uint8_t* codes = codesA;
   const int16_t* et = etA;
@@ -381,8 +384,8 @@ __global__ void __launch_bounds__(256) k_rebase(uint8_t* codesA, const int16_t* 
     bits = bitsB;
     rp = np;
   }
-  // segment i = (k-block, row): et is [k/64][rows], the codes [k/64][rows][64]
-  // every load first (one round of latency), then the arithmetic
+  // segment i = (k-block, row): et is [k/64][rows], the codes [k/64][rows][64];
+  // every load first (one round of latency), then the lookups
   const int row = (int)(i % (size_t)rp);
   uint4* q = reinterpret_cast<uint4*>(codes) + 4 * i;
   uint4 y[4];
@@ -395,11 +398,14 @@ __global__ void __launch_bounds__(256) k_rebase(uint8_t* codesA, const int16_t* 
     for (int u = 0; u < 4; ++u) q[u] = make_uint4(0u, 0u, 0u, 0u);
     return;
   }
-  const int D = exp_of_bits(b) - et_i;
+  const uint8_t* t = lut + 256 * min(exp_of_bits(b) - et_i, 4);
+  auto word = [t](uint32_t w) {
+    return (uint32_t)t[w & 0xFFu] | ((uint32_t)t[(w >> 8) & 0xFFu] << 8) |
+           ((uint32_t)t[(w >> 16) & 0xFFu] << 16) | ((uint32_t)t[w >> 24] << 24);
+  };
 #pragma unroll
   for (int u = 0; u < 4; ++u)
-    q[u] = make_uint4(rebase_word(y[u].x, D), rebase_word(y[u].y, D), rebase_word(y[u].z, D),
-                      rebase_word(y[u].w, D));
+    q[u] = make_uint4(word(y[u].x), word(y[u].y), word(y[u].z), word(y[u].w));
 }
 
 __global__ void k_scales(Oz2Dims d, const unsigned long long* __restrict__ rowbits,
