@@ -23,11 +23,7 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 constexpr int PP = 80;   // bytes per plane row (64 + 16: spreads the LDS banks)
 constexpr int NTB = 512;
 
-constexpr int XP = 66;   // doubles per staged row of A / column of B (64 + 2)
-
 struct Smem {
-  double xa[64][XP];      // the problem's A (row, k) and B (column, k), staged once
-  double xb[64][XP];
   uint8_t pa[3][64][PP];
   uint8_t pb[3][64][PP];
   unsigned long long rbits[64], cbits[64];
@@ -60,24 +56,31 @@ __device__ __forceinline__ v4f mfma(v8i a, v8i b, v4f c) {
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
 
-// 8 plane bytes of this thread's chunk into the planes of modulus i; the
-// chunk (8 consecutive k of one row, already zero for T1 rows) is read from
-// the staged copy in LDS
+// Quantise (Eq. (scale)) the thread's chunk (8 consecutive k of one row,
+// already zero for T1 rows) once per problem: a = rint(x 2^s) = h 2^32 + l
+// with |h| <= 2^30 (|a| <= 2^62) and 0 <= l < 2^32, kept as 32-bit integers.
+__device__ __forceinline__ void quantise8(const double (&x)[8], int sc, bool& t2, int (&h)[8],
+                                          uint32_t (&l)[8]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const double a = rint(ldexp(x[j], sc));
+    t2 |= (x[j] != 0.0) && (a == 0.0);
+    const double hd = floor(a * 0x1p-32);
+    h[j] = (int)hd;
+    l[j] = (uint32_t)fma(-hd, 0x1p32, a);
+  }
+}
+
+// 8 plane bytes of this thread's quantised chunk into the planes of modulus i
 __device__ __forceinline__ void split8(const Oz2Const& c, int i, const uint32_t* tab,
-                                       const double* X, int sc, bool first, bool& t2,
+                                       const int (&h)[8], const uint32_t (&l)[8],
                                        uint8_t (*pl)[64][PP], int row, int ch) {
   const double m = (double)c.m[i], c32 = (double)c.c32[i], dinv = c.dinv[i];
   const int to = c.toff[i];
   uint32_t e[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const double xj = X[j];
-    const double a = rint(ldexp(xj, sc));
-    if (first) t2 |= (xj != 0.0) && (a == 0.0);
-    const double h = floor(a * 0x1p-32);
-    const double l = fma(-h, 0x1p32, a);
-    e[j] = tab[to + centred_residue(h, l, m, c32, dinv)];
-  }
+  for (int j = 0; j < 8; ++j)
+    e[j] = tab[to + centred_residue((double)h[j], (double)l[j], m, c32, dinv)];
   uint2 v0, v1;
   v0.x = gather_byte(e[0], e[1], e[2], e[3], 0x05010400u);
   v0.y = gather_byte(e[4], e[5], e[6], e[7], 0x05010400u);
@@ -215,16 +218,6 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
     }
     ma = oct_max(ma);
     mb = oct_max(mb);
-    {
-      const bool za = ma >= kInfBits, zb = mb >= kInfBits;   // T1: quantised as zero
-#pragma unroll
-      for (int j = 0; j < 8; j += 2) {
-        *reinterpret_cast<double2*>(&S.xa[row][ch + j]) =
-            make_double2(za ? 0.0 : xa[j], za ? 0.0 : xa[j + 1]);
-        *reinterpret_cast<double2*>(&S.xb[row][ch + j]) =
-            make_double2(zb ? 0.0 : xb[j], zb ? 0.0 : xb[j + 1]);
-      }
-    }
     if ((t & 7) == 0) {
       S.rbits[row] = ma;
       S.cbits[row] = mb;
@@ -285,16 +278,23 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
       S.sT[j] = s;
     }
     __syncthreads();
-    const int sa = S.sS[row], sb = S.sT[row];
-    const double* Xa = &S.xa[row][ch];
-    const double* Xb = &S.xb[row][ch];
+    // the thread's chunks, quantised once (T1 rows and columns as zeros)
+    int ha[8], hb[8];
+    uint32_t la[8], lb[8];
+    bool t2a = false, t2b = false;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      xa[j] = t1a ? 0.0 : xa[j];
+      xb[j] = t1b ? 0.0 : xb[j];
+    }
+    quantise8(xa, S.sS[row], t2a, ha, la);
+    quantise8(xb, S.sT[row], t2b, hb, lb);
     // residues of every modulus: one uint4 (8 int16 outputs) per modulus
     uint4 res[R];
-    bool t2a = false, t2b = false;
 #pragma nounroll
     for (int i = 0; i < R; ++i) {
-      split8(c, i, tab, Xa, sa, i == 0, t2a, S.pa, row, ch);
-      split8(c, i, tab, Xb, sb, i == 0, t2b, S.pb, row, ch);
+      split8(c, i, tab, ha, la, S.pa, row, ch);
+      split8(c, i, tab, hb, lb, S.pb, row, ch);
       __syncthreads();
       put_res<R>(res, i, modulus_products(c, i, S, rb0, cb0));
       __syncthreads();
