@@ -153,13 +153,19 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    # the timed steps carry no instrumentation; the per-stage split comes from
+    # as many further steps with HIP events between the stages (an event
+    # record between two launches costs the stream a few microseconds)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(events[i])
+        step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
 
     ms_step = (t1 - t0) * 1e3 / args.steps
     dec = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
@@ -288,20 +294,24 @@ def stationary_line(args, cfg, r, dev, A, B):
 
     for i in range(args.warmup):
         step(i)
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i, events[i])
+        step(args.warmup + i)
     torch.cuda.synchronize()
     ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    # per-stage split from as many further, instrumented steps
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        step(args.warmup + args.steps + i, events[i])
+    torch.cuda.synchronize()
     dec = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
     gem = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
     rec = float(np.mean([e[2].elapsed_time(e[3]) for e in events]))
     flop = 2.0 * m * n * k
     fp8_flop = 3 * r * flop
     achieved = fp8_flop / (gem * 1e-3) / 1e12
-    Blast = B if ((args.warmup + args.steps - 1) & 1) == 0 else B2
+    Blast = B if ((args.warmup + 2 * args.steps - 1) & 1) == 0 else B2
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(A, Blast, r, Cd, min(args.cpu_sample, 256), mode="fixed")
