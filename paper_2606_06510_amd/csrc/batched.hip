@@ -24,6 +24,10 @@ constexpr int PP = 80;   // bytes per plane row (64 + 16: spreads the LDS banks)
 constexpr int NTB = 512;
 
 struct Smem {
+  // the quantised A and B (row or column, k): a = h 2^32 + l, one int2 (h, l)
+  // per element, written once per problem and read for every modulus
+  int2 qa[64][64];
+  int2 qb[64][64];
   uint8_t pa[3][64][PP];
   uint8_t pb[3][64][PP];
   unsigned long long rbits[64], cbits[64];
@@ -58,29 +62,34 @@ __device__ __forceinline__ v4f mfma(v8i a, v8i b, v4f c) {
 
 // Quantise (Eq. (scale)) the thread's chunk (8 consecutive k of one row,
 // already zero for T1 rows) once per problem: a = rint(x 2^s) = h 2^32 + l
-// with |h| <= 2^30 (|a| <= 2^62) and 0 <= l < 2^32, kept as 32-bit integers.
-__device__ __forceinline__ void quantise8(const double (&x)[8], int sc, bool& t2, int (&h)[8],
-                                          uint32_t (&l)[8]) {
+// with |h| <= 2^30 (|a| <= 2^62) and 0 <= l < 2^32, stored as (h, l) in LDS.
+__device__ __forceinline__ void quantise8(const double (&x)[8], int sc, bool& t2, int2* q) {
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const double a = rint(ldexp(x[j], sc));
-    t2 |= (x[j] != 0.0) && (a == 0.0);
-    const double hd = floor(a * 0x1p-32);
-    h[j] = (int)hd;
-    l[j] = (uint32_t)fma(-hd, 0x1p32, a);
+  for (int j = 0; j < 8; j += 2) {
+    int2 v[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const double a = rint(ldexp(x[j + u], sc));
+      t2 |= (x[j + u] != 0.0) && (a == 0.0);
+      const double hd = floor(a * 0x1p-32);
+      v[u] = make_int2((int)hd, (int)(uint32_t)fma(-hd, 0x1p32, a));
+    }
+    *reinterpret_cast<int4*>(q + j) = make_int4(v[0].x, v[0].y, v[1].x, v[1].y);
   }
 }
 
 // 8 plane bytes of this thread's quantised chunk into the planes of modulus i
 __device__ __forceinline__ void split8(const Oz2Const& c, int i, const uint32_t* tab,
-                                       const int (&h)[8], const uint32_t (&l)[8],
-                                       uint8_t (*pl)[64][PP], int row, int ch) {
+                                       const int2* q, uint8_t (*pl)[64][PP], int row, int ch) {
   const double m = (double)c.m[i], c32 = (double)c.c32[i], dinv = c.dinv[i];
   const int to = c.toff[i];
   uint32_t e[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j)
-    e[j] = tab[to + centred_residue((double)h[j], (double)l[j], m, c32, dinv)];
+  for (int j = 0; j < 8; j += 2) {
+    const int4 hl = *reinterpret_cast<const int4*>(q + j);
+    e[j] = tab[to + centred_residue((double)hl.x, (double)(uint32_t)hl.y, m, c32, dinv)];
+    e[j + 1] = tab[to + centred_residue((double)hl.z, (double)(uint32_t)hl.w, m, c32, dinv)];
+  }
   uint2 v0, v1;
   v0.x = gather_byte(e[0], e[1], e[2], e[3], 0x05010400u);
   v0.y = gather_byte(e[4], e[5], e[6], e[7], 0x05010400u);
@@ -278,23 +287,22 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
       S.sT[j] = s;
     }
     __syncthreads();
-    // the thread's chunks, quantised once (T1 rows and columns as zeros)
-    int ha[8], hb[8];
-    uint32_t la[8], lb[8];
+    // the thread's chunks, quantised once (T1 rows and columns as zeros); the
+    // thread reads back only its own chunk, so no barrier is needed here
     bool t2a = false, t2b = false;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       xa[j] = t1a ? 0.0 : xa[j];
       xb[j] = t1b ? 0.0 : xb[j];
     }
-    quantise8(xa, S.sS[row], t2a, ha, la);
-    quantise8(xb, S.sT[row], t2b, hb, lb);
+    quantise8(xa, S.sS[row], t2a, &S.qa[row][ch]);
+    quantise8(xb, S.sT[row], t2b, &S.qb[row][ch]);
     // residues of every modulus: one uint4 (8 int16 outputs) per modulus
     uint4 res[R];
 #pragma nounroll
     for (int i = 0; i < R; ++i) {
-      split8(c, i, tab, ha, la, S.pa, row, ch);
-      split8(c, i, tab, hb, lb, S.pb, row, ch);
+      split8(c, i, tab, &S.qa[row][ch], S.pa, row, ch);
+      split8(c, i, tab, &S.qb[row][ch], S.pb, row, ch);
       __syncthreads();
       put_res<R>(res, i, modulus_products(c, i, S, rb0, cb0));
       __syncthreads();
