@@ -68,7 +68,10 @@ class Plan:
     def __del__(self):
         h = getattr(self, "handle", None)
         if h is not None and h.value:
-            _lib.ozaki2_plan_destroy(h)
+            try:
+                _lib.ozaki2_plan_destroy(h)
+            except Exception:   # interpreter shutdown: the library may be gone already
+                pass
             self.handle = None
 
     def deconstruct(self, A, B, stream=None):

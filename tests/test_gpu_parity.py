@@ -342,3 +342,43 @@ def test_operand_stationary_planes():
     adaptive.deconstruct(Ad, B1d)
     with pytest.raises(oz.Ozaki2Error):
         adaptive.deconstruct_b(B2d)
+
+
+def test_side_streams_and_concurrent_plans():
+    """Work is enqueued on the stream it is given: two plans of different
+    shapes run interleaved on two side streams, ozaki2_dgemm_ex on a third;
+    the first plan's A is overwritten on its own stream just before its
+    deconstruction, so a library that ignored the stream could read stale
+    data.  Every result is bit-exact against the oracle."""
+    import torch
+    import paper_2606_06510_amd as oz
+    dev = device()
+    A1, B1 = synth.lognormal(300, 260, 500, seed=41)
+    A1b = synth.lognormal(300, 260, 500, seed=43)[0]
+    A2, B2 = synth.uniform(257, 129, 700, seed=42)
+    res1 = oracle.dgemm(A1b, B1, 12)
+    res2 = oracle.dgemm(A2, B2, 12)
+    res3 = oracle.dgemm(A2, B2, 13)
+    Ad1, Bd1 = oz.to_device_colmajor(A1, dev), oz.to_device_colmajor(B1, dev)
+    Anew = oz.to_device_colmajor(A1b, dev)
+    Ad2, Bd2 = oz.to_device_colmajor(A2, dev), oz.to_device_colmajor(B2, dev)
+    C1 = oz.colmajor_empty(300, 260, device=dev)
+    C2 = oz.colmajor_empty(257, 129, device=dev)
+    C3 = oz.colmajor_empty(257, 129, device=dev)
+    p1 = oz.Plan(300, 260, 500, 12, 0, device=dev)
+    p2 = oz.Plan(257, 129, 700, 12, 0, device=dev)
+    torch.cuda.synchronize()
+    s1, s2, s3 = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    with torch.cuda.stream(s1):
+        Ad1.copy_(Anew)                     # ordered before the deconstruction on s1
+    p1.deconstruct(Ad1, Bd1, stream=s1)
+    p2.deconstruct(Ad2, Bd2, stream=s2)
+    oz.matmul(Ad2, Bd2, num_moduli=13, C=C3, stream=s3)
+    p1.residue_gemm(stream=s1)
+    p2.residue_gemm(stream=s2)
+    p1.reconstruct(C1, stream=s1)
+    p2.reconstruct(C2, stream=s2)
+    torch.cuda.synchronize()
+    compare_C(oz.from_device_colmajor(C1), A1b, B1, res1)
+    compare_C(oz.from_device_colmajor(C2), A2, B2, res2)
+    compare_C(oz.from_device_colmajor(C3), A2, B2, res3)
