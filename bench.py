@@ -32,8 +32,9 @@ HBM_PEAK_GBS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=30)
+    # the clock takes about ten 4096^3 steps (some 20 ms of work) to settle
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="gemm4096_lognormal")
     ap.add_argument("--moduli", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
