@@ -241,6 +241,22 @@ Oz2Layout make_layout(const Oz2Dims& d, const Oz2Const& c) {
 const unsigned kKnownFlags = OZ2_ACCUMULATE | OZ2_SCALE_FIXED | OZ2_QUANT_TZ | OZ2_NO_FALLBACK |
                              OZ2_FORCE_FALLBACK;
 
+}  // namespace
+
+int oz2_device_cus() {
+  static const int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      return 256;
+    return n;
+  }();
+  return cus;
+}
+
+namespace {
+
 // gfx950 check, cached per device
 int device_ok() {
   static std::mutex mu;

@@ -319,9 +319,7 @@ hipError_t launch_r(const Oz2Const& c, int m, int n, int k, int batch, const dou
                     long long sA, const double* B, int ldb, long long sB, double* C, int ldc,
                     long long sC, const uint32_t* tab, hipStream_t s) {
   const size_t lds = (size_t)c.tabsz * 4;
-  int dev = 0, cus = 256;
-  if (hipGetDevice(&dev) == hipSuccess)
-    (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  const int cus = oz2_device_cus();
   (void)hipFuncSetAttribute((const void*)k_batched<R>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)lds);
   int per = 0;

@@ -9,6 +9,8 @@
 // with lanes along the rows so every load instruction is a contiguous 512 B;
 // B's columns are contiguous along k.  Outputs (codes, planes) are K-blocked
 // byte planes [k/64][rows][64] (the GEMM's stage order), 16 bytes per lane.
+#include <mutex>
+
 #include "oz2_device.h"
 
 namespace {
@@ -671,17 +673,11 @@ hipError_t oz2_launch_tables(const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
 }
 
 // workgroups of k_split that stay resident on the whole device for a given
-// LDS table size (cached per size: the table size depends only on r)
+// LDS table size (cached per size under a lock: the size depends only on r)
 static int split_resident(size_t lds) {
+  static std::mutex mu;
   static int cache_lds[OZ2_MAXR + 1] = {0}, cache_n[OZ2_MAXR + 1] = {0};
-  static int cus = 0;
-  if (!cus) {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        cus <= 0)
-      cus = 256;
-  }
+  std::lock_guard<std::mutex> g(mu);
   const int slot = (int)(lds % (OZ2_MAXR + 1));
   if (cache_lds[slot] == (int)lds) return cache_n[slot];
   // dynamic LDS above 64 KiB (tables for r = 16 plus the staged tile) must be opted into
@@ -693,8 +689,8 @@ static int split_resident(size_t lds) {
       per_cu <= 0)
     per_cu = 1;
   cache_lds[slot] = (int)lds;
-  cache_n[slot] = per_cu * cus;
-  return per_cu * cus;
+  cache_n[slot] = per_cu * oz2_device_cus();
+  return cache_n[slot];
 }
 
 hipError_t oz2_launch_split(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,

@@ -506,14 +506,7 @@ hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Con
                               uint8_t* ws, hipStream_t s) {
   // moduli per workgroup: all r when the tiles alone fill the device (one
   // resident workgroup per CU), else split so tiles x groups still covers it
-  static int cus = 0;
-  if (!cus) {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        cus <= 0)
-      cus = 256;
-  }
+  const int cus = oz2_device_cus();
   const int tiles = (d.mp / TILE) * (d.np / TILE);
   const int groups = std::min(c.r, (cus + tiles - 1) / tiles);
   const int mpw = (c.r + groups - 1) / groups;

@@ -77,6 +77,10 @@ struct Oz2Layout {
   size_t total;
 };
 
+// compute units of the current device (queried once per process, thread-safe;
+// 256 if the query fails)
+int oz2_device_cus();
+
 // ---------------------------------------------------------------- launchers
 // Each returns hipGetLastError() of its launches.  `side` of the per-operand
 // deconstruct launchers: OZ2_SIDE_A, OZ2_SIDE_B or both.
