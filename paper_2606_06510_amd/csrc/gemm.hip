@@ -504,12 +504,19 @@ hipError_t oz2_launch_codegemm(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws
 
 hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
                               uint8_t* ws, hipStream_t s) {
-  // moduli per workgroup: all r when the tiles alone fill the device (one
-  // resident workgroup per CU), else split so tiles x groups still covers it
+  // moduli per workgroup.  Enough groups that tiles x groups covers the
+  // device (one resident workgroup per CU), and no more than about WG_STEPS
+  // K-steps of plane products (three per modulus) in one workgroup: the CUs
+  // run at slightly different clocks, and the dispatcher evens that out only
+  // when a workgroup is a small share of a CU's work.  A short k keeps all
+  // moduli together, since each workgroup pays a prologue and an epilogue.
+  constexpr int WG_STEPS = 768;
   const int cus = oz2_device_cus();
   const int tiles = (d.mp / TILE) * (d.np / TILE);
-  const int groups = std::min(c.r, (cus + tiles - 1) / tiles);
-  const int mpw = (c.r + groups - 1) / groups;
+  const int fill = std::min(c.r, (cus + tiles - 1) / tiles);
+  const int ksteps = (std::min(d.kp, OZ2_KSLAB) + KS - 1) / KS;
+  const int by_work = std::max(1, WG_STEPS / (3 * ksteps));
+  const int mpw = std::min((c.r + fill - 1) / fill, by_work);
   dim3 grid(tiles, (c.r + mpw - 1) / mpw);
   for (int kb = 0, sl = 0; kb < d.kp; kb += OZ2_KSLAB, ++sl) {
     const int ke = kb + OZ2_KSLAB < d.kp ? kb + OZ2_KSLAB : d.kp;
