@@ -232,11 +232,14 @@ def test_batched_single_launch_fallback_and_zeros():
 
 @pytest.mark.parametrize("shape,r", [((1536, 1536, 200), 12), ((2000, 2100, 130), 12),
                                      ((2560, 2560, 96), 12), ((4096, 2048, 64), 12),
-                                     ((2048, 2048, 100), 16), ((4096, 2048, 70), 13)])
+                                     ((2048, 2048, 100), 16), ((4096, 2048, 70), 13),
+                                     ((4096, 4096, 2048), 12), ((4096, 4096, 1536), 13)])
 def test_moduli_per_workgroup_grids(shape, r):
     """Tile counts between 1 and 2 per CU make each residue-GEMM workgroup walk
-    2, 3, 4, 6 or 7 moduli (the last group shorter for r = 13); sampled
-    outputs, including the ragged last row and column blocks, are bit-exact."""
+    2, 3, 4, 6 or 7 moduli (the last group shorter for r = 13); at k = 2048
+    and 1536 the work per workgroup sets the split instead (8 + 4 and 10 + 3
+    moduli).  Sampled outputs, including the ragged last row and column
+    blocks, are bit-exact."""
     import paper_2606_06510_amd as oz
     import torch
     m, n, k = shape
@@ -280,6 +283,31 @@ def test_subnormal_and_overflowing_results():
     assert np.isinf(res.C).sum() == 32 * 24
     plan, C = run_staged(A, B, 12)
     compare_all(plan, C, A, B, 12, res)
+
+
+@pytest.mark.parametrize("r", [12, 15])
+def test_batched_subnormal_and_overflowing_results(r):
+    """The single-launch path rounds into the subnormal range and overflows
+    to infinity bit-exactly: problem 0 has rows and columns scaled so that
+    one block of C is subnormal and another overflows; problem 1 stays in
+    range (r = 12 takes the three-limb CRT, r = 15 the 32-bit words)."""
+    Ab, Bb = synth.batched(2, 64, 64, 64, seed=90 + r)
+    Ab = Ab.copy()
+    Bb = Bb.copy()
+    Ab[0] /= np.abs(Ab[0]).max()          # undo the per-matrix scale of the workload
+    Bb[0] /= np.abs(Bb[0]).max()
+    Ab[0, :16] *= 2.0 ** -560
+    Ab[0, 48:] *= 2.0 ** 520
+    Bb[0, :, :12] *= 2.0 ** -500
+    Bb[0, :, 40:] *= 2.0 ** 520
+    C = _batched_run(Ab, Bb, r)
+    r0 = oracle.dgemm(Ab[0], Bb[0], r)
+    assert ((r0.C != 0) & (np.abs(r0.C) < 2.0 ** -1022)).sum() == 16 * 12
+    assert np.isinf(r0.C).sum() == 16 * 24
+    for b in range(2):
+        rb = r0 if b == 0 else oracle.dgemm(Ab[b], Bb[b], r)
+        assert not len(rb.fallback_rows) and not len(rb.fallback_cols)
+        assert np.array_equal(bits(C[b]), bits(rb.C)), b
 
 
 def test_repeated_reconstruct_keeps_fallback_lists():
