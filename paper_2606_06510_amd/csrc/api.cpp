@@ -353,7 +353,10 @@ int run_reconstruct(ozaki2_plan_s& p, double* C, int ldc, hipStream_t s) {
   return hip_status(e);
 }
 
-// internal grow-only workspace of ozaki2_dgemm, per device
+// internal grow-only workspace of ozaki2_dgemm, per device.  Callers hold
+// g_pool_mu from pool_get until their work is enqueued: a grow synchronises
+// the device before it frees the old buffer, so work enqueued under the lock
+// has finished with it by then, whichever thread grows the pool next.
 struct Pool {
   void* ptr = nullptr;
   size_t bytes = 0;
@@ -361,10 +364,9 @@ struct Pool {
 std::mutex g_pool_mu;
 Pool g_pool[64];
 
-int pool_get(size_t need, void** out) {
+int pool_get(size_t need, void** out) {   // g_pool_mu held by the caller
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return OZ2_E_DEVICE;
-  std::lock_guard<std::mutex> g(g_pool_mu);
   Pool& P = g_pool[dev];
   if (P.bytes < need) {
     if (P.ptr) {
@@ -547,6 +549,7 @@ int ozaki2_dgemm(int m, int n, int k, const double* A, int lda, const double* B,
   if (need == 0) return OZ2_E_INVALID;
   st = device_ok();
   if (st != OZ2_OK) return st;
+  std::lock_guard<std::mutex> g(g_pool_mu);
   void* ws = nullptr;
   st = pool_get(need, &ws);
   if (st != OZ2_OK) return st;
@@ -568,6 +571,7 @@ int ozaki2_dgemm_strided_batched(int m, int n, int k, const double* A, int lda, 
     if (!make_const(num_moduli, c)) return OZ2_E_INVALID;
     st = device_ok();
     if (st != OZ2_OK) return st;
+    std::lock_guard<std::mutex> g(g_pool_mu);
     void* ws = nullptr;
     st = pool_get(align256((size_t)c.tabsz * 4), &ws);
     if (st != OZ2_OK) return st;
@@ -584,6 +588,7 @@ int ozaki2_dgemm_strided_batched(int m, int n, int k, const double* A, int lda, 
   if (need == 0) return OZ2_E_INVALID;
   st = device_ok();
   if (st != OZ2_OK) return st;
+  std::lock_guard<std::mutex> g(g_pool_mu);
   void* ws = nullptr;
   st = pool_get(need, &ws);
   if (st != OZ2_OK) return st;

@@ -173,6 +173,54 @@ def test_plain_entry_point_and_batched():
         assert np.array_equal(bits(Cb[b]), bits(rb.C))
 
 
+def test_plain_entry_point_from_two_threads():
+    """Two host threads issue plain ozaki2_dgemm calls on one stream while the
+    library's internal workspace grows under them (each thread's calls get
+    larger).  A thread holds the workspace from lookup to enqueue, and a grow
+    synchronises before it frees, so no call's kernels run on a buffer that
+    another thread's grow released; every product is bit-exact."""
+    import threading
+    import paper_2606_06510_amd as oz
+    import torch
+    dev = device()
+    torch.cuda.synchronize()
+    oz.ozaki2_finalize()                      # start from an empty workspace
+    stream = torch.cuda.current_stream().cuda_stream
+    shapes = [[(96, 80, 64), (200, 150, 260), (330, 270, 520), (420, 390, 700)],
+              [(64, 72, 90), (180, 210, 300), (300, 330, 610), (450, 400, 640)]]
+    jobs = []
+    for t, lst in enumerate(shapes):
+        row = []
+        for i, (m, n, k) in enumerate(lst):
+            A, B = synth.lognormal(m, n, k, seed=500 + 10 * t + i)
+            row.append((A, B, oz.to_device_colmajor(A, dev), oz.to_device_colmajor(B, dev),
+                        oz.colmajor_empty(m, n, device=dev)))
+        jobs.append(row)
+    torch.cuda.synchronize()
+    errors = []
+
+    def work(row):
+        try:
+            for A, B, Ad, Bd, Cd in row:
+                m, k = A.shape
+                n = B.shape[1]
+                oz.ozaki2_dgemm(m, n, k, Ad, m, Bd, k, Cd, m, 12, stream)
+        except Exception as e:               # reported after the join
+            errors.append(e)
+
+    threads = [threading.Thread(target=work, args=(row,)) for row in jobs]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for row in jobs:
+        for A, B, Ad, Bd, Cd in row:
+            res = oracle.dgemm(A, B, 12)
+            assert np.array_equal(bits(oz.from_device_colmajor(Cd)), bits(res.C)), A.shape
+
+
 def _batched_run(Ab, Bb, r):
     import paper_2606_06510_amd as oz
     import torch
