@@ -106,10 +106,10 @@ __device__ __forceinline__ void split8(const Oz2Const& c, int i, const uint32_t*
 }
 
 // The three plane products of modulus i for the wave's two blocks (the
-// chains of the residue GEMM), then the centred residues of the 8 outputs,
-// two per word: word q holds outputs 2q, 2q+1 (output = 4 block + e).
-__device__ __forceinline__ uint4 modulus_products(const Oz2Const& c, int i, const Smem& S, int rb0,
-                                                  int cb0) {
+// chains of the residue GEMM): acc[q][e] is output 4q + e, an exact integer
+// below 2^16 in magnitude, congruent to C~ / fin mod m.
+__device__ __forceinline__ void modulus_chain(const Oz2Const& c, int i, const Smem& S, int rb0,
+                                              int cb0, v4f (&acc)[2]) {
   const int m = c.m[i], s = c.sq[i];
   const float fm = (float)m, inv = c.finv[i];
   auto reduce_mul = [&](v4f v, float rho) {
@@ -117,7 +117,8 @@ __device__ __forceinline__ uint4 modulus_products(const Oz2Const& c, int i, cons
     for (int e = 0; e < 4; ++e) v[e] = __builtin_fmaf(-rintf(v[e] * inv), fm, v[e]) * rho;
     return v;
   };
-  v4f acc[2] = {v4f{0.f}, v4f{0.f}};
+  acc[0] = v4f{0.f};
+  acc[1] = v4f{0.f};
   if (s) {          // (d1 e0 + d0 e1) x s + d0 e0
     const v8i a1 = frag(S.pa[1], rb0), a0 = frag(S.pa[0], rb0);
 #pragma unroll
@@ -138,6 +139,16 @@ __device__ __forceinline__ uint4 modulus_products(const Oz2Const& c, int i, cons
       acc[q] = mfma(a2, frag(S.pb[2], cb0 + 16 * q), acc[q]);
     }
   }
+}
+
+// The centred residues of the 8 outputs of modulus i, two per word: word q
+// holds outputs 2q, 2q+1 (output = 4 block + e).
+__device__ __forceinline__ uint4 modulus_products(const Oz2Const& c, int i, const Smem& S, int rb0,
+                                                  int cb0) {
+  const int m = c.m[i];
+  const float fm = (float)m, inv = c.finv[i];
+  v4f acc[2];
+  modulus_chain(c, i, S, rb0, cb0, acc);
   const int fin = c.fin[i];
   int rr[8];
 #pragma unroll
@@ -152,6 +163,59 @@ __device__ __forceinline__ uint4 modulus_products(const Oz2Const& c, int i, cons
 #pragma unroll
   for (int q = 0; q < 4; ++q) w[q] = ((uint32_t)rr[2 * q] & 0xFFFFu) | ((uint32_t)rr[2 * q + 1] << 16);
   return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// r <= 12: output 4q + e's residue of modulus i, reduced once, added into its
+// CRT sums.  The chain value v (|v| < 2^16, exact) times fin, reduced with
+// the fp32 quotient estimate, lies within m/2 + 1 of zero: any representative
+// of magnitude <= 577 serves the sums, whose limbs stay below 2^52.
+__device__ __forceinline__ void crt_add(const Oz2Const& c, int i, const v4f (&acc)[2],
+                                        double (&S0)[8], double (&S1)[8], double (&S2)[8]) {
+  const float fm = (float)c.m[i], inv = c.finv[i], fin = (float)c.fin[i];
+  const bool scaled = c.fin[i] != 1;
+  const double w0 = c.W38[i][0], w1 = c.W38[i][1], w2 = c.W38[i][2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float v = acc[q][e];
+      if (scaled) v = __builtin_fmaf(-rintf(v * inv), fm, v) * fin;
+      const double x = (double)__builtin_fmaf(-rintf(v * inv), fm, v);
+      const int I = 4 * q + e;
+      S0[I] = fma(x, w0, S0[I]);
+      S1[I] = fma(x, w1, S1[I]);
+      S2[I] = fma(x, w2, S2[I]);
+    }
+}
+
+// r <= 12: the lane's eight outputs (output I at row rb0 + 4 (lane/16) + I%4,
+// column cb0 + 16 (I/4) + lane%16) from their CRT sums: reduction by the
+// quotient estimate, one rounding with the exponent shift; flagged rows and
+// columns recomputed in native FP64; only outputs inside m x n stored.
+__device__ __forceinline__ void emit38(const Oz2Const& c, const double (&S0)[8],
+                                       const double (&S1)[8], const double (&S2)[8],
+                                       const Smem& S, int rb0, int cb0, int m, int n, int k,
+                                       const double* __restrict__ A, int lda,
+                                       const double* __restrict__ B, int ldb, double* C, int ldc) {
+  const int lane = threadIdx.x & 63;
+  const int r0 = rb0 + 4 * (lane >> 4), c0 = cb0 + (lane & 15);
+#pragma unroll
+  for (int I = 0; I < 8; ++I) {
+    const int row = r0 + (I & 3), col = c0 + 16 * (I >> 2);
+    if (row < m && col < n) {
+      double v;
+      if ((S.fA[row] | S.fB[col]) & (OZ2_T1 | OZ2_T2)) {
+        double sacc = 0.0;   // native FP64, one FMA per k in ascending k
+        for (int l = 0; l < k; ++l) sacc = fma(A[row + (size_t)l * lda], B[l + (size_t)col * ldb], sacc);
+        v = sacc;
+      } else {
+        double s0 = S0[I], s1 = S1[I], s2 = S2[I];
+        if (crt38_reduce(c, s0, s1, s2)) crt38_fix(c, s0, s1, s2);
+        v = round38(s0, s1, s2, S.sS[row] + S.sT[col]);
+      }
+      C[row + (size_t)col * ldc] = v;
+    }
+  }
 }
 
 // res[i] = v for a runtime i without dynamic register indexing
@@ -179,8 +243,6 @@ struct Emit {
         double sacc = 0.0;   // native FP64, one FMA per k in ascending k
         for (int l = 0; l < k; ++l) sacc = fma(A[row + (size_t)l * lda], B[l + (size_t)col * ldb], sacc);
         v = sacc;
-      } else if constexpr (R <= 12) {
-        v = crt38_rounded<R, I>(c, x, S.sS[row] + S.sT[col]);
       } else {
         uint32_t w[NW];
         crt_words<R, NW, I>(c, x, w);
@@ -297,20 +359,42 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
     }
     quantise8(xa, S.sS[row], t2a, &S.qa[row][ch]);
     quantise8(xb, S.sT[row], t2b, &S.qb[row][ch]);
-    // residues of every modulus: one uint4 (8 int16 outputs) per modulus
-    uint4 res[R];
+    if constexpr (R <= 12) {
+      // each modulus's residues go straight into the CRT sums (three
+      // radix-2^38 limbs per output)
+      double S0[8], S1[8], S2[8];
+#pragma unroll
+      for (int I = 0; I < 8; ++I) S0[I] = S1[I] = S2[I] = 0.0;
 #pragma nounroll
-    for (int i = 0; i < R; ++i) {
-      split8(c, i, tab, &S.qa[row][ch], S.pa, row, ch);
-      split8(c, i, tab, &S.qb[row][ch], S.pb, row, ch);
+      for (int i = 0; i < R; ++i) {
+        split8(c, i, tab, &S.qa[row][ch], S.pa, row, ch);
+        split8(c, i, tab, &S.qb[row][ch], S.pb, row, ch);
+        __syncthreads();
+        v4f acc[2];
+        modulus_chain(c, i, S, rb0, cb0, acc);
+        crt_add(c, i, acc, S0, S1, S2);
+        __syncthreads();
+      }
+      if (t2a && row < m) atomicOr(&S.fA[row], OZ2_T2);
+      if (t2b && row < n) atomicOr(&S.fB[row], OZ2_T2);
       __syncthreads();
-      put_res<R>(res, i, modulus_products(c, i, S, rb0, cb0));
+      emit38(c, S0, S1, S2, S, rb0, cb0, m, n, k, Ab, lda, Bb, ldb, Cb, ldc);
+    } else {
+      // residues of every modulus: one uint4 (8 int16 outputs) per modulus
+      uint4 res[R];
+#pragma nounroll
+      for (int i = 0; i < R; ++i) {
+        split8(c, i, tab, &S.qa[row][ch], S.pa, row, ch);
+        split8(c, i, tab, &S.qb[row][ch], S.pb, row, ch);
+        __syncthreads();
+        put_res<R>(res, i, modulus_products(c, i, S, rb0, cb0));
+        __syncthreads();
+      }
+      if (t2a && row < m) atomicOr(&S.fA[row], OZ2_T2);
+      if (t2b && row < n) atomicOr(&S.fB[row], OZ2_T2);
       __syncthreads();
+      Emit<R, 0>::run(c, res, S, rb0, cb0, m, n, k, Ab, lda, Bb, ldb, Cb, ldc);
     }
-    if (t2a && row < m) atomicOr(&S.fA[row], OZ2_T2);
-    if (t2b && row < n) atomicOr(&S.fB[row], OZ2_T2);
-    __syncthreads();
-    Emit<R, 0>::run(c, res, S, rb0, cb0, m, n, k, Ab, lda, Bb, ldb, Cb, ldc);
   }
 }
 

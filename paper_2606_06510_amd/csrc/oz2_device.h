@@ -272,10 +272,41 @@ __device__ __forceinline__ double round38(double S0, double S1, double S2, int e
   return ldexp(v, sh - e);
 }
 
+// X - qM with q = rint(X/M) from the top limbs (within 2^-36 of X/M),
+// normalised.  Returns whether the estimate lay within that of +-1/2, where
+// q may be off by one and crt38_fix settles the range exactly.
+__device__ __forceinline__ bool crt38_reduce(const Oz2Const& c, double& S0, double& S1,
+                                             double& S2) {
+  const double f = fma(S1, 0x1p-38, S2) * c.mtop38;
+  const double q = rint(f);
+  S0 = fma(-q, c.M38[0], S0);
+  S1 = fma(-q, c.M38[1], S1);
+  S2 = fma(-q, c.M38[2], S2);
+  normalise38(S0, S1, S2);
+  return fabs(f - q) > 0.49999;
+}
+
+// X in [-floor(M/2), ceil(M/2) - 1]: P = X - M + floor(M/2) >= 0 means
+// X >= ceil(M/2) (subtract M); N = X + floor(M/2) < 0 means X <
+// -floor(M/2) (add M); the sign of a normalised limb vector is that of its
+// top limb
+__device__ __forceinline__ void crt38_fix(const Oz2Const& c, double& S0, double& S1, double& S2) {
+  double P0 = S0 - c.M38[0] + c.Mhalf38[0], P1 = S1 - c.M38[1] + c.Mhalf38[1],
+         P2 = S2 - c.M38[2] + c.Mhalf38[2];
+  double N0 = S0 + c.Mhalf38[0], N1 = S1 + c.Mhalf38[1], N2 = S2 + c.Mhalf38[2];
+  normalise38(P0, P1, P2);
+  normalise38(N0, N1, N2);
+  const double adj = (P2 >= 0.0) ? -1.0 : ((N2 < 0.0) ? 1.0 : 0.0);
+  S0 = fma(adj, c.M38[0], S0);
+  S1 = fma(adj, c.M38[1], S1);
+  S2 = fma(adj, c.M38[2], S2);
+  normalise38(S0, S1, S2);
+}
+
 // C~ of output I of a thread (R <= 12 residues, |x_i| <= 577) rounded with the
-// exponent shift -e: the direct CRT sum in radix-2^38 limbs, the quotient
-// q = rint(X/M) from the top limbs (within 2^-36 of X/M), the exact range
-// check for the ambiguous case, then round38.
+// exponent shift -e: the direct CRT sum in radix-2^38 limbs, the reduction by
+// the quotient estimate (with the exact range check where it is ambiguous),
+// then round38.
 template <int R, int I>
 __device__ __forceinline__ double crt38_rounded(const Oz2Const& c, const uint4 (&x)[R], int e) {
   static_assert(R <= 12, "three radix-2^38 limbs hold [-M/2, M/2) only for r <= 12");
@@ -287,28 +318,7 @@ __device__ __forceinline__ double crt38_rounded(const Oz2Const& c, const uint4 (
     S1 = fma(xi, c.W38[i][1], S1);
     S2 = fma(xi, c.W38[i][2], S2);
   }
-  const double f = fma(S1, 0x1p-38, S2) * c.mtop38;
-  const double q = rint(f);
-  S0 = fma(-q, c.M38[0], S0);
-  S1 = fma(-q, c.M38[1], S1);
-  S2 = fma(-q, c.M38[2], S2);
-  normalise38(S0, S1, S2);
-  if (fabs(f - q) > 0.49999) {
-    // X in [-floor(M/2), ceil(M/2) - 1]: P = X - M + floor(M/2) >= 0 means
-    // X >= ceil(M/2) (subtract M); N = X + floor(M/2) < 0 means X <
-    // -floor(M/2) (add M); the sign of a normalised limb vector is that of
-    // its top limb
-    double P0 = S0 - c.M38[0] + c.Mhalf38[0], P1 = S1 - c.M38[1] + c.Mhalf38[1],
-           P2 = S2 - c.M38[2] + c.Mhalf38[2];
-    double N0 = S0 + c.Mhalf38[0], N1 = S1 + c.Mhalf38[1], N2 = S2 + c.Mhalf38[2];
-    normalise38(P0, P1, P2);
-    normalise38(N0, N1, N2);
-    const double adj = (P2 >= 0.0) ? -1.0 : ((N2 < 0.0) ? 1.0 : 0.0);
-    S0 = fma(adj, c.M38[0], S0);
-    S1 = fma(adj, c.M38[1], S1);
-    S2 = fma(adj, c.M38[2], S2);
-    normalise38(S0, S1, S2);
-  }
+  if (crt38_reduce(c, S0, S1, S2)) crt38_fix(c, S0, S1, S2);
   return round38(S0, S1, S2, e);
 }
 
