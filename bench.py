@@ -38,8 +38,8 @@ def parse():
     ap.add_argument("--config", default="gemm4096_lognormal")
     ap.add_argument("--moduli", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=int, default=1792,
-                    help="sampled rows and columns of the CPU-oracle baseline (about 10 s of "
+    ap.add_argument("--cpu-sample", type=int, default=2304,
+                    help="sampled rows and columns of the CPU-oracle baseline (about 12 s of "
                          "oracle work on the GPU hosts at 4096^3)")
     ap.add_argument("--no-probes", action="store_true", help="skip the measured-peak probes")
     ap.add_argument("--copy-calibration", action="store_true",
