@@ -4,6 +4,8 @@
     python -m paper_2606_06510_amd.rocprof_summary traffic FETCH_CSV WRITE_CSV OUT_TXT \\
         KERNEL COPY_BYTES SOURCE CMD_FETCH CMD_WRITE
     python -m paper_2606_06510_amd.rocprof_summary mfma COUNTER_CSV OUT_TXT SOURCE CMD
+    python -m paper_2606_06510_amd.rocprof_summary hbm STATS_CSV FETCH_CSV WRITE_CSV OUT_MD \
+        COPY_BYTES M N K R PSTORE CMD_TRACE CMD_FETCH CMD_WRITE
 
 ``stats`` turns a ``--kernel-trace --stats`` kernel_stats.csv into a markdown
 table.  ``traffic`` reads two ``--pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE``
@@ -16,6 +18,11 @@ GRBM_GUI_ACTIVE`` counter_collection.csv and reports, per FP8-MFMA kernel,
 the FP8 operations per launch (MOPS x 512), the share of SIMD cycles the MFMA
 unit was busy and the shader clock the launch ran at (GRBM_GUI_ACTIVE is
 summed over the XCDs: cycles = sum / XCDs, clock = cycles / duration).
+``hbm`` puts the memory-bound kernels of an m x n x k product at r moduli
+(PSTORE plane bytes per input element) side by side: mean duration from the
+kernel trace, algorithmic bytes, the copy-scaled FETCH_SIZE + WRITE_SIZE
+bytes, and the achieved rate (algorithmic bytes / mean duration) against
+the 8 TB/s HBM peak.
 """
 from __future__ import annotations
 
@@ -114,6 +121,52 @@ def mfma(src, dst, source, cmd, xcds=8, simds=1024):
                     f"{100 * sum(x[2] for x in xs) / n:.1f}% | {sum(x[3] for x in xs) / n / 1e9:.2f} |\n")
 
 
+def _algorithmic(m, n, k, r, pstore):
+    """Algorithmic bytes per launch of the memory-bound kernels: each operand
+    read once per pass, each code, plane, residue and output written once."""
+    ea, eb = m * k, k * n
+    return {
+        "k_scan_codes_rows": 9 * ea,              # A read (8 B), code byte written (1 B)
+        "k_scan_codes_cols": 9 * eb,
+        "k_rebase": 2 * (ea + eb),                # code bytes read and rewritten in place
+        "k_split": (8 + pstore) * (ea + eb),      # operand read, plane bytes written
+        f"void k_reconstruct<{r}>": (2 * r + 8) * m * n,   # int16 residues read, FP64 written
+    }
+
+
+def hbm(stats_csv, fetch_csv, write_csv, dst, copy_bytes, m, n, k, r, pstore, cmd_t, cmd_f, cmd_w,
+        peak=8.0e12):
+    avg = {_short(x["Name"]): float(x["AverageNs"]) * 1e-9 for x in csv.DictReader(open(stats_csv))}
+    fetch = _per_launch(fetch_csv, "FETCH_SIZE")
+    write = _per_launch(write_csv, "WRITE_SIZE")
+    copy = next(x for x in fetch if x.startswith("k_copy"))
+    sf = copy_bytes / (fetch[copy] * 1024.0)
+    sw = copy_bytes / (write[copy] * 1024.0)
+    alg = _algorithmic(m, n, k, r, pstore)
+    with open(dst, "w") as f:
+        f.write(f"# Memory-bound kernels of the emulated DGEMM {m}x{n}x{k}, r = {r}: achieved HBM "
+                f"rate against the {peak / 1e12:.0f} TB/s peak\n\n")
+        f.write("Commands (from the repository root, on one MI355X): the kernel trace for the mean "
+                "durations, then one counter pass each for FETCH_SIZE and WRITE_SIZE (each scaled "
+                f"by its reading for a plain copy of {copy_bytes} bytes: x{sf:.4f} and x{sw:.4f}).\n\n")
+        f.write(f"```\n{cmd_t}\n{cmd_f}\n{cmd_w}\n```\n\n")
+        f.write("| kernel | avg (us) | algorithmic bytes | measured bytes (fetch + write) | "
+                "measured / algorithmic | achieved (algorithmic / avg) | of peak |\n")
+        f.write("|---|---|---|---|---|---|---|\n")
+        tot_t = tot_a = 0.0
+        for name, ab in alg.items():
+            if name not in avg or name not in fetch:
+                continue
+            t = avg[name]
+            mb = fetch[name] * 1024.0 * sf + write.get(name, 0.0) * 1024.0 * sw
+            tot_t += t
+            tot_a += ab
+            f.write(f"| {name} | {t * 1e6:.1f} | {ab / 1e6:.1f} MB | {mb / 1e6:.1f} MB | "
+                    f"{mb / ab:.3f} | {ab / t / 1e12:.2f} TB/s | {100 * ab / t / peak:.0f}% |\n")
+        f.write(f"| all of the above | {tot_t * 1e6:.1f} | {tot_a / 1e6:.1f} MB | | | "
+                f"{tot_a / tot_t / 1e12:.2f} TB/s | {100 * tot_a / tot_t / peak:.0f}% |\n")
+
+
 def main(argv):
     if argv[0] == "stats":
         stats(*argv[1:5])
@@ -121,6 +174,9 @@ def main(argv):
         traffic(argv[1], argv[2], argv[3], argv[4], int(argv[5]), argv[6], argv[7], argv[8])
     elif argv[0] == "mfma":
         mfma(*argv[1:5])
+    elif argv[0] == "hbm":
+        hbm(argv[1], argv[2], argv[3], argv[4], int(argv[5]), *map(int, argv[6:11]),
+            argv[11], argv[12], argv[13])
     else:
         raise SystemExit(__doc__)
 
