@@ -221,6 +221,96 @@ def test_plain_entry_point_from_two_threads():
             assert np.array_equal(bits(oz.from_device_colmajor(Cd)), bits(res.C)), A.shape
 
 
+def _padded(X, ld, off, dev, fill=float("nan")):
+    """Column-major device view of X (m x n) with leading dimension ld, its
+    first element `off` doubles into a buffer whose other entries hold fill."""
+    import torch
+    m, n = X.shape
+    buf = torch.full((off + ld * n,), fill, dtype=torch.float64, device=dev)
+    view = buf[off:].view(n, ld)[:, :m].t()
+    view.copy_(torch.from_numpy(np.ascontiguousarray(X)).to(dev))
+    return buf, view
+
+
+@pytest.mark.parametrize("pad,off", [((2, 6, 4), 0), ((1, 3, 5), 1), ((64, 0, 0), 2)])
+def test_padded_leading_dimensions(pad, off):
+    """Leading dimensions above the row counts (even, odd) and base addresses
+    that are not 16-byte aligned, through the staged plan, the workspace entry
+    point with accumulation and the plain one: products bit-exact, padding of
+    A and B (NaN, which would flag any row that read it) never used, padding
+    of C untouched."""
+    import paper_2606_06510_amd as oz
+    import torch
+    dev = device()
+    m, n, k = 300, 260, 200
+    A, B = synth.lognormal(m, n, k, seed=60 + off)
+    C0 = synth.lognormal(m, n, 1, seed=70 + off)[0][:, :1] * np.ones((1, n))
+    lda, ldb, ldc = m + pad[0], k + pad[1], m + pad[2]
+    _, Ad = _padded(A, lda, off, dev)
+    _, Bd = _padded(B, ldb, off, dev)
+    res = oracle.dgemm(A, B, 12)
+    assert len(res.fallback_rows) == 0 and len(res.fallback_cols) == 0
+    sentinel = -7.25
+
+    def check(cbuf, cview, expect):
+        assert np.array_equal(bits(oz.from_device_colmajor(cview)), bits(expect))
+        whole = cbuf[off:].view(n, ldc)
+        assert bool((whole[:, m:] == sentinel).all()) and bool((cbuf[:off] == sentinel).all())
+
+    # staged plan
+    cbuf, Cd = _padded(np.zeros((m, n)), ldc, off, dev, fill=sentinel)
+    plan = oz.Plan(m, n, k, 12, 0, device=dev)
+    plan.deconstruct(Ad, Bd)
+    plan.residue_gemm()
+    plan.reconstruct(Cd)
+    torch.cuda.synchronize()
+    check(cbuf, Cd, res.C)
+    # workspace entry point, C <- C0 + A B
+    cbuf, Cd = _padded(C0, ldc, off, dev, fill=sentinel)
+    oz.matmul(Ad, Bd, 12, oz.OZ2_ACCUMULATE, C=Cd)
+    torch.cuda.synchronize()
+    check(cbuf, Cd, oracle.dgemm(A, B, 12, C_in=C0).C)
+    # plain entry point
+    cbuf, Cd = _padded(np.zeros((m, n)), ldc, off, dev, fill=sentinel)
+    oz.ozaki2_dgemm(m, n, k, Ad, lda, Bd, ldb, Cd, ldc, 12)
+    torch.cuda.synchronize()
+    check(cbuf, Cd, res.C)
+    del plan
+    torch.cuda.synchronize()
+
+
+def test_batched_padded_leading_dimensions():
+    """The single-launch batched path with lda, ldb, ldc above the row counts
+    (odd), strides with gaps between problems and an unaligned base."""
+    import paper_2606_06510_amd as oz
+    import torch
+    dev = device()
+    nb, m, n, k = 5, 40, 50, 30
+    Ab, Bb = synth.batched(nb, m, n, k, seed=88)
+    lda, ldb, ldc = m + 3, k + 1, m + 5
+    sA, sB, sC = lda * k + 7, ldb * n + 3, ldc * n + 9
+    off = 1
+    abuf = torch.full((off + sA * nb,), float("nan"), dtype=torch.float64, device=dev)
+    bbuf = torch.full((off + sB * nb,), float("nan"), dtype=torch.float64, device=dev)
+    cbuf = torch.full((off + sC * nb,), -7.25, dtype=torch.float64, device=dev)
+    for b in range(nb):
+        abuf[off + b * sA:off + b * sA + lda * k].view(k, lda)[:, :m].copy_(
+            torch.from_numpy(np.ascontiguousarray(Ab[b].T)).to(dev))
+        bbuf[off + b * sB:off + b * sB + ldb * n].view(n, ldb)[:, :k].copy_(
+            torch.from_numpy(np.ascontiguousarray(Bb[b].T)).to(dev))
+    oz.ozaki2_dgemm_strided_batched(m, n, k, abuf[off:], lda, sA, bbuf[off:], ldb, sB, cbuf[off:],
+                                    ldc, sC, nb, 12)
+    torch.cuda.synchronize()
+    host = cbuf.cpu().numpy()
+    used = np.zeros(host.shape, dtype=bool)
+    for b in range(nb):
+        base = off + b * sC
+        Cb = host[base:base + ldc * n].reshape(n, ldc)[:, :m].T
+        used[base:base + ldc * n].reshape(n, ldc)[:, :m] = True
+        assert np.array_equal(bits(Cb), bits(oracle.dgemm(Ab[b], Bb[b], 12).C)), b
+    assert np.all(host[~used] == -7.25)
+
+
 def _batched_run(Ab, Bb, r):
     import paper_2606_06510_amd as oz
     import torch
