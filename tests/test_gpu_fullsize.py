@@ -136,6 +136,25 @@ def test_rankk32768x256_accumulate_sampled():
     _free()
 
 
+def test_outputs_beyond_2_pow_31():
+    """65536 x 40000 outputs (2.6e9, above 2^31) at k = 64: C, the staged
+    residues (12 x 2.6e9 int16, 63 GB) and the launch grids all need 64-bit
+    indexing; sampled entries, including the last row and columns whose
+    column-major offsets exceed 2^31, are bit-exact."""
+    m, n, k = 65536, 40000, 64
+    A, B = synth.lognormal(m, n, k, seed=77)
+    rng = np.random.default_rng(13)
+    rows = np.unique(np.concatenate([rng.choice(m, 10, replace=False), [0, m - 1]]))
+    cols = np.unique(np.concatenate([rng.choice(n, 10, replace=False), [0, 32768, n - 2, n - 1]]))
+    assert (m - 1) + (n - 1) * m > 2 ** 31
+    plan, Cd = _run(A, B, 12)
+    C = _sample_C(Cd, rows, cols)
+    res = oracle.dgemm(A, B, 12, rows=rows, cols=cols)
+    assert _check(C, res, A, B, rows, cols) == len(rows) * len(cols)
+    del plan, Cd
+    _free()
+
+
 def test_batched8192x64_sampled():
     import paper_2606_06510_amd as oz
     import torch
