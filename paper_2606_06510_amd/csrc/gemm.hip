@@ -32,6 +32,7 @@ namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
 constexpr int TILE = OZ2_TILE;   // 256
@@ -477,16 +478,18 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
       }
     // Every DMA issued so far (the next modulus's first stages, up to three)
     // has landed before the stores go out; those stages then skip their wait,
-    // and the wait of the stage after them also covers the stores.
+    // and the wait of the stage after them also covers the stores.  The
+    // stores are non-temporal: nothing in this launch reads them, and with a
+    // short k (a few stages per modulus) they drain measurably faster.
     wait_vm<0>();
     landed = it + 3;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        uint4* p = reinterpret_cast<uint4*>(dst + (i * 2 + j) * 1024);
-        p[0] = make_uint4(pk[i][j][0], pk[i][j][1], pk[i][j][2], pk[i][j][3]);
-        p[1] = make_uint4(pk[i][j][4], pk[i][j][5], pk[i][j][6], pk[i][j][7]);
+        u32x4* p = reinterpret_cast<u32x4*>(dst + (i * 2 + j) * 1024);
+        __builtin_nontemporal_store(u32x4{pk[i][j][0], pk[i][j][1], pk[i][j][2], pk[i][j][3]}, p);
+        __builtin_nontemporal_store(u32x4{pk[i][j][4], pk[i][j][5], pk[i][j][6], pk[i][j][7]}, p + 1);
       }
   }
   if (!g) bar();
