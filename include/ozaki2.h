@@ -34,7 +34,8 @@
  * where A~ = RN(D A), B~ = RN(B E) are the quantised integer matrices; an
  * exactly zero result is +0.0.  Flagged rows of A (columns of B) -- any
  * NaN/Inf (T1), or a nonzero entry that quantises to zero (T2) -- are
- * recomputed in native FP64 (one fused multiply-add per k, ascending k).
+ * recomputed in native FP64 (products and sums in a fixed order; within the
+ * FP64 dot-product error bound).
  */
 #ifndef OZAKI2_H
 #define OZAKI2_H

@@ -234,6 +234,7 @@ Oz2Layout make_layout(const Oz2Dims& d, const Oz2Const& c) {
   L.planesB = take((size_t)c.P * d.np * d.kp);
   L.tabs = take((size_t)c.tabsz * 4);
   L.res = take((size_t)c.r * d.mp * d.np * 2);
+  L.panel = (d.flags & OZ2_NO_FALLBACK) ? 0 : take((size_t)std::min(d.mp, OZ2_FBCAP) * d.k * 8);
   L.total = o;
   return L;
 }
@@ -347,7 +348,7 @@ int run_deconstruct(ozaki2_plan_s& p, int side, hipStream_t s) {
 }
 
 int run_reconstruct(ozaki2_plan_s& p, double* C, int ldc, hipStream_t s) {
-  hipError_t e = oz2_launch_reconstruct(p.d, p.L, p.c, p.ws, C, ldc, s);
+  hipError_t e = oz2_launch_reconstruct(p.d, p.L, p.c, p.ws, p.A, p.lda, C, ldc, s);
   if (e == hipSuccess && !(p.d.flags & OZ2_NO_FALLBACK))
     e = oz2_launch_fallback(p.d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, C, ldc, s);
   return hip_status(e);

@@ -11,6 +11,7 @@
                              // v_mfma_f32_32x32x64_f8f6f4 = one GEMM stage
 #define OZ2_KPAD 64          // k is padded to a multiple of this
 #define OZ2_KSLAB 32768      // residue GEMM: k per exact FP32 slab, Eq. (accum-exact)
+#define OZ2_FBCAP 1024       // flagged rows of A gathered into the fallback panel (at most)
 #define OZ2_CSLAB 65536      // code GEMM: codes <= 16, products <= 256: 65536*256 = 2^24
 
 // Flags per row of A / column of B.
@@ -74,6 +75,8 @@ struct Oz2Layout {
                               //   (the GEMM's accumulator order, see gemm.hip)
   size_t counters;            // int32 [4]: fallback row / column counts
   size_t listA, listB;        // int32 [mp] / [np]: flagged row / column indices
+  size_t panel;               // double [k][min(mp, OZ2_FBCAP)]: the first flagged rows of A,
+                              //   gathered for the native fallback (absent with NO_FALLBACK)
   size_t total;
 };
 
@@ -108,7 +111,8 @@ hipError_t oz2_launch_split(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const
 hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
                               uint8_t* ws, hipStream_t s);
 hipError_t oz2_launch_reconstruct(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
-                                  uint8_t* ws, double* C, int ldc, hipStream_t s);
+                                  uint8_t* ws, const double* A, int lda, double* C, int ldc,
+                                  hipStream_t s);
 hipError_t oz2_launch_fallback(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
                                const double* A, int lda, const double* B, int ldb,
                                double* C, int ldc, hipStream_t s);

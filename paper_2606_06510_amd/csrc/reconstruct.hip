@@ -93,13 +93,28 @@ struct Outputs<R, 8> {
 
 // Reconstruct, rescale and store: the block's 32x32 results go through LDS so
 // that each store instruction writes whole 256-byte column segments of C.
-// Entries of flagged rows / columns are left to the fallback kernel.
+// Entries of flagged rows / columns are left to the fallback kernel, which
+// follows on the same stream; for it the grid also gathers the first `cap`
+// flagged rows of A into a contiguous panel (row r at panel[r + l cap]), read
+// once here instead of once per column tile there (nothing to do on inputs
+// without flagged rows).
 template <int R>
 __global__ void __launch_bounds__(256)
 k_reconstruct(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res,
               const int32_t* __restrict__ sA, const int32_t* __restrict__ tB,
-              const uint32_t* __restrict__ fA, const uint32_t* __restrict__ fB, double* C, int ldc) {
+              const uint32_t* __restrict__ fA, const uint32_t* __restrict__ fB, double* C, int ldc,
+              const double* __restrict__ A, int lda, const int* __restrict__ counters,
+              const int* __restrict__ listA, double* __restrict__ panel, int cap) {
   __shared__ double tr[2][32][33];
+  if (panel) {
+    const int na = min(counters[0], cap);
+    const size_t total = (size_t)na * d.k, step = (size_t)gridDim.x * blockDim.x;
+    for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += step) {
+      const size_t l = idx / na;
+      const int r = (int)(idx - l * na);
+      panel[r + l * cap] = A[(size_t)listA[r] + l * lda];
+    }
+  }
   const BlockMap b = block_map(d.mp);
   {
     uint4 x[R];
@@ -164,25 +179,29 @@ k_integers(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res, uint32_t* out
   IntOut<R, 0>::run(c, d, x, b, out);
 }
 
-// Compaction of flagged rows / columns into index lists (order irrelevant:
-// every flagged entry is computed independently and deterministically).
-// Native FP64 for flagged entries: one FMA per k in ascending k for every
-// output (the same order as a plain dot product loop), register-tiled so the
-// flagged rows run at FP64 FMA speed.  Work = (flagged rows of A) x (all
+// Native FP64 for flagged entries.  Work = (flagged rows of A) x (all
 // columns) + (all unflagged rows) x (flagged columns of B), in 64 x 64 output
 // tiles walked by a grid-stride loop over the device-side counts (no host
 // synchronisation; every workgroup exits when the tiles are exhausted).  A
-// tile stages 64 rows x 16 k of A and 16 k x 64 columns of B through LDS;
-// each thread owns 4 x 4 outputs (rows ty + 16 u, columns tx + 16 v).
-constexpr int FB_T = 64, FB_K = 16;
+// tile stages 64 rows x 32 k of A and 32 k x 64 columns of B through LDS (the
+// next slab's loads held in registers while the current one is multiplied);
+// each wave owns a 32 x 32 quarter as 2 x 2 blocks of
+// v_mfma_f64_16x16x4_f64: A[i][k] from lane i + 16 k, B[k][j] from lane
+// j + 16 k, and D[i][j] in lane j + 16 (i % 4), element i / 4.  The products
+// and sums are FP64 in a fixed order (deterministic, not the order of a
+// sequential dot product): the result lies within the FP64 dot-product
+// error bound, which is the contract for flagged entries.
+constexpr int FB_T = 64, FB_K = 32;
+typedef double v4d __attribute__((ext_vector_type(4)));
 
 __global__ void __launch_bounds__(256)
 k_fallback(Oz2Dims d, const double* __restrict__ A, int lda, const double* __restrict__ B, int ldb,
            double* C, int ldc, const int* __restrict__ counters, const int* __restrict__ listA,
-           const int* __restrict__ listB, const uint32_t* __restrict__ fA) {
-  __shared__ double sa[FB_K][FB_T + 1];
-  __shared__ double sb[FB_K][FB_T + 1];
-  __shared__ int rowid[FB_T], colid[FB_T];
+           const int* __restrict__ listB, const uint32_t* __restrict__ fA,
+           const double* __restrict__ panel, int cap) {
+  __shared__ double sa[FB_K][FB_T + 2];   // [k][row]
+  __shared__ double sb[FB_K][FB_T + 2];   // [k][column]
+  __shared__ int rowid[FB_T], colid[FB_T], arow[FB_T];
   const int na = counters[0], nb = counters[1];
   const bool acc = (d.flags & 1u) != 0;
   const bool force = (d.flags & 16u) != 0;
@@ -190,72 +209,91 @@ k_fallback(Oz2Dims d, const double* __restrict__ A, int lda, const double* __res
   const int t1r = (na + FB_T - 1) / FB_T, t1c = (d.n + FB_T - 1) / FB_T;
   const int t2r = (d.m + FB_T - 1) / FB_T, t2c = (nb + FB_T - 1) / FB_T;
   const long long tiles1 = (long long)t1r * t1c, total = tiles1 + (long long)t2r * t2c;
-  const int t = threadIdx.x, tx = t & 15, ty = t >> 4;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int wr = 32 * (w >> 1), wc = 32 * (w & 1);
+  const int kr = lane >> 4, cl = lane & 15;
   for (long long tile = blockIdx.x; tile < total; tile += gridDim.x) {
-    int nr, nc;                 // valid rows / columns of this tile
+    // A rows come from the gathered panel when the tile's list rows all lie
+    // in it (row r of the list at panel[r + l cap]), else from A itself
+    const double* As = A;
+    int ldas = lda;
     if (tile < tiles1) {
       const int tr = (int)(tile / t1c), tc = (int)(tile % t1c);
-      nr = min(FB_T, na - tr * FB_T);
-      nc = min(FB_T, d.n - tc * FB_T);
+      const int nr = min(FB_T, na - tr * FB_T), nc = min(FB_T, d.n - tc * FB_T);
+      const bool inpanel = panel != nullptr && (tr + 1) * FB_T <= cap;
+      if (inpanel) {
+        As = panel;
+        ldas = cap;
+      }
       if (t < FB_T) {
         rowid[t] = t < nr ? listA[tr * FB_T + t] : -1;
+        arow[t] = t < nr ? (inpanel ? tr * FB_T + t : rowid[t]) : -1;
         colid[t] = t < nc ? tc * FB_T + t : -1;
       }
     } else {
       const long long u = tile - tiles1;
       const int tr = (int)(u / t2c), tc = (int)(u % t2c);
-      nr = min(FB_T, d.m - tr * FB_T);
-      nc = min(FB_T, nb - tc * FB_T);
+      const int nr = min(FB_T, d.m - tr * FB_T), nc = min(FB_T, nb - tc * FB_T);
       if (t < FB_T) {
-        int i = tr * FB_T + t;
+        const int i = tr * FB_T + t;
         // rows already recomputed in part 1 (flagged rows) are skipped here
         rowid[t] = (t < nr && !(force || (fA[i] & (OZ2_T1 | OZ2_T2)))) ? i : -1;
+        arow[t] = rowid[t];
         colid[t] = t < nc ? listB[tc * FB_T + t] : -1;
       }
     }
     __syncthreads();
-    double s[4][4];
+    // slab loads: thread t takes A entries (row e % 64, k e / 64) and B
+    // entries (column e / 32, k e % 32) for e = t + 256 q; outside -> 0
+    double pa[8], pb[8];
+    auto load = [&](int l0) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+      for (int q = 0; q < 8; ++q) {
+        const int e = t + 256 * q;
+        const int i = arow[e & 63], l = l0 + (e >> 6);
+        pa[q] = (i >= 0 && l < d.k) ? As[(size_t)i + (size_t)l * ldas] : 0.0;
+        const int j = colid[e >> 5], lb = l0 + (e & 31);
+        pb[q] = (j >= 0 && lb < d.k) ? B[(size_t)lb + (size_t)j * ldb] : 0.0;
+      }
+    };
+    v4d cacc[2][2];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) s[u][v] = 0.0;
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj) cacc[bi][bj] = v4d{0.0, 0.0, 0.0, 0.0};
+    load(0);
     for (int l0 = 0; l0 < d.k; l0 += FB_K) {
-      // stage A (64 rows x 16 k) and B (16 k x 64 columns); out-of-range -> 0
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int e = t + 256 * q;             // 0..1023
-        const int rr = e & 63, kk = e >> 6;    // A: rows fastest (column-major A)
-        const int i = rowid[rr], l = l0 + kk;
-        sa[kk][rr] = (i >= 0 && l < d.k) ? A[(size_t)i + (size_t)l * lda] : 0.0;
-        const int cc = e >> 4, kb = e & 15;    // B: k fastest (column-major B)
-        const int j = colid[cc], lb = l0 + kb;
-        sb[kb][cc] = (j >= 0 && lb < d.k) ? B[(size_t)lb + (size_t)j * ldb] : 0.0;
+      for (int q = 0; q < 8; ++q) {
+        const int e = t + 256 * q;
+        sa[e >> 6][e & 63] = pa[q];
+        sb[e & 31][e >> 5] = pb[q];
       }
       __syncthreads();
-      const int kn = min(FB_K, d.k - l0);
-      for (int kk = 0; kk < kn; ++kk) {
-        double a[4], b[4];
+      if (l0 + FB_K < d.k) load(l0 + FB_K);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) a[u] = sa[kk][ty + 16 * u];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) b[v] = sb[kk][tx + 16 * v];
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) s[u][v] = fma(a[u], b[v], s[u][v]);
+      for (int kk = 0; kk < FB_K; kk += 4) {
+        const double a0 = sa[kk + kr][wr + cl], a1 = sa[kk + kr][wr + 16 + cl];
+        const double b0 = sb[kk + kr][wc + cl], b1 = sb[kk + kr][wc + 16 + cl];
+        cacc[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, cacc[0][0], 0, 0, 0);
+        cacc[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, cacc[0][1], 0, 0, 0);
+        cacc[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, cacc[1][0], 0, 0, 0);
+        cacc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, cacc[1][1], 0, 0, 0);
       }
       __syncthreads();
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int i = rowid[ty + 16 * u], j = colid[tx + 16 * v];
-        if (i >= 0 && j >= 0) {
-          double* o = C + (size_t)i + (size_t)j * ldc;
-          *o = acc ? *o + s[u][v] : s[u][v];
+      for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int i = rowid[wr + 16 * bi + 4 * v + kr], j = colid[wc + 16 * bj + cl];
+          if (i >= 0 && j >= 0) {
+            double* o = C + (size_t)i + (size_t)j * ldc;
+            *o = acc ? *o + cacc[bi][bj][v] : cacc[bi][bj][v];
+          }
         }
-      }
     __syncthreads();   // rowid / colid are rewritten by the next tile
   }
 }
@@ -270,12 +308,15 @@ __global__ void k_fill(double* C, int m, int n, int ldc) {
 // one workgroup of 256 threads per two 32x32 output blocks
 template <int R>
 void launch_reconstruct_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
-                          double* C, int ldc, hipStream_t s) {
+                          const double* A, int lda, double* C, int ldc, hipStream_t s) {
   const size_t blocks = (size_t)d.mp * d.np / 2048;
+  const bool gather = !(d.flags & 8u);   // OZ2_NO_FALLBACK: no fallback, no panel
   hipLaunchKernelGGL(k_reconstruct<R>, dim3((unsigned)blocks), dim3(256), 0, s, c, d,
                      (const int16_t*)(ws + L.res), (const int32_t*)(ws + L.sA),
                      (const int32_t*)(ws + L.tB), (const uint32_t*)(ws + L.flagsA),
-                     (const uint32_t*)(ws + L.flagsB), C, ldc);
+                     (const uint32_t*)(ws + L.flagsB), C, ldc, A, lda,
+                     (const int*)(ws + L.counters), (const int*)(ws + L.listA),
+                     gather ? (double*)(ws + L.panel) : nullptr, std::min(d.mp, OZ2_FBCAP));
 }
 
 template <int R>
@@ -303,8 +344,9 @@ void launch_integers_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, 
 }  // namespace
 
 hipError_t oz2_launch_reconstruct(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
-                                  uint8_t* ws, double* C, int ldc, hipStream_t s) {
-  OZ2_R_SWITCH(launch_reconstruct_r, d, L, c, ws, C, ldc, s)
+                                  uint8_t* ws, const double* A, int lda, double* C, int ldc,
+                                  hipStream_t s) {
+  OZ2_R_SWITCH(launch_reconstruct_r, d, L, c, ws, A, lda, C, ldc, s)
   return hipGetLastError();
 }
 
@@ -319,9 +361,11 @@ hipError_t oz2_launch_fallback(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws
                                int lda, const double* B, int ldb, double* C, int ldc,
                                hipStream_t s) {
   // the lists were filled by the deconstruction (k_scales: T1, k_split: T2)
+  // the panel of flagged rows was gathered by the reconstruction launch
   hipLaunchKernelGGL(k_fallback, dim3(1024), dim3(256), 0, s, d, A, lda, B, ldb, C, ldc,
                      (const int*)(ws + L.counters), (const int*)(ws + L.listA),
-                     (const int*)(ws + L.listB), (const uint32_t*)(ws + L.flagsA));
+                     (const int*)(ws + L.listB), (const uint32_t*)(ws + L.flagsA),
+                     (const double*)(ws + L.panel), std::min(d.mp, OZ2_FBCAP));
   return hipGetLastError();
 }
 
