@@ -106,15 +106,7 @@ k_reconstruct(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res,
               const double* __restrict__ A, int lda, const int* __restrict__ counters,
               const int* __restrict__ listA, double* __restrict__ panel, int cap) {
   __shared__ double tr[2][32][33];
-  if (panel) {
-    const int na = min(counters[0], cap);
-    const size_t total = (size_t)na * d.k, step = (size_t)gridDim.x * blockDim.x;
-    for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += step) {
-      const size_t l = idx / na;
-      const int r = (int)(idx - l * na);
-      panel[r + l * cap] = A[(size_t)listA[r] + l * lda];
-    }
-  }
+  const int nflag = panel ? counters[0] : 0;   // used at the end; loaded early
   const BlockMap b = block_map(d.mp);
   {
     uint4 x[R];
@@ -129,18 +121,25 @@ k_reconstruct(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res,
   const bool force = (d.flags & 16u) != 0;     // OZ2_FORCE_FALLBACK
   const int rr = b.tt & 31;
   const int row = b.row0 + rr;
-  if (row >= d.m) return;
-  const bool rowfb = !nofb && (force || (fA[row] & (OZ2_T1 | OZ2_T2)));
-  if (rowfb) return;
+  if (row < d.m && !(!nofb && (force || (fA[row] & (OZ2_T1 | OZ2_T2))))) {
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int cc = j * 4 + (b.tt >> 5);
-    const int col = b.col0 + cc;
-    if (col < d.n && (nofb || !(fB[col] & (OZ2_T1 | OZ2_T2)))) {
-      double* o = C + (size_t)col * ldc + row;
-      const double v = tr[b.hb][cc][rr];
-      *o = acc ? *o + v : v;
+    for (int j = 0; j < 8; ++j) {
+      const int cc = j * 4 + (b.tt >> 5);
+      const int col = b.col0 + cc;
+      if (col < d.n && (nofb || !(fB[col] & (OZ2_T1 | OZ2_T2)))) {
+        double* o = C + (size_t)col * ldc + row;
+        const double v = tr[b.hb][cc][rr];
+        *o = acc ? *o + v : v;
+      }
     }
+  }
+  // the fallback's panel: grid-stride over (row of the list, k)
+  const int na = min(nflag, cap);
+  const size_t total = (size_t)na * d.k, step = (size_t)gridDim.x * blockDim.x;
+  for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += step) {
+    const size_t l = idx / na;
+    const int r = (int)(idx - l * na);
+    panel[r + l * cap] = A[(size_t)listA[r] + l * lda];
   }
 }
 
