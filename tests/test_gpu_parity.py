@@ -120,6 +120,21 @@ def test_no_fallback_and_force_fallback():
     compare_C(C2, A, B, res2)
 
 
+def test_force_fallback_beyond_the_panel():
+    """All 1300 rows flagged (and two columns of B by their values): the
+    fallback reads the first 1024 listed rows of A from the panel the
+    reconstruction gathered and the rest straight from A; every entry within
+    the FP64 dot-product bound."""
+    A, B = synth.uniform(1300, 150, 120, seed=15)
+    B = B.copy()
+    B[::2, 7] *= 1e-250                       # T2 on two columns of B
+    B[::3, 90] *= 1e250
+    res = oracle.dgemm(A, B, 12, force_fallback=True)
+    assert len(res.fallback_rows) == 1300
+    plan, C = run_staged(A, B, 12, flags=16)
+    compare_C(C, A, B, res)
+
+
 def test_multi_slab_k():
     """k above the 32768 residue slab and the 65536 code slab."""
     A, B = synth.uniform(40, 48, 70000, seed=12)
