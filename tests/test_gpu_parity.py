@@ -188,6 +188,26 @@ def test_plain_entry_point_and_batched():
         assert np.array_equal(bits(Cb[b]), bits(rb.C))
 
 
+@pytest.mark.parametrize("shape", [(100, 80, 70), (48, 40, 200)])
+def test_strided_batched_beyond_the_single_launch(shape):
+    """Strided-batched products larger than 64 in some dimension take the
+    staged path once per problem on the internal workspace; each bit-exact."""
+    import paper_2606_06510_amd as oz
+    import torch
+    dev = device()
+    m, n, k = shape
+    nb = 3
+    Ab, Bb = synth.batched(nb, m, n, k, seed=m + n + k)
+    Ad = torch.from_numpy(np.ascontiguousarray(Ab.transpose(0, 2, 1))).to(dev)
+    Bd = torch.from_numpy(np.ascontiguousarray(Bb.transpose(0, 2, 1))).to(dev)
+    Cd = torch.full((nb, n, m), float("nan"), dtype=torch.float64, device=dev)
+    oz.ozaki2_dgemm_strided_batched(m, n, k, Ad, m, m * k, Bd, k, k * n, Cd, m, m * n, nb, 12)
+    torch.cuda.synchronize()
+    Cb = Cd.cpu().numpy().transpose(0, 2, 1)
+    for b in range(nb):
+        assert np.array_equal(bits(Cb[b]), bits(oracle.dgemm(Ab[b], Bb[b], 12).C)), b
+
+
 def test_plain_entry_point_from_two_threads():
     """Two host threads issue plain ozaki2_dgemm calls on one stream while the
     library's internal workspace grows under them (each thread's calls get
