@@ -56,6 +56,17 @@ __device__ __forceinline__ v8i frag(const uint8_t (*pl)[PP], int base) {
   return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
 }
 
+// two operands in one: k 0..63 of plane `lo` in lanes 0..31 and k 0..63 of
+// plane `hi` in lanes 32..63 (the instruction's K = 128), so one MFMA sums
+// the products of both pairs
+__device__ __forceinline__ v8i frag2(const uint8_t (*lo)[PP], const uint8_t (*hi)[PP], int base) {
+  const int lane = threadIdx.x & 63;
+  const uint8_t* p = (lane < 32 ? lo : hi)[base + (lane & 15)] + 32 * ((lane >> 4) & 1);
+  const uint4 l4 = *reinterpret_cast<const uint4*>(p);
+  const uint4 h4 = *reinterpret_cast<const uint4*>(p + 16);
+  return v8i{(int)l4.x, (int)l4.y, (int)l4.z, (int)l4.w, (int)h4.x, (int)h4.y, (int)h4.z, (int)h4.w};
+}
+
 __device__ __forceinline__ v4f mfma(v8i a, v8i b, v4f c) {
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
@@ -119,12 +130,11 @@ __device__ __forceinline__ void modulus_chain(const Oz2Const& c, int i, const Sm
   };
   acc[0] = v4f{0.f};
   acc[1] = v4f{0.f};
-  if (s) {          // (d1 e0 + d0 e1) x s + d0 e0
-    const v8i a1 = frag(S.pa[1], rb0), a0 = frag(S.pa[0], rb0);
+  if (s) {          // (d1 e0 + d0 e1) x s + d0 e0, the cross pair in one MFMA
+    const v8i a10 = frag2(S.pa[1], S.pa[0], rb0), a0 = frag(S.pa[0], rb0);
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      acc[q] = mfma(a1, frag(S.pb[0], cb0 + 16 * q), acc[q]);
-      acc[q] = mfma(a0, frag(S.pb[1], cb0 + 16 * q), acc[q]);
+      acc[q] = mfma(a10, frag2(S.pb[0], S.pb[1], cb0 + 16 * q), acc[q]);
       acc[q] = reduce_mul(acc[q], (float)s);
       acc[q] = mfma(a0, frag(S.pb[0], cb0 + 16 * q), acc[q]);
     }
