@@ -29,7 +29,7 @@ struct Smem {
   int2 qa[64][64];
   int2 qb[64][64];
   uint8_t pa[3][64][PP];
-  uint8_t pb[3][64][PP];
+  uint8_t pb[4][64][PP];     // B: d0, d1, d0 + d1 and, for nonsquare moduli, -16 d1
   unsigned long long rbits[64], cbits[64];
   uint32_t Rm[64], Km[64];
   int sS[64], sT[64];
@@ -90,6 +90,8 @@ __device__ __forceinline__ void quantise8(const double (&x)[8], int sc, bool& t2
 }
 
 // 8 plane bytes of this thread's quantised chunk into the planes of modulus i
+// (FOUR: also the -16 d1 plane of a nonsquare modulus, for B)
+template <bool FOUR>
 __device__ __forceinline__ void split8(const Oz2Const& c, int i, const uint32_t* tab,
                                        const int2* q, uint8_t (*pl)[64][PP], int row, int ch) {
   const double m = (double)c.m[i], c32 = (double)c.c32[i], dinv = c.dinv[i];
@@ -113,6 +115,12 @@ __device__ __forceinline__ void split8(const Oz2Const& c, int i, const uint32_t*
     v2.x = gather_byte(e[0], e[1], e[2], e[3], 0x05010602u);
     v2.y = gather_byte(e[4], e[5], e[6], e[7], 0x05010602u);
     *reinterpret_cast<uint2*>(&pl[2][row][ch]) = v2;
+    if (FOUR) {
+      uint2 v3;
+      v3.x = gather_byte(e[0], e[1], e[2], e[3], 0x05010703u);
+      v3.y = gather_byte(e[4], e[5], e[6], e[7], 0x05010703u);
+      *reinterpret_cast<uint2*>(&pl[3][row][ch]) = v3;
+    }
   }
 }
 
@@ -138,13 +146,13 @@ __device__ __forceinline__ void modulus_chain(const Oz2Const& c, int i, const Sm
       acc[q] = reduce_mul(acc[q], (float)s);
       acc[q] = mfma(a0, frag(S.pb[0], cb0 + 16 * q), acc[q]);
     }
-  } else {          // ((d1 e1) x rho0 + d0 e0) x rho1 + (d0+d1)(e0+e1), then x 16
-    const v8i a1 = frag(S.pa[1], rb0), a0 = frag(S.pa[0], rb0), a2 = frag(S.pa[2], rb0);
+  } else {          // (d1 (-16 e1) + d0 e0) x rho1 + (d0+d1)(e0+e1), then x 16
+    // (-16 = 240 / -15 mod m; the first pair in one MFMA, exact for k <= 64:
+    // |sum| < 2^19)
+    const v8i a10 = frag2(S.pa[1], S.pa[0], rb0), a2 = frag(S.pa[2], rb0);
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      acc[q] = mfma(a1, frag(S.pb[1], cb0 + 16 * q), acc[q]);
-      acc[q] = reduce_mul(acc[q], (float)c.rho0[i]);
-      acc[q] = mfma(a0, frag(S.pb[0], cb0 + 16 * q), acc[q]);
+      acc[q] = mfma(a10, frag2(S.pb[3], S.pb[0], cb0 + 16 * q), acc[q]);
       acc[q] = reduce_mul(acc[q], (float)c.rho1[i]);
       acc[q] = mfma(a2, frag(S.pb[2], cb0 + 16 * q), acc[q]);
     }
@@ -377,8 +385,8 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
       for (int I = 0; I < 8; ++I) S0[I] = S1[I] = S2[I] = 0.0;
 #pragma nounroll
       for (int i = 0; i < R; ++i) {
-        split8(c, i, tab, &S.qa[row][ch], S.pa, row, ch);
-        split8(c, i, tab, &S.qb[row][ch], S.pb, row, ch);
+        split8<false>(c, i, tab, &S.qa[row][ch], S.pa, row, ch);
+        split8<true>(c, i, tab, &S.qb[row][ch], S.pb, row, ch);
         __syncthreads();
         v4f acc[2];
         modulus_chain(c, i, S, rb0, cb0, acc);
@@ -394,8 +402,8 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
       uint4 res[R];
 #pragma nounroll
       for (int i = 0; i < R; ++i) {
-        split8(c, i, tab, &S.qa[row][ch], S.pa, row, ch);
-        split8(c, i, tab, &S.qb[row][ch], S.pb, row, ch);
+        split8<false>(c, i, tab, &S.qa[row][ch], S.pa, row, ch);
+        split8<true>(c, i, tab, &S.qb[row][ch], S.pb, row, ch);
         __syncthreads();
         put_res<R>(res, i, modulus_products(c, i, S, rb0, cb0));
         __syncthreads();

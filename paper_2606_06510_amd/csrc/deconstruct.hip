@@ -467,7 +467,9 @@ __global__ void k_scales(Oz2Dims d, const unsigned long long* __restrict__ rowbi
 }
 
 // residue -> plane bytes: entry toff[i] + d = E4M3(d0) | E4M3(d1) << 8 |
-// E4M3(d0 + d1) << 16 (the third byte unused for square moduli)
+// E4M3(d0 + d1) << 16 | E4M3(-16 d1) << 24 (exact: |16 d1| <= 256; the
+// last two bytes are used for nonsquare moduli only, the fourth by the
+// single-launch batched kernel)
 __global__ void k_plane_tables(Oz2Const c, uint32_t* tab) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= c.tabsz) return;
@@ -479,7 +481,9 @@ __global__ void k_plane_tables(Oz2Const c, uint32_t* tab) {
   oz2_digits(d, m, c.sq[i], d0, d1);
   const int lo = __builtin_amdgcn_cvt_pk_fp8_f32((float)d0, (float)d1, 0, false);
   const int hi = __builtin_amdgcn_cvt_pk_fp8_f32((float)(d0 + d1), 0.0f, 0, false);
-  tab[idx] = ((uint32_t)lo & 0xFFFFu) | (((uint32_t)hi & 0xFFu) << 16);
+  const int b3 = __builtin_amdgcn_cvt_pk_fp8_f32((float)(-16 * d1), 0.0f, 0, false);
+  tab[idx] = ((uint32_t)lo & 0xFFFFu) | (((uint32_t)hi & 0xFFu) << 16) |
+             (((uint32_t)b3 & 0xFFu) << 24);
 }
 
 // Plane bytes are written once and read back only by the residue GEMMs, after
