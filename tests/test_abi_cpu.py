@@ -68,6 +68,14 @@ def test_workspace_bytes():
     b = oz.ozaki2_workspace_bytes(4096, 4096, 4096, 12)
     assert b >= 30 * 2 * 4096 * 4096 + 24 * 4096 * 4096
     assert b < 1.05 * (31 * 2 * 4096 * 4096 + 24 * 4096 * 4096) + (1 << 20)
+    # the native fallback's panel of gathered rows: min(mp, 1024) x k doubles,
+    # absent with OZ2_NO_FALLBACK
+    for m, k in [(4096, 4096), (300, 200), (32768, 256)]:
+        mp = (m + 255) // 256 * 256
+        diff = oz.ozaki2_workspace_bytes(m, 512, k, 12) - \
+            oz.ozaki2_workspace_bytes(m, 512, k, 12, oz.OZ2_NO_FALLBACK)
+        panel = min(mp, 1024) * k * 8
+        assert panel <= diff < panel + 256, (m, k, diff, panel)
     assert oz.ozaki2_workspace_bytes(10, 10, 10, 7) == 0
     assert oz.ozaki2_workspace_bytes(10, 10, 10, 12, 1 << 10) == 0
     assert oz.ozaki2_workspace_bytes(-1, 10, 10, 12) == 0
