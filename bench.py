@@ -101,8 +101,8 @@ def pmc_mfma(kernel_src, tag):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on exactly one GPU (the emulated GEMM is a "
-              "single-GPU kernel path; see the sharding design notes). Use --gpus 1.",
+        print("bench.py: the emulated GEMM runs on one GPU (a single-GPU kernel path; "
+              "its sharding over several GPUs is not implemented). Use --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
 
