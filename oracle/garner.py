@@ -43,14 +43,6 @@ def garner_digits(x, ms):
     return v
 
 
-def garner_op_count(r):
-    """Narrow operations Garner performs per output, counted as the paper does
-    in Alg. 1: r(r-1)/2 multiply-adds of the digit sums plus two narrow
-    operations (subtract-and-reduce, scale by the inverse) per modulus."""
-    mads = sum(k for k in range(r))          # sum_{k=1}^{r-1} k
-    return mads + 2 * r
-
-
 def mixed_radix_value(v, ms):
     """X = sum_k v_k P_{k-1} as Python ints (object array), X in [0, M)."""
     P = prefix_products(ms)

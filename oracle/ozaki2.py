@@ -18,9 +18,9 @@ Phase 2 (modular GEMMs, Eq. (modgemm)): centred residues of A~, B~ per
   modulus; C^(i) = (A~ mod m_i)(B~ mod m_i) mod m_i, centred.
 Phase 3 (Eq. (garner)): CRT -> exact integer C~ in [-M/2, M/2), then
   C = D^-1 C~ E^-1 rounded once to binary64.
-Fallback (Alg. 1 "fall back to native FP64 on the offending rows"; the
-  contract's item (vi)): T1/T2 rows of A and columns of B are computed in
-  native FP64 instead.
+Fallback (Alg. 1, fallback step; the contract's item (vi)): rows of A and
+  columns of B the scaling cannot certify (T1/T2) are computed in native FP64
+  instead.
 
 READINGS (where the paper is silent; each is also listed in the design notes):
 * The max-magnitude pass is realised with 4-bit codes relative to the row
@@ -110,6 +110,13 @@ def magnitude_codes(A, E, t1):
     c = np.where(a > 0, np.maximum(c, 1.0), 0.0)
     c = np.where(t1[:, None], 0.0, c)
     return c.astype(np.int64)
+
+
+def combine_slabs(total, slab_max):
+    """R_i over a k longer than one 65536-wide code slab: the SUM of the
+    slab-wise row maxima (READING; an upper bound of max_j G'_ij because the
+    maximum of a sum is at most the sum of the maxima)."""
+    return total + slab_max
 
 
 def ell(x):
@@ -235,9 +242,9 @@ def dgemm(A, B, r=12, *, rows=None, cols=None, mode="bound", quant="rn",
         for l0 in range(0, max(k, 1), CODE_SLAB):
             sl = slice(l0, min(k, l0 + CODE_SLAB))
             if n:
-                R[rows] += (cAm[rows, sl] @ cBm[sl]).max(axis=1).astype(np.int64)
+                R[rows] = combine_slabs(R[rows], (cAm[rows, sl] @ cBm[sl]).max(axis=1).astype(np.int64))
             if m:
-                K[cols] += (cAm[:, sl] @ cBm[sl, cols]).max(axis=0).astype(np.int64)
+                K[cols] = combine_slabs(K[cols], (cAm[:, sl] @ cBm[sl, cols]).max(axis=0).astype(np.int64))
         sig = widths(R, cA)
         tau = widths(K, cB)
     elif mode == "fixed":

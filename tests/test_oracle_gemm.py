@@ -217,3 +217,57 @@ def test_row_col_sampling_matches_full():
     part = oracle.dgemm(A, B, 12, rows=rows, cols=cols)
     assert np.array_equal(part.C, full.C[np.ix_(rows, cols)])
     assert np.array_equal(part.residues, full.residues[:, rows][:, :, cols])
+
+
+def _slab_bound_case(r):
+    """1 x 196608 times 196608 x 1, every entry 1 - 2^-53: three full 65536-wide
+    code slabs, every code 16 (the largest), so each slab's code product is
+    256 * 65536 = 2^24.  Returns the oracle result, the exact
+    sum_l |A~_l| |B~_l| (Python ints) and M."""
+    k = 3 * ozaki2.CODE_SLAB
+    x = 1.0 - 2.0 ** -53
+    A = np.full((1, k), x)
+    B = np.full((k, 1), x)
+    res = oracle.dgemm(A, B, r)
+    Aq, Bq = res.extras["Aq"], res.extras["Bq"]
+    assert np.all(Aq == Aq[0, 0]) and np.all(Bq == Bq[0, 0])
+    total = k * abs(int(Aq[0, 0])) * abs(int(Bq[0, 0]))
+    return res, total, res.extras["M"], A, B
+
+
+@pytest.mark.parametrize("r", [8, 9, 12, 15])
+def test_code_slab_bound_beyond_65536(r):
+    """k above one code slab: R_i and K_j are the sums of the three slab maxima
+    (3 * 2^24), Eq. (M-bound) holds exactly (Python ints), and C is the
+    correctly rounded value of the exact product A~ B~ 2^-(s+t), within the
+    closed-form quantisation bound of the exact A B."""
+    res, total, M, A, B = _slab_bound_case(r)
+    assert int(res.R[0]) == 3 * 2 ** 24 and int(res.K[0]) == 3 * 2 ** 24
+    assert 2 * total < M
+    assert int(res.X[0, 0]) == total            # all terms positive and equal
+    e = int(res.sA[0] + res.tB[0])
+    want = Fraction(total, 2 ** e) if e >= 0 else Fraction(total * 2 ** -e)
+    assert res.C[0, 0] == float(want)
+    exact = Fraction(A.shape[1]) * Fraction(A[0, 0]) * Fraction(B[0, 0])
+    k = A.shape[1]
+    bound = (Fraction(1, 2) * Fraction(2) ** -int(res.sA[0]) * k * Fraction(B[0, 0])
+             + Fraction(1, 2) * Fraction(2) ** -int(res.tB[0]) * k * Fraction(A[0, 0])
+             + Fraction(k, 4) * Fraction(2) ** -e + Fraction(2) ** -53 * abs(exact))
+    assert abs(Fraction(res.C[0, 0]) - exact) <= bound
+
+
+@pytest.mark.parametrize("r", [8, 9, 15])
+def test_code_slab_bound_catches_a_max_over_slabs_slip(r, monkeypatch):
+    """The pin above is not vacuous: with the slip of taking the maximum over
+    slabs instead of the sum (planted in the oracle here, on the CPU) the
+    scales grow by one binary order on each side and the range condition
+    Eq. (M-bound) fails for this input at r = 8, 9 and 15 (at r = 12 the
+    factor-4 growth happens to stay below M/2)."""
+    monkeypatch.setattr(ozaki2, "combine_slabs", np.maximum)
+    try:
+        res, total, M, A, B = _slab_bound_case(r)
+        assert int(res.R[0]) == 2 ** 24             # the slip is in effect
+        violated = 2 * total >= M
+    except AssertionError as e:                     # the oracle's own range check
+        violated = "range condition" in str(e)
+    assert violated

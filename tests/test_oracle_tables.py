@@ -5,7 +5,7 @@ import math
 import numpy as np
 import pytest
 
-from oracle import e4m3, garner, moduli, planes
+from oracle import e4m3, moduli, planes
 
 
 def test_set_S_matches_paper(golden):
@@ -29,10 +29,6 @@ def test_log2M_and_plane_counts(golden):
     assert moduli.p_store(ms) == golden["p_store_S"]["value"]
     assert moduli.p_mma(ms) == golden["p_mma_S"]["value"]
     assert moduli.alpha(ms) == golden["alpha_r12"]["value"]
-
-
-def test_garner_op_count(golden):
-    assert garner.garner_op_count(12) == golden["N_gamma_r12"]["value"]
 
 
 def test_e4m3_format(golden):
