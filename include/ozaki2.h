@@ -25,7 +25,10 @@
  * and ozaki2_finalize.
  * Validation happens before any launch: on an error nothing is written.
  * Asynchronous device faults surface at the caller's next synchronisation.
- * num_moduli (r) must be in [8, 16]; the moduli are the paper's r = 12 set
+ * num_moduli (r) must be in [8, 16]: the paper works with 8-12 moduli and up
+ * to a conservative 15; with fewer the modulus product leaves too few bits for
+ * anything near FP64 accuracy (r = 8 already stops near 1e-11 on the
+ * lognormal workload), so r < 8 returns OZ2_E_INVALID.  The moduli are the paper's r = 12 set
  * (1089, 1024, 961, 841, 625, 529, 511, 509, 503, 499, 491, 487) extended by
  * the nonsquare 481, 479, 467, 463 and truncated to the r largest.
  * Limits: m, n, k >= 0 and m*k, k*n, m*n each below 2^40.
@@ -62,7 +65,13 @@ enum {
   OZ2_SCALE_FIXED = 2u,    /* no max-magnitude pass: mu = k max|A~| max|B~| (alpha = 3r) */
   OZ2_QUANT_TZ = 4u,       /* quantise by truncation toward zero instead of RN-even */
   OZ2_NO_FALLBACK = 8u,    /* never recompute flagged rows natively */
-  OZ2_FORCE_FALLBACK = 16u /* recompute every row natively (testing aid) */
+  OZ2_FORCE_FALLBACK = 16u,/* recompute every row natively (testing aid) */
+  OZ2_KEEP_RESIDUES = 32u, /* materialise the r residues of every output in the workspace:
+                              ozaki2_dgemm_ex then takes the staged route even where its
+                              fused residue-GEMM + reconstruction kernel would serve; a
+                              plan's stages always keep them (implied) */
+  OZ2_TIME_STAGES = 64u    /* plans only: record HIP events between the stages on the
+                              stream of each call (OZ2_Q_STAGE_TIMES) */
 };
 
 /* C = A*B with the default flags (accumulation: ozaki2_dgemm_ex).
@@ -130,7 +139,8 @@ int ozaki2_deconstruct_a(ozaki2_plan_t plan, const double* A, int lda, void* str
 int ozaki2_deconstruct_b(ozaki2_plan_t plan, const double* B, int ldb, void* stream);
 
 /* Phase 2: the 3r FP8 plane products and their exact modular accumulation;
- * writes the r centred residues of every output entry into the workspace. */
+ * writes, per modulus, a representative of every output's residue into the
+ * workspace (OZ2_Q_RESIDUES). */
 int ozaki2_residue_gemm(ozaki2_plan_t plan, void* stream);
 
 /* Phase 3: CRT reconstruction, inverse scaling with one rounding, then the
@@ -141,15 +151,24 @@ int ozaki2_reconstruct(ozaki2_plan_t plan, double* C, int ldc, void* stream);
 /* Diagnostics for tests: synchronises the device, then copies a plan
  * quantity to host memory.  ozaki2_plan_query_bytes gives the size. */
 enum {
-  OZ2_Q_EXPONENTS = 1,     /* int32 E^A[m] then E^B[n] (frexp exponent of row/col max) */
+  OZ2_Q_EXPONENTS = 1,     /* int32 E^A[m] then E^B[n]: frexp exponent of the row/col maximum
+                              as the scale kernel computed it (0 for a zero or T1 row) */
   OZ2_Q_MAXIMA = 2,        /* uint64 R[m] then K[n] (code-product row/col maxima) */
   OZ2_Q_SCALES = 3,        /* int32 s[m] then t[n] (power-of-two scales) */
   OZ2_Q_FLAGS = 4,         /* uint32 flagsA[m] then flagsB[n]: bit0 T1, bit1 T2 */
   OZ2_Q_CODES = 5,         /* uint8 codes of A [m][k] then of B [n][k] (E4M3 bytes) */
   OZ2_Q_PLANES = 6,        /* uint8 planes of A [p_store][m][k] then of B [p_store][n][k] */
-  OZ2_Q_RESIDUES = 7,      /* int16 [r][n][m] centred residues (after residue_gemm) */
-  OZ2_Q_INTEGERS = 8,      /* uint32 [n][m][5]: exact integer, two's complement, 160 bits LE */
-  OZ2_Q_FALLBACK_COUNT = 9 /* int32 [2]: rows of A, columns of B the reconstruction recomputes natively */
+  OZ2_Q_RESIDUES = 7,      /* int16 [r][n][m]: per modulus the representative of C~ mod m_i the
+                              residue GEMMs left for the reconstruction (any value congruent
+                              to C~ with magnitude <= m_i/2 + 32; after residue_gemm) */
+  OZ2_Q_INTEGERS = 8,      /* uint32 [n][m][5]: exact integer, two's complement, 160 bits LE,
+                              formed from those residues by the reconstruction's own routine */
+  OZ2_Q_FALLBACK_COUNT = 9,/* int32 [2]: rows of A, columns of B the reconstruction recomputes natively */
+  OZ2_Q_STAGE_TIMES = 10   /* float [6], milliseconds, of the last deconstruct / residue_gemm /
+                              reconstruct of an OZ2_TIME_STAGES plan: scan + codes (a1, a2),
+                              max-magnitude GEMM (a3), scales + split (a4), residue GEMMs
+                              (a5), reconstruction (a6), native fallback (a7); OZ2_E_INVALID
+                              unless all three stages ran since the last deconstruct */
 };
 size_t ozaki2_plan_query_bytes(ozaki2_plan_t plan, int what);
 int ozaki2_plan_query(ozaki2_plan_t plan, int what, void* host_out, size_t bytes);

@@ -56,6 +56,33 @@ int ozaki2_probe_mfma_digits(int iters, double* tflops);
  * *gbs = (read + write bytes) / s / 1e9. */
 int ozaki2_probe_copy_peak(size_t bytes, int reps, double* gbs);
 
+/* The reconstruction's own integer and rounding routines (the direct CRT
+ * sum of Eq. (garner)'s unique integer in radix-2^38 limbs for r <= 12, in
+ * 32-bit words above; one RN-even rounding) applied to n given residue
+ * vectors, for tests that reach the rare branches -- integers next to +-M/2,
+ * where the quotient estimate needs the exact range check -- which random
+ * products almost never produce.  residues: int16 [num_moduli][n] (modulus i
+ * in ascending order; any representative with |x| <= 577, the bound the
+ * residue GEMMs guarantee; larger values give undefined results but no
+ * out-of-bounds access), shifts: int [n]; words: uint32 [n][5] (the integer
+ * in [-M/2, M/2), two's complement, little endian), rounded: double [n]
+ * (the integer times 2^-shift, rounded once).  Device pointers; asynchronous.
+ * OZ2_E_INVALID for n < 0, num_moduli outside [8, 16] or a null pointer. */
+int ozaki2_probe_crt(int num_moduli, const short* residues, const int* shifts, int n,
+                     unsigned* words, double* rounded, void* stream);
+
+/* The single-launch batched kernel of ozaki2_dgemm_strided_batched
+ * (m, n, k <= 64) with its last step switched to writing, instead of C, the
+ * exact integer it reconstructs for every output whose row and column are
+ * not flagged: words = uint32 [batch][n][m][5] (device, two's complement,
+ * little endian; entries of flagged rows / columns are left untouched).
+ * Same A, B conventions as ozaki2_dgemm_strided_batched.  Uses the library's
+ * internal workspace for the plane tables.  OZ2_E_INVALID for sizes outside
+ * 1..64, a negative batch or stride, lda < m, ldb < k or a null pointer. */
+int ozaki2_probe_batched_integers(int m, int n, int k, const double* A, int lda,
+                                  long long strideA, const double* B, int ldb, long long strideB,
+                                  int batch, int num_moduli, unsigned* words, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

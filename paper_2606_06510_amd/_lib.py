@@ -27,6 +27,8 @@ OZ2_SCALE_FIXED = 2
 OZ2_QUANT_TZ = 4
 OZ2_NO_FALLBACK = 8
 OZ2_FORCE_FALLBACK = 16
+OZ2_KEEP_RESIDUES = 32
+OZ2_TIME_STAGES = 64
 
 OZ2_Q_EXPONENTS = 1
 OZ2_Q_MAXIMA = 2
@@ -37,6 +39,10 @@ OZ2_Q_PLANES = 6
 OZ2_Q_RESIDUES = 7
 OZ2_Q_INTEGERS = 8
 OZ2_Q_FALLBACK_COUNT = 9
+OZ2_Q_STAGE_TIMES = 10
+
+# the six stages OZ2_Q_STAGE_TIMES reports, in its order
+STAGE_NAMES = ["scan_codes", "maxmag_gemm", "split", "residue_gemm", "reconstruct", "fallback"]
 
 EXPORTS = [
     "ozaki2_dgemm", "ozaki2_dgemm_ex", "ozaki2_dgemm_strided_batched",
@@ -50,7 +56,8 @@ EXPORTS = [
 # include/ozaki2_probes.h
 PROBE_EXPORTS = [
     "ozaki2_probe_e4m3", "ozaki2_probe_accum", "ozaki2_probe_copy", "ozaki2_probe_mfma_peak",
-    "ozaki2_probe_mfma_digits", "ozaki2_probe_copy_peak",
+    "ozaki2_probe_mfma_digits", "ozaki2_probe_copy_peak", "ozaki2_probe_crt",
+    "ozaki2_probe_batched_integers",
 ]
 
 
@@ -96,6 +103,8 @@ def load():
         "ozaki2_probe_mfma_peak": (i, [i, ctypes.POINTER(ctypes.c_double)]),
         "ozaki2_probe_mfma_digits": (i, [i, ctypes.POINTER(ctypes.c_double)]),
         "ozaki2_probe_copy_peak": (i, [sz, i, ctypes.POINTER(ctypes.c_double)]),
+        "ozaki2_probe_crt": (i, [i, p, p, i, p, p, p]),
+        "ozaki2_probe_batched_integers": (i, [i, i, i, p, i, ll, p, i, ll, i, i, p, p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -267,3 +276,15 @@ def ozaki2_probe_copy_peak(nbytes, reps):
     v = ctypes.c_double(0.0)
     _check("ozaki2_probe_copy_peak", load().ozaki2_probe_copy_peak(nbytes, reps, ctypes.byref(v)))
     return v.value
+
+
+def ozaki2_probe_crt(num_moduli, residues, shifts, n, words, rounded, stream=None):
+    return _check("ozaki2_probe_crt", load().ozaki2_probe_crt(
+        num_moduli, _ptr(residues), _ptr(shifts), n, _ptr(words), _ptr(rounded), _stream(stream)))
+
+
+def ozaki2_probe_batched_integers(m, n, k, A, lda, strideA, B, ldb, strideB, batch, num_moduli,
+                                  words, stream=None):
+    return _check("ozaki2_probe_batched_integers", load().ozaki2_probe_batched_integers(
+        m, n, k, _ptr(A), lda, strideA, _ptr(B), ldb, strideB, batch, num_moduli, _ptr(words),
+        _stream(stream)))

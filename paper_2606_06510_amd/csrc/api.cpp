@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "../../include/ozaki2.h"
+#include "../../include/ozaki2_probes.h"
 #include "oz2_internal.h"
 
 namespace {
@@ -223,6 +224,8 @@ Oz2Layout make_layout(const Oz2Dims& d, const Oz2Const& c) {
   L.Kmax = take((size_t)d.cslabs * d.np * 4);
   L.sA = take((size_t)d.mp * 4);
   L.tB = take((size_t)d.np * 4);
+  L.eA = take((size_t)d.mp * 4);
+  L.eB = take((size_t)d.np * 4);
   L.counters = take(64);
   L.listA = take((size_t)d.mp * 4);
   L.listB = take((size_t)d.np * 4);
@@ -240,7 +243,7 @@ Oz2Layout make_layout(const Oz2Dims& d, const Oz2Const& c) {
 }
 
 const unsigned kKnownFlags = OZ2_ACCUMULATE | OZ2_SCALE_FIXED | OZ2_QUANT_TZ | OZ2_NO_FALLBACK |
-                             OZ2_FORCE_FALLBACK;
+                             OZ2_FORCE_FALLBACK | OZ2_KEEP_RESIDUES | OZ2_TIME_STAGES;
 
 }  // namespace
 
@@ -306,6 +309,11 @@ int hip_status(hipError_t e) { return e == hipSuccess ? OZ2_OK : OZ2_E_DEVICE; }
 }  // namespace
 
 // ------------------------------------------------------------------ plans
+// Stage events of an OZ2_TIME_STAGES plan: 0 deconstruct start, 1 after scan +
+// codes, 2 after the max-magnitude GEMM, 3 after the split, 4 / 5 around the
+// residue GEMMs, 6 reconstruction start, 7 after it, 8 after the fallback.
+constexpr int kStageEvents = 9;
+
 struct ozaki2_plan_s {
   Oz2Dims d;
   Oz2Const c;
@@ -317,9 +325,20 @@ struct ozaki2_plan_s {
   int stage = 0;      // 0 created, 1 deconstructed, 2 residues ready, 3 reconstructed
   int sides = 0;      // operands whose planes are in the workspace (OZ2_SIDE_A | OZ2_SIDE_B)
   bool tables = false;   // residue -> plane-byte tables built in the workspace (they depend on r only)
+  hipEvent_t ev[kStageEvents] = {};
+  bool timed = false;    // OZ2_TIME_STAGES: ev[] exist
+  unsigned recorded = 0; // events recorded since the last deconstruct (bit i: ev[i])
 };
 
 namespace {
+
+// records stage event i of a timed plan on stream s (no-op otherwise)
+hipError_t mark(ozaki2_plan_s& p, int i, hipStream_t s) {
+  if (!p.timed) return hipSuccess;
+  const hipError_t e = hipEventRecord(p.ev[i], s);
+  if (e == hipSuccess) p.recorded |= 1u << i;
+  return e;
+}
 
 // Phase 1 for the operands in `side` (OZ2_SIDE_A, OZ2_SIDE_B or both).  One
 // operand alone only under OZ2_SCALE_FIXED, where its scales do not depend on
@@ -330,27 +349,35 @@ int run_deconstruct(ozaki2_plan_s& p, int side, hipStream_t s) {
   // both operands are split in one launch, B's tiles first, so that the
   // second read finds B (read last) still in the 256 MiB memory-side cache.
   const bool codes = !(d.flags & OZ2_SCALE_FIXED);
-  hipError_t e = oz2_launch_init(d, p.L, p.ws, side, s);
+  p.recorded = 0;
+  hipError_t e = mark(p, 0, s);
+  if (e == hipSuccess) e = oz2_launch_init(d, p.L, p.ws, side, s);
   for (int one : {OZ2_SIDE_A, OZ2_SIDE_B}) {
     if (!(side & one) || e != hipSuccess) continue;
     e = codes ? oz2_launch_scan_codes(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, one, s)
               : oz2_launch_scan(d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, one, s);
   }
   if (codes && e == hipSuccess) e = oz2_launch_rebase(d, p.L, p.ws, side, s);
+  if (e == hipSuccess) e = mark(p, 1, s);
   if (codes && e == hipSuccess) e = oz2_launch_codegemm(d, p.L, p.ws, s);
+  if (e == hipSuccess) e = mark(p, 2, s);
   if (e == hipSuccess) e = oz2_launch_scales(d, p.L, p.c, p.ws, side, s);
   if (e == hipSuccess && !p.tables) {
     e = oz2_launch_tables(p.L, p.c, p.ws, s);
     p.tables = e == hipSuccess;
   }
   if (e == hipSuccess) e = oz2_launch_split(d, p.L, p.c, p.ws, p.A, p.lda, p.B, p.ldb, side, s);
+  if (e == hipSuccess) e = mark(p, 3, s);
   return hip_status(e);
 }
 
 int run_reconstruct(ozaki2_plan_s& p, double* C, int ldc, hipStream_t s) {
-  hipError_t e = oz2_launch_reconstruct(p.d, p.L, p.c, p.ws, p.A, p.lda, C, ldc, s);
+  hipError_t e = mark(p, 6, s);
+  if (e == hipSuccess) e = oz2_launch_reconstruct(p.d, p.L, p.c, p.ws, p.A, p.lda, C, ldc, s);
+  if (e == hipSuccess) e = mark(p, 7, s);
   if (e == hipSuccess && !(p.d.flags & OZ2_NO_FALLBACK))
     e = oz2_launch_fallback(p.d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, C, ldc, s);
+  if (e == hipSuccess) e = mark(p, 8, s);
   return hip_status(e);
 }
 
@@ -441,12 +468,24 @@ int ozaki2_plan_create(ozaki2_plan_t* out, int m, int n, int k, int num_moduli, 
     delete p;
     return st;
   }
+  if (flags & OZ2_TIME_STAGES) {
+    for (int i = 0; i < kStageEvents; ++i) {
+      if (hipEventCreate(&p->ev[i]) != hipSuccess) {
+        for (int j = 0; j < i; ++j) (void)hipEventDestroy(p->ev[j]);
+        delete p;
+        return OZ2_E_DEVICE;
+      }
+    }
+    p->timed = true;
+  }
   p->ws = (uint8_t*)workspace;
   *out = p;
   return OZ2_OK;
 }
 
 int ozaki2_plan_destroy(ozaki2_plan_t plan) {
+  if (plan && plan->timed)
+    for (int i = 0; i < kStageEvents; ++i) (void)hipEventDestroy(plan->ev[i]);
   delete plan;
   return OZ2_OK;
 }
@@ -495,7 +534,11 @@ int ozaki2_deconstruct_b(ozaki2_plan_t p, const double* B, int ldb, void* stream
 
 int ozaki2_residue_gemm(ozaki2_plan_t p, void* stream) {
   if (!p || p->stage < 1) return OZ2_E_INVALID;
-  int st = hip_status(oz2_launch_resgemm(p->d, p->L, p->c, p->ws, (hipStream_t)stream));
+  const hipStream_t s = (hipStream_t)stream;
+  hipError_t e = mark(*p, 4, s);
+  if (e == hipSuccess) e = oz2_launch_resgemm(p->d, p->L, p->c, p->ws, s);
+  if (e == hipSuccess) e = mark(*p, 5, s);
+  int st = hip_status(e);
   if (st == OZ2_OK) p->stage = 2;
   return st;
 }
@@ -512,7 +555,7 @@ int ozaki2_reconstruct(ozaki2_plan_t p, double* C, int ldc, void* stream) {
 int ozaki2_dgemm_ex(int m, int n, int k, const double* A, int lda, const double* B, int ldb,
                     double* C, int ldc, int num_moduli, unsigned flags, void* workspace,
                     size_t ws_bytes, void* stream) {
-  if (flags & ~kKnownFlags) return OZ2_E_INVALID;
+  if ((flags & ~kKnownFlags) || (flags & OZ2_TIME_STAGES)) return OZ2_E_INVALID;
   if (num_moduli < 8 || num_moduli > OZ2_MAXR) return OZ2_E_INVALID;
   int st = check_mats(m, n, k, A, lda, B, ldb, C, ldc);
   if (st != OZ2_OK) return st;
@@ -582,7 +625,7 @@ int ozaki2_dgemm_strided_batched(int m, int n, int k, const double* A, int lda, 
     hipError_t e = oz2_launch_tables(L, c, (uint8_t*)ws, s);
     if (e == hipSuccess)
       e = oz2_launch_batched(c, m, n, k, batch, A, lda, strideA, B, ldb, strideB, C, ldc, strideC,
-                             (const uint32_t*)ws, s);
+                             (const uint32_t*)ws, nullptr, s);
     return e == hipSuccess ? OZ2_OK : OZ2_E_DEVICE;
   }
   size_t need = ozaki2_workspace_bytes(m, n, k, num_moduli, 0);
@@ -632,6 +675,7 @@ size_t ozaki2_plan_query_bytes(ozaki2_plan_t p, int what) {
     case OZ2_Q_RESIDUES: return (size_t)p->c.r * m * n * 2;
     case OZ2_Q_INTEGERS: return m * n * OZ2_NLIMB * 4;
     case OZ2_Q_FALLBACK_COUNT: return 8;
+    case OZ2_Q_STAGE_TIMES: return 6 * sizeof(float);
     default: return 0;
   }
 }
@@ -651,23 +695,10 @@ int ozaki2_plan_query(ozaki2_plan_t p, int what, void* host_out, size_t bytes) {
     return hipMemcpy(dst, src, b, hipMemcpyDeviceToHost) == hipSuccess;
   };
   switch (what) {
-    case OZ2_Q_EXPONENTS: {
-      std::vector<uint64_t> rb(d.m), cb(d.n);
-      if (!cp(rb.data(), ws + L.rowbits, d.m * 8) || !cp(cb.data(), ws + L.colbits, d.n * 8))
+    case OZ2_Q_EXPONENTS:
+      if (!cp(out, ws + L.eA, (size_t)d.m * 4) || !cp(out + (size_t)d.m * 4, ws + L.eB, (size_t)d.n * 4))
         return OZ2_E_DEVICE;
-      int32_t* o = (int32_t*)out;
-      auto ex = [](uint64_t b) -> int32_t {
-        if (b == 0 || b >= 0x7FF0000000000000ull) return 0;
-        double x;
-        std::memcpy(&x, &b, 8);
-        int e;
-        std::frexp(x, &e);
-        return e;
-      };
-      for (int i = 0; i < d.m; ++i) o[i] = ex(rb[i]);
-      for (int j = 0; j < d.n; ++j) o[d.m + j] = ex(cb[j]);
       return OZ2_OK;
-    }
     case OZ2_Q_MAXIMA: {
       std::vector<uint32_t> R((size_t)d.cslabs * d.mp), K((size_t)d.cslabs * d.np);
       if (!cp(R.data(), ws + L.Rmax, R.size() * 4) || !cp(K.data(), ws + L.Kmax, K.size() * 4))
@@ -733,15 +764,9 @@ int ozaki2_plan_query(ozaki2_plan_t p, int what, void* host_out, size_t bytes) {
           if (col >= d.n) continue;
           for (int e = 0; e < 16; ++e) {
             const int rr = row + 8 * (e >> 2) + (e & 3);
-            if (rr < d.m) {
-              // the workspace holds a representative of magnitude <= m/2 + 32;
-              // the query returns the centred residue in [-floor(m/2), ceil(m/2) - 1]
-              const int mi = p->c.m[i];
-              int v = raw[(size_t)i * plane + tile * (OZ2_TILE * OZ2_TILE) + (size_t)q * 16 + e];
-              v = ((v % mi) + mi) % mi;
-              if (v >= (mi + 1) / 2) v -= mi;
-              o[((size_t)i * d.n + col) * d.m + rr] = (int16_t)v;
-            }
+            if (rr < d.m)   // the stored representative itself (|x| <= m_i/2 + 32)
+              o[((size_t)i * d.n + col) * d.m + rr] =
+                  raw[(size_t)i * plane + tile * (OZ2_TILE * OZ2_TILE) + (size_t)q * 16 + e];
           }
         }
       return OZ2_OK;
@@ -757,9 +782,58 @@ int ozaki2_plan_query(ozaki2_plan_t p, int what, void* host_out, size_t bytes) {
     }
     case OZ2_Q_FALLBACK_COUNT:
       return cp(out, ws + L.counters, 8) ? OZ2_OK : OZ2_E_DEVICE;
+    case OZ2_Q_STAGE_TIMES: {
+      if (!p->timed || p->recorded != (1u << kStageEvents) - 1u) return OZ2_E_INVALID;
+      float* o = (float*)out;
+      const int from[6] = {0, 1, 2, 4, 6, 7}, to[6] = {1, 2, 3, 5, 7, 8};
+      for (int i = 0; i < 6; ++i)
+        if (hipEventElapsedTime(&o[i], p->ev[from[i]], p->ev[to[i]]) != hipSuccess)
+          return OZ2_E_DEVICE;
+      return OZ2_OK;
+    }
     default:
       return OZ2_E_INVALID;
   }
+}
+
+// ---------------------------------------------------------------- probes
+// (include/ozaki2_probes.h; these two need the plan constants, the rest
+// are in probes.hip)
+int ozaki2_probe_crt(int num_moduli, const short* residues, const int* shifts, int n,
+                     unsigned* words, double* rounded, void* stream) {
+  Oz2Const c;
+  if (n < 0 || !make_const(num_moduli, c)) return OZ2_E_INVALID;
+  if (n > 0 && (!residues || !shifts || !words || !rounded)) return OZ2_E_INVALID;
+  const int st = device_ok();
+  if (st != OZ2_OK) return st;
+  return hip_status(oz2_launch_crt_probe(c, (const int16_t*)residues, shifts, n, (uint32_t*)words,
+                                         rounded, (hipStream_t)stream));
+}
+
+int ozaki2_probe_batched_integers(int m, int n, int k, const double* A, int lda,
+                                  long long strideA, const double* B, int ldb, long long strideB,
+                                  int batch, int num_moduli, unsigned* words, void* stream) {
+  Oz2Const c;
+  if (m < 1 || n < 1 || k < 1 || m > 64 || n > 64 || k > 64 || batch < 0) return OZ2_E_INVALID;
+  if (lda < m || ldb < k || strideA < 0 || strideB < 0 || !make_const(num_moduli, c))
+    return OZ2_E_INVALID;
+  if (batch == 0) return OZ2_OK;
+  if (!A || !B || !words) return OZ2_E_INVALID;
+  int st = device_ok();
+  if (st != OZ2_OK) return st;
+  std::lock_guard<std::mutex> g(g_pool_mu);
+  void* ws = nullptr;
+  st = pool_get(align256((size_t)c.tabsz * 4), &ws);
+  if (st != OZ2_OK) return st;
+  Oz2Layout L{};
+  L.tabs = 0;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = oz2_launch_tables(L, c, (uint8_t*)ws, s);
+  // C is not written on this path (the kernel writes the integers instead)
+  if (e == hipSuccess)
+    e = oz2_launch_batched(c, m, n, k, batch, A, lda, strideA, B, ldb, strideB, nullptr, m, 0,
+                           (const uint32_t*)ws, (uint32_t*)words, s);
+  return hip_status(e);
 }
 
 }  // extern "C"

@@ -210,19 +210,37 @@ __device__ __forceinline__ void crt_add(const Oz2Const& c, int i, const v4f (&ac
 // column cb0 + 16 (I/4) + lane%16) from their CRT sums: reduction by the
 // quotient estimate, one rounding with the exponent shift; flagged rows and
 // columns recomputed in native FP64; only outputs inside m x n stored.
+// With iout (a diagnostic probe) the exact integers of the unflagged outputs
+// are written there instead, 5 words each at [col][row] of the problem's
+// m x n block, and C is not touched.
 __device__ __forceinline__ void emit38(const Oz2Const& c, const double (&S0)[8],
                                        const double (&S1)[8], const double (&S2)[8],
                                        const Smem& S, int rb0, int cb0, int m, int n, int k,
                                        const double* __restrict__ A, int lda,
-                                       const double* __restrict__ B, int ldb, double* C, int ldc) {
+                                       const double* __restrict__ B, int ldb, double* C, int ldc,
+                                       uint32_t* iout) {
   const int lane = threadIdx.x & 63;
   const int r0 = rb0 + 4 * (lane >> 4), c0 = cb0 + (lane & 15);
 #pragma unroll
   for (int I = 0; I < 8; ++I) {
     const int row = r0 + (I & 3), col = c0 + 16 * (I >> 2);
     if (row < m && col < n) {
+      const bool flagged = ((S.fA[row] | S.fB[col]) & (OZ2_T1 | OZ2_T2)) != 0;
+      if (iout) {
+        if (!flagged) {
+          double s0 = S0[I], s1 = S1[I], s2 = S2[I];
+          if (crt38_reduce(c, s0, s1, s2)) crt38_fix(c, s0, s1, s2);
+          uint32_t w[4];
+          limbs38_words(s0, s1, s2, w);
+          uint32_t* o = iout + ((size_t)col * m + row) * NL;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) o[q] = w[q];
+          o[4] = (uint32_t)((int32_t)w[3] >> 31);
+        }
+        continue;
+      }
       double v;
-      if ((S.fA[row] | S.fB[col]) & (OZ2_T1 | OZ2_T2)) {
+      if (flagged) {
         double sacc = 0.0;   // native FP64, one FMA per k in ascending k
         for (int l = 0; l < k; ++l) sacc = fma(A[row + (size_t)l * lda], B[l + (size_t)col * ldb], sacc);
         v = sacc;
@@ -250,39 +268,52 @@ struct Emit {
                                              const Smem& S, int rb0, int cb0, int m, int n, int k,
                                              const double* __restrict__ A, int lda,
                                              const double* __restrict__ B, int ldb, double* C,
-                                             int ldc) {
+                                             int ldc, uint32_t* iout) {
     constexpr int NW = NWords<R>::value;
     const int lane = threadIdx.x & 63;
     const int row = rb0 + 4 * (lane >> 4) + (I & 3);
     const int col = cb0 + 16 * (I >> 2) + (lane & 15);
     if (row < m && col < n) {
-      double v;
-      if ((S.fA[row] | S.fB[col]) & (OZ2_T1 | OZ2_T2)) {
-        double sacc = 0.0;   // native FP64, one FMA per k in ascending k
-        for (int l = 0; l < k; ++l) sacc = fma(A[row + (size_t)l * lda], B[l + (size_t)col * ldb], sacc);
-        v = sacc;
+      const bool flagged = ((S.fA[row] | S.fB[col]) & (OZ2_T1 | OZ2_T2)) != 0;
+      if (iout) {
+        if (!flagged) {
+          uint32_t w[NW];
+          crt_words<R, NW, I>(c, x, w);
+          uint32_t* o = iout + ((size_t)col * m + row) * NL;
+#pragma unroll
+          for (int q = 0; q < NL; ++q) o[q] = q < NW ? w[q < NW ? q : 0] : (uint32_t)((int32_t)w[NW - 1] >> 31);
+        }
       } else {
-        uint32_t w[NW];
-        crt_words<R, NW, I>(c, x, w);
-        v = round_scaled<NW>(w, S.sS[row] + S.sT[col]);
+        double v;
+        if (flagged) {
+          double sacc = 0.0;   // native FP64, one FMA per k in ascending k
+          for (int l = 0; l < k; ++l) sacc = fma(A[row + (size_t)l * lda], B[l + (size_t)col * ldb], sacc);
+          v = sacc;
+        } else {
+          uint32_t w[NW];
+          crt_words<R, NW, I>(c, x, w);
+          v = round_scaled<NW>(w, S.sS[row] + S.sT[col]);
+        }
+        C[row + (size_t)col * ldc] = v;
       }
-      C[row + (size_t)col * ldc] = v;
     }
-    Emit<R, I + 1>::run(c, x, S, rb0, cb0, m, n, k, A, lda, B, ldb, C, ldc);
+    Emit<R, I + 1>::run(c, x, S, rb0, cb0, m, n, k, A, lda, B, ldb, C, ldc, iout);
   }
 };
 template <int R>
 struct Emit<R, 8> {
   __device__ __forceinline__ static void run(const Oz2Const&, const uint4 (&)[R], const Smem&, int,
                                              int, int, int, int, const double*, int, const double*,
-                                             int, double*, int) {}
+                                             int, double*, int, uint32_t*) {}
 };
 
-template <int R>
+// INT (a diagnostic instantiation): write the exact integers to iout instead
+// of C; the product path runs INT = false, where iout is not used at all.
+template <int R, bool INT>
 __global__ void __launch_bounds__(NTB)
 k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__ A, int lda,
           long long strideA, const double* __restrict__ B, int ldb, long long strideB, double* C,
-          int ldc, long long strideC, const uint32_t* __restrict__ gtab) {
+          int ldc, long long strideC, const uint32_t* __restrict__ gtab, uint32_t* iout) {
   extern __shared__ uint32_t tab[];
   __shared__ __attribute__((aligned(16))) Smem S;
   for (int i = threadIdx.x; i < c.tabsz; i += blockDim.x) tab[i] = gtab[i];
@@ -293,6 +324,7 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
     const double* Ab = A + (size_t)b * strideA;
     const double* Bb = B + (size_t)b * strideB;
     double* Cb = C + (size_t)b * strideC;
+    uint32_t* Ib = INT ? iout + (size_t)b * m * n * NL : nullptr;
     __syncthreads();   // the previous problem (and the table copy) are done with S
     // scan: row maxima of |A|, column maxima of |B| (bit patterns), T1
     double xa[8], xb[8];
@@ -396,7 +428,7 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
       if (t2a && row < m) atomicOr(&S.fA[row], OZ2_T2);
       if (t2b && row < n) atomicOr(&S.fB[row], OZ2_T2);
       __syncthreads();
-      emit38(c, S0, S1, S2, S, rb0, cb0, m, n, k, Ab, lda, Bb, ldb, Cb, ldc);
+      emit38(c, S0, S1, S2, S, rb0, cb0, m, n, k, Ab, lda, Bb, ldb, Cb, ldc, Ib);
     } else {
       // residues of every modulus: one uint4 (8 int16 outputs) per modulus
       uint4 res[R];
@@ -411,7 +443,7 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
       if (t2a && row < m) atomicOr(&S.fA[row], OZ2_T2);
       if (t2b && row < n) atomicOr(&S.fB[row], OZ2_T2);
       __syncthreads();
-      Emit<R, 0>::run(c, res, S, rb0, cb0, m, n, k, Ab, lda, Bb, ldb, Cb, ldc);
+      Emit<R, 0>::run(c, res, S, rb0, cb0, m, n, k, Ab, lda, Bb, ldb, Cb, ldc, Ib);
     }
   }
 }
@@ -419,18 +451,19 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
 template <int R>
 hipError_t launch_r(const Oz2Const& c, int m, int n, int k, int batch, const double* A, int lda,
                     long long sA, const double* B, int ldb, long long sB, double* C, int ldc,
-                    long long sC, const uint32_t* tab, hipStream_t s) {
+                    long long sC, const uint32_t* tab, uint32_t* iout, hipStream_t s) {
   const size_t lds = (size_t)c.tabsz * 4;
   const int cus = oz2_device_cus();
-  (void)hipFuncSetAttribute((const void*)k_batched<R>, hipFuncAttributeMaxDynamicSharedMemorySize,
+  auto kern = iout ? k_batched<R, true> : k_batched<R, false>;
+  (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)lds);
   int per = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, k_batched<R>, NTB, lds) != hipSuccess ||
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kern, NTB, lds) != hipSuccess ||
       per < 1)
     per = 1;
   const int grid = min(batch, per * cus);
-  hipLaunchKernelGGL(k_batched<R>, dim3(grid), dim3(NTB), lds, s, c, m, n, k, batch, A, lda, sA,
-                     B, ldb, sB, C, ldc, sC, tab);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(NTB), lds, s, c, m, n, k, batch, A, lda, sA,
+                     B, ldb, sB, C, ldc, sC, tab, iout);
   return hipGetLastError();
 }
 
@@ -439,17 +472,17 @@ hipError_t launch_r(const Oz2Const& c, int m, int n, int k, int batch, const dou
 hipError_t oz2_launch_batched(const Oz2Const& c, int m, int n, int k, int batch, const double* A,
                               int lda, long long sA, const double* B, int ldb, long long sB,
                               double* C, int ldc, long long sC, const uint32_t* tab,
-                              hipStream_t s) {
+                              uint32_t* iout, hipStream_t s) {
   switch (c.r) {
-    case 8: return launch_r<8>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, s);
-    case 9: return launch_r<9>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, s);
-    case 10: return launch_r<10>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, s);
-    case 11: return launch_r<11>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, s);
-    case 12: return launch_r<12>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, s);
-    case 13: return launch_r<13>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, s);
-    case 14: return launch_r<14>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, s);
-    case 15: return launch_r<15>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, s);
-    case 16: return launch_r<16>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, s);
+    case 8: return launch_r<8>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, iout, s);
+    case 9: return launch_r<9>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, iout, s);
+    case 10: return launch_r<10>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, iout, s);
+    case 11: return launch_r<11>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, iout, s);
+    case 12: return launch_r<12>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, iout, s);
+    case 13: return launch_r<13>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, iout, s);
+    case 14: return launch_r<14>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, iout, s);
+    case 15: return launch_r<15>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, iout, s);
+    case 16: return launch_r<16>(c, m, n, k, batch, A, lda, sA, B, ldb, sB, C, ldc, sC, tab, iout, s);
     default: return hipErrorInvalidValue;
   }
 }

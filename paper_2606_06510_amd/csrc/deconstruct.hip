@@ -413,8 +413,9 @@ __global__ void __launch_bounds__(256) k_rebase(uint8_t* codesA, const int16_t* 
 __global__ void k_scales(Oz2Dims d, const unsigned long long* __restrict__ rowbits,
                          const unsigned long long* __restrict__ colbits,
                          const uint32_t* __restrict__ Rmax, const uint32_t* __restrict__ Kmax,
-                         int32_t* sA, int32_t* tB, uint32_t* fA, uint32_t* fB, int cA, int cB,
-                         int* counters, int* listA, int* listB, int side) {
+                         int32_t* sA, int32_t* tB, int32_t* eA, int32_t* eB, uint32_t* fA,
+                         uint32_t* fB, int cA, int cB, int* counters, int* listA, int* listB,
+                         int side) {
   int idx = blockIdx.x * blockDim.x + threadIdx.x;
   bool fixed = (d.flags & 2u) != 0;   // OZ2_SCALE_FIXED
   const bool force = (d.flags & 16u) != 0;   // OZ2_FORCE_FALLBACK: every row of A natively
@@ -423,13 +424,13 @@ __global__ void k_scales(Oz2Dims d, const unsigned long long* __restrict__ rowbi
     if (!(side & OZ2_SIDE_A)) return;
     int i = idx;
     unsigned long long b = rowbits[i];
-    int s = 0;
+    int s = 0, E = 0;
     uint32_t f = 0;
     if (i < d.m) {
       if (b >= kInfBits) {
         f = OZ2_T1;
       } else {
-        int E = b ? exp_of_bits(b) : 0;
+        E = b ? exp_of_bits(b) : 0;
         unsigned long long R = fixedR;
         if (!fixed) {
           R = 0;
@@ -439,19 +440,20 @@ __global__ void k_scales(Oz2Dims d, const unsigned long long* __restrict__ rowbi
       }
     }
     sA[i] = s;
+    eA[i] = E;
     fA[i] = f;
     if (i < d.m && (force || f)) listA[atomicAdd(counters + 0, 1)] = i;
   } else if (idx < d.mp + d.np) {
     if (!(side & OZ2_SIDE_B)) return;
     int j = idx - d.mp;
     unsigned long long b = colbits[j];
-    int t = 0;
+    int t = 0, E = 0;
     uint32_t f = 0;
     if (j < d.n) {
       if (b >= kInfBits) {
         f = OZ2_T1;
       } else {
-        int E = b ? exp_of_bits(b) : 0;
+        E = b ? exp_of_bits(b) : 0;
         unsigned long long K = fixedR;
         if (!fixed) {
           K = 0;
@@ -461,6 +463,7 @@ __global__ void k_scales(Oz2Dims d, const unsigned long long* __restrict__ rowbi
       }
     }
     tB[j] = t;
+    eB[j] = E;
     fB[j] = f;
     if (j < d.n && !force && f) listB[atomicAdd(counters + 1, 1)] = j;
   }
@@ -665,7 +668,7 @@ hipError_t oz2_launch_scales(const Oz2Dims& d, const Oz2Layout& L, const Oz2Cons
                      (const unsigned long long*)(ws + L.rowbits),
                      (const unsigned long long*)(ws + L.colbits), (const uint32_t*)(ws + L.Rmax),
                      (const uint32_t*)(ws + L.Kmax), (int32_t*)(ws + L.sA), (int32_t*)(ws + L.tB),
-                     (uint32_t*)(ws + L.flagsA), (uint32_t*)(ws + L.flagsB), c.cA, c.cB,
+                     (int32_t*)(ws + L.eA), (int32_t*)(ws + L.eB), (uint32_t*)(ws + L.flagsA), (uint32_t*)(ws + L.flagsB), c.cA, c.cB,
                      (int*)(ws + L.counters), (int*)(ws + L.listA), (int*)(ws + L.listB), side);
   return hipGetLastError();
 }

@@ -240,6 +240,19 @@ __device__ __forceinline__ void normalise38(double& S0, double& S1, double& S2) 
   S2 += cy;
 }
 
+// The normalised limbs (S0, S1 in [0, 2^38), S2 signed, |S2| < 2^37) as four
+// 32-bit words of two's complement, little endian: X = b1 2^64 + b0 with
+// b0 = S0 + (S1 mod 2^26) 2^38 and b1 = S2 2^12 + floor(S1 / 2^26).
+__device__ __forceinline__ void limbs38_words(double S0, double S1, double S2, uint32_t (&w)[4]) {
+  const unsigned long long u0 = (unsigned long long)S0, u1 = (unsigned long long)S1;
+  const unsigned long long b0 = u0 | (u1 << 38);
+  const long long b1 = (long long)S2 * 4096 + (long long)(u1 >> 26);
+  w[0] = (uint32_t)b0;
+  w[1] = (uint32_t)(b0 >> 32);
+  w[2] = (uint32_t)b1;
+  w[3] = (uint32_t)((unsigned long long)b1 >> 32);
+}
+
 // RN-even binary64 value of X 2^-e from normalised limbs.  If S2 is in
 // [-2^15, 2^15), H = S2 2^38 + S1 is exact (|H| <= 2^53) and one fma rounds
 // H 2^38 + S0 once.  Otherwise |S2 2^38 + S1| >= 2^53, where binary64
@@ -261,12 +274,9 @@ __device__ __forceinline__ double round38(double S0, double S1, double S2, int e
   if (v == 0.0) return 0.0;        // exact zero is +0.0
   const int ev = (int)((__double_as_longlong(v) >> 52) & 0x7ff) - 1023;   // |v| >= 1
   if (ev + sh - e < -1022) {
-    // subnormal result: X as four 32-bit words, X = b1 2^64 + b0
-    const unsigned long long u0 = (unsigned long long)S0, u1 = (unsigned long long)S1;
-    const unsigned long long b0 = u0 | (u1 << 38);
-    const long long b1 = (long long)S2 * 4096 + (long long)(u1 >> 26);
-    const uint32_t w[4] = {(uint32_t)b0, (uint32_t)(b0 >> 32), (uint32_t)b1,
-                           (uint32_t)((unsigned long long)b1 >> 32)};
+    // subnormal result: X as four 32-bit words
+    uint32_t w[4];
+    limbs38_words(S0, S1, S2, w);
     return round_scaled<4>(w, e);
   }
   return ldexp(v, sh - e);
@@ -307,10 +317,18 @@ __device__ __forceinline__ void crt38_fix(const Oz2Const& c, double& S0, double&
 // exponent shift -e: the direct CRT sum in radix-2^38 limbs, the reduction by
 // the quotient estimate (with the exact range check where it is ambiguous),
 // then round38.
+// The exact integer C~ of output I of a thread (R <= 12 residues, |x_i| <= 577)
+// as normalised radix-2^38 limbs: the direct CRT sum, the reduction by the
+// quotient estimate, and the exact range check where the estimate is
+// ambiguous.  (The reconstruction rounds these limbs; the integer query of
+// the staged API exports them.)
 template <int R, int I>
-__device__ __forceinline__ double crt38_rounded(const Oz2Const& c, const uint4 (&x)[R], int e) {
+__device__ __forceinline__ void crt38_limbs(const Oz2Const& c, const uint4 (&x)[R], double& S0,
+                                            double& S1, double& S2) {
   static_assert(R <= 12, "three radix-2^38 limbs hold [-M/2, M/2) only for r <= 12");
-  double S0 = 0.0, S1 = 0.0, S2 = 0.0;
+  S0 = 0.0;
+  S1 = 0.0;
+  S2 = 0.0;
 #pragma unroll
   for (int i = 0; i < R; ++i) {
     const double xi = res_at<I>(x[i]);
@@ -319,6 +337,12 @@ __device__ __forceinline__ double crt38_rounded(const Oz2Const& c, const uint4 (
     S2 = fma(xi, c.W38[i][2], S2);
   }
   if (crt38_reduce(c, S0, S1, S2)) crt38_fix(c, S0, S1, S2);
+}
+
+template <int R, int I>
+__device__ __forceinline__ double crt38_rounded(const Oz2Const& c, const uint4 (&x)[R], int e) {
+  double S0, S1, S2;
+  crt38_limbs<R, I>(c, x, S0, S1, S2);
   return round38(S0, S1, S2, e);
 }
 

@@ -66,6 +66,7 @@ struct Oz2Layout {
   size_t flagsA, flagsB;      // uint32 [mp] / [np]
   size_t Rmax, Kmax;          // uint32 [cslabs][mp] / [cslabs][np]
   size_t sA, tB;              // int32 [mp] / [np]
+  size_t eA, eB;              // int32 [mp] / [np]: frexp exponents of the row / column maxima
   size_t codesA, codesB;      // uint8 [kp/64][mp][64] / [kp/64][np][64] (K-blocked)
   size_t etA, etB;            // int16 [kp/64][mp] / [kp/64][np]: exponents of the tile-row maxima
   size_t planesA, planesB;    // uint8 [P][kp/64][mp][64] / [P][kp/64][np][64] (K-blocked)
@@ -118,12 +119,19 @@ hipError_t oz2_launch_fallback(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws
                                double* C, int ldc, hipStream_t s);
 hipError_t oz2_launch_integers(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
                                uint8_t* ws, uint32_t* out, hipStream_t s);
+// the reconstruction's integer and rounding routines on n given residue
+// vectors (res: int16 [r][n], e: int [n] shifts; words: uint32 [n][5],
+// rounded: double [n])
+hipError_t oz2_launch_crt_probe(const Oz2Const& c, const int16_t* res, const int* e, int n,
+                                uint32_t* words, double* rounded, hipStream_t s);
 hipError_t oz2_launch_fill(double* C, int m, int n, int ldc, hipStream_t s);
 // all of Alg. 1 for `batch` problems of m, n, k <= 64 in one launch; tab = the
-// residue -> plane-byte tables (oz2_launch_tables)
+// residue -> plane-byte tables (oz2_launch_tables); iout (normally null, a
+// diagnostic): write the exact integers of the unflagged outputs there,
+// uint32 [batch][n][m][5], instead of C
 hipError_t oz2_launch_batched(const Oz2Const& c, int m, int n, int k, int batch, const double* A,
                               int lda, long long sA, const double* B, int ldb, long long sB,
-                              double* C, int ldc, long long sC, const uint32_t* tab,
+                              double* C, int ldc, long long sC, const uint32_t* tab, uint32_t* iout,
                               hipStream_t s);
 
 // ---------------------------------------------------------------- digit rule

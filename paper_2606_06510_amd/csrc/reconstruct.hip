@@ -1,8 +1,8 @@
 // Phase 3 of Alg. 1 on gfx950: CRT reconstruction of the exact integer,
-// removal of the power-of-two scaling with ONE rounding (the paper's "one
-// rounded conversion" of the multi-limb integer), and the native-FP64
-// fallback for flagged rows of A / columns of B (Alg. 1, "fall back to
-// native FP64 on the offending rows"; the numerical contract's item (vi)).
+// removal of the power-of-two scaling with ONE rounding of the multi-limb
+// integer (App. B), and the native-FP64 fallback for flagged rows of A /
+// columns of B (Alg. 1, fallback step: rows the scaling cannot certify are
+// recomputed in plain FP64; the numerical contract's item (vi)).
 //
 // Reconstruction.  The integer C~ in [-M/2, M/2) is unique given its r
 // residues (Eq. (M-bound)), so any exact CRT algorithm yields the same bits
@@ -143,6 +143,38 @@ k_reconstruct(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res,
   }
 }
 
+// The exact integer of output I of a thread as NL 32-bit words (two's
+// complement, little endian), formed by the routine the reconstruction
+// itself uses: radix-2^38 limbs for R <= 12, 32-bit words above.
+template <int R, int I>
+__device__ __forceinline__ void store_integer(const Oz2Const& c, const uint4 (&x)[R], uint32_t* o) {
+  constexpr int NW = R <= 12 ? 4 : NWords<R>::value;
+  uint32_t w[NW];
+  if constexpr (R <= 12) {
+    double S0, S1, S2;
+    crt38_limbs<R, I>(c, x, S0, S1, S2);
+    limbs38_words(S0, S1, S2, w);
+  } else {
+    crt_words<R, NW, I>(c, x, w);
+  }
+  const uint32_t ext = (uint32_t)((int32_t)w[NW - 1] >> 31);
+#pragma unroll
+  for (int q = 0; q < NL; ++q) o[q] = q < NW ? w[q < NW ? q : 0] : ext;
+}
+
+// The rounded value of output I exactly as the reconstruction forms it.
+template <int R, int I>
+__device__ __forceinline__ double rounded_value(const Oz2Const& c, const uint4 (&x)[R], int e) {
+  if constexpr (R <= 12) {
+    return crt38_rounded<R, I>(c, x, e);
+  } else {
+    constexpr int NW = NWords<R>::value;
+    uint32_t w[NW];
+    crt_words<R, NW, I>(c, x, w);
+    return round_scaled<NW>(w, e);
+  }
+}
+
 template <int R, int I>
 struct IntOut {
   __device__ __forceinline__ static void run(const Oz2Const& c, const Oz2Dims& d,
@@ -152,12 +184,8 @@ struct IntOut {
     const int row = b.row0 + b.rb + 8 * (I >> 2) + (I & 3);
     const int col = b.col0 + b.cl;
     if (row < d.m && col < d.n) {
-      uint32_t w[NW];
-      crt_words<R, NW, I>(c, x, w);
       uint32_t* o = out + ((size_t)col * d.m + row) * NL;
-      const uint32_t ext = (uint32_t)((int32_t)w[NW - 1] >> 31);
-#pragma unroll
-      for (int q = 0; q < NL; ++q) o[q] = q < NW ? w[q < NW ? q : 0] : ext;
+      store_integer<R, I>(c, x, o);
     }
     IntOut<R, I + 1>::run(c, d, x, b, out);
   }
@@ -176,6 +204,23 @@ k_integers(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res, uint32_t* out
   uint4 x[R];
   load_residues<R>(res, (size_t)d.mp * d.np, b.roff, x);
   IntOut<R, 0>::run(c, d, x, b, out);
+}
+
+// The reconstruction's integer and rounding routines on given residues (a
+// probe): thread t takes residue t of each modulus (res[i n + t], any
+// representative with |x| <= 577) and writes the exact integer as 5 words and
+// its value rounded with the shift e[t].
+template <int R>
+__global__ void __launch_bounds__(256)
+k_crt_probe(Oz2Const c, const int16_t* __restrict__ res, const int* __restrict__ e, int n,
+            uint32_t* __restrict__ words, double* __restrict__ rounded) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n) return;
+  uint4 x[R];
+#pragma unroll
+  for (int i = 0; i < R; ++i) x[i] = make_uint4((uint32_t)(uint16_t)res[(size_t)i * n + t], 0u, 0u, 0u);
+  store_integer<R, 0>(c, x, words + (size_t)t * NL);
+  rounded[t] = rounded_value<R, 0>(c, x, e[t]);
 }
 
 // Native FP64 for flagged entries.  Work = (flagged rows of A) x (all
@@ -326,6 +371,13 @@ void launch_integers_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, 
                      (const int16_t*)(ws + L.res), out);
 }
 
+template <int R>
+void launch_crt_probe_r(const Oz2Const& c, const int16_t* res, const int* e, int n,
+                        uint32_t* words, double* rounded, hipStream_t s) {
+  hipLaunchKernelGGL(k_crt_probe<R>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, c, res, e,
+                     n, words, rounded);
+}
+
 #define OZ2_R_SWITCH(FN, ...)                 \
   switch (c.r) {                              \
     case 8: FN<8>(__VA_ARGS__); break;        \
@@ -355,6 +407,13 @@ hipError_t oz2_launch_integers(const Oz2Dims& d, const Oz2Layout& L, const Oz2Co
   return hipGetLastError();
 }
 
+
+hipError_t oz2_launch_crt_probe(const Oz2Const& c, const int16_t* res, const int* e, int n,
+                                uint32_t* words, double* rounded, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  OZ2_R_SWITCH(launch_crt_probe_r, c, res, e, n, words, rounded, s)
+  return hipGetLastError();
+}
 
 hipError_t oz2_launch_fallback(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, const double* A,
                                int lda, const double* B, int ldb, double* C, int ldc,

@@ -1,6 +1,7 @@
 """Render rocprofv3 output into the short text summaries kept under profiles/.
 
     python -m paper_2606_06510_amd.rocprof_summary stats STATS_CSV OUT_MD TITLE COMMAND
+    python -m paper_2606_06510_amd.rocprof_summary trace TRACE_CSV OUT_MD TITLE COMMAND SKIP COUNT
     python -m paper_2606_06510_amd.rocprof_summary traffic FETCH_CSV WRITE_CSV OUT_TXT \\
         KERNEL COPY_BYTES SOURCE CMD_FETCH CMD_WRITE
     python -m paper_2606_06510_amd.rocprof_summary mfma COUNTER_CSV OUT_TXT SOURCE CMD
@@ -8,7 +9,11 @@
         COPY_BYTES M N K R PSTORE CMD_TRACE CMD_FETCH CMD_WRITE
 
 ``stats`` turns a ``--kernel-trace --stats`` kernel_stats.csv into a markdown
-table.  ``traffic`` reads two ``--pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE``
+table.  ``trace`` does the same from the per-dispatch kernel_trace.csv, keeping
+only dispatches SKIP .. SKIP+COUNT-1 of each kernel (in launch order): with
+SKIP = the bench's warm-up steps and COUNT = its timed steps, the averages
+cover the timed steps alone (kernels launched once per plan, not per step,
+drop out).  ``traffic`` reads two ``--pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE``
 counter_collection.csv files (KiB per dispatch), takes the mean per launch of
 KERNEL and of the plain copy kernel (COPY_BYTES read and written), and scales
 the kernel's figures by copy_bytes / copy_reading; the result carries the
@@ -47,6 +52,40 @@ def stats(src, dst, title, cmd):
             f.write(f"| {_short(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
                     f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
                     f"{float(r['Percentage']):.1f}% |\n")
+
+
+def trace(src, dst, title, cmd, skip, count):
+    by = collections.defaultdict(list)
+    for r in csv.DictReader(open(src)):
+        by[_short(r["Kernel_Name"])].append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    rows = []
+    for name, ds in by.items():
+        ds.sort()
+        sel = [(e - b) * 1e-3 for b, e in ds[skip:skip + count]]
+        if sel:
+            rows.append((name, len(sel), sum(sel) / len(sel), min(sel), max(sel), sum(sel)))
+    tot = sum(r[5] for r in rows) or 1.0
+    rows.sort(key=lambda r: -r[5])
+    with open(dst, "w") as f:
+        f.write(f"# {title}
+
+Command (from the repository root, on one MI355X):
+
+```
+{cmd}
+```
+
+")
+        f.write(f"Dispatches {skip} .. {skip + count - 1} of each kernel (launch order), i.e. the "
+                f"timed steps only; warm-up launches excluded.
+
+")
+        f.write("| kernel | calls | avg (us) | min (us) | max (us) | share |
+|---|---|---|---|---|---|
+")
+        for name, n, avg, lo, hi, t in rows:
+            f.write(f"| {name} | {n} | {avg:.1f} | {lo:.1f} | {hi:.1f} | {100 * t / tot:.1f}% |
+")
 
 
 def _per_launch(path, counter):
@@ -170,6 +209,8 @@ def hbm(stats_csv, fetch_csv, write_csv, dst, copy_bytes, m, n, k, r, pstore, cm
 def main(argv):
     if argv[0] == "stats":
         stats(*argv[1:5])
+    elif argv[0] == "trace":
+        trace(*argv[1:5], int(argv[5]), int(argv[6]))
     elif argv[0] == "traffic":
         traffic(argv[1], argv[2], argv[3], argv[4], int(argv[5]), argv[6], argv[7], argv[8])
     elif argv[0] == "mfma":

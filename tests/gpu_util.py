@@ -83,9 +83,14 @@ def compare_all(plan, C, A, B, r, res, check_integers=True):
             assert np.array_equal(PA[pi + t], expected_bytes(pa[t])), (mi, t, "A")
             assert np.array_equal(PB[pi + t], expected_bytes(pb[t])), (mi, t, "B")
         pi += len(pa)
-    Rg = plan.query(oz.OZ2_Q_RESIDUES)
-    assert np.array_equal(Rg, res.residues)
+    # the residue GEMMs leave a representative of each residue (not unique):
+    # congruent to the oracle's centred residue, of magnitude <= m/2 + 32
+    Rg = plan.query(oz.OZ2_Q_RESIDUES).astype(np.int64)
+    for t, mi in enumerate(res.ms):
+        assert np.all((Rg[t] - res.residues[t]) % mi == 0), ("residue", mi)
+        assert np.all(np.abs(Rg[t]) <= mi // 2 + 32), ("representative range", mi)
     if check_integers:
+        # the integers formed by the reconstruction's own routine (unique)
         X = plan.query(oz.OZ2_Q_INTEGERS)
         assert all(int(a) == int(b) for a, b in zip(X.ravel(), res.X.ravel()))
     compare_C(C, A, B, res)

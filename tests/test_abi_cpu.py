@@ -26,7 +26,7 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, n), n
     assert sorted(_lib.EXPORTS) == names
     probes = _declared("ozaki2_probes.h")
-    assert len(probes) == 6
+    assert len(probes) == 8
     for n in probes:
         assert hasattr(L, n), n
     assert sorted(_lib.PROBE_EXPORTS) == probes
@@ -47,6 +47,18 @@ def test_probe_argument_checks():
         oz.ozaki2_probe_mfma_digits(3)                # odd iteration count
     with pytest.raises(oz.Ozaki2Error):
         oz.ozaki2_probe_copy_peak(1 << 20, 1)         # below 16 MiB
+    with pytest.raises(oz.Ozaki2Error):
+        oz.ozaki2_probe_crt(12, FAKE, FAKE, -1, FAKE, FAKE, 0)     # n < 0
+    with pytest.raises(oz.Ozaki2Error):
+        oz.ozaki2_probe_crt(7, FAKE, FAKE, 4, FAKE, FAKE, 0)       # r outside [8, 16]
+    with pytest.raises(oz.Ozaki2Error):
+        oz.ozaki2_probe_crt(12, FAKE, None, 4, FAKE, FAKE, 0)      # null pointer
+    for bad in [dict(m=65), dict(k=0), dict(lda=3), dict(batch=-1), dict(r=17), dict(W=None)]:
+        a = dict(m=4, n=4, k=4, lda=4, ldb=4, batch=2, r=12, W=FAKE)
+        a.update(bad)
+        with pytest.raises(oz.Ozaki2Error):
+            oz.ozaki2_probe_batched_integers(a["m"], a["n"], a["k"], FAKE, a["lda"], 16, FAKE,
+                                             a["ldb"], 16, a["batch"], a["r"], a["W"], 0)
 
 
 def test_status_strings():
@@ -110,6 +122,17 @@ def test_zero_sized_output_is_a_noop():
     L = oz.load()
     assert L.ozaki2_dgemm_ex(0, 5, 6, None, 1, None, 6, None, 1, 12, 0, None, 0, None) == 0
     assert L.ozaki2_dgemm(4, 0, 6, None, 4, None, 6, None, 4, 12, None) == 0
+
+
+def test_stage_timing_flag_is_for_plans_only():
+    L = oz.load()
+    st = L.ozaki2_dgemm_ex(4, 5, 6, FAKE, 4, FAKE + (1 << 20), 6, FAKE + (2 << 20), 4, 12,
+                           oz.OZ2_TIME_STAGES, FAKE + (3 << 20), 1 << 30, None)
+    assert st == _lib.OZ2_E_INVALID
+    # a known flag (KEEP_RESIDUES) leaves the workspace size as it is: the
+    # staged route always materialises the residues
+    assert oz.ozaki2_workspace_bytes(300, 200, 100, 12, oz.OZ2_KEEP_RESIDUES) == \
+        oz.ozaki2_workspace_bytes(300, 200, 100, 12)
 
 
 def test_plan_create_validation():
