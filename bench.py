@@ -4,13 +4,17 @@
 One step = one whole pass of the path over one batch of input already
 resident in HBM: deconstruct (scan, max-magnitude code GEMM, scales, residue
 planes) -> residue GEMMs -> reconstruction (+ fallback).  The default
-workload is the 4096^3 GEMM with entries (u-0.5)*exp(0.5 g) at r = 12
-moduli.  Prints ONE JSON line (rank 0, one GPU).
+workload is the largest single-GPU one: the 16384^3 GEMM with entries
+(u-0.5)*exp(2 g) and 1% of the rows of A scaled by 1e200, at r = 15 moduli
+(the FP64-grade count for that range).  Prints ONE JSON line (rank 0, one
+GPU).
 
-Extra fields beside the contract: per-stage times (HIP events on the launch
-stream), the native FP64 DGEMM (torch.matmul float64) on the same inputs, and
-the CPU oracle on a bounded sample of the same workload (with bit-parity and
-exact-error checks of that sample).
+Extra fields beside the contract: the residue GEMMs' launch times (HIP
+events around them on the launch stream, in the timed steps themselves), the
+six-way stage split (a plan created with OZ2_TIME_STAGES, in extra steps
+after the timed ones), the native FP64 DGEMM (torch.matmul float64) on the
+same inputs, and the CPU oracle on a bounded sample of the same workload
+(with bit-parity and exact-error checks of that sample).
 """
 from __future__ import annotations
 
@@ -27,20 +31,24 @@ sys.path.insert(0, ROOT)
 
 FP8_PEAK_TFLOPS = 5000.0      # MI355X dense FP8 (E4M3) MFMA
 HBM_PEAK_GBS = 8000.0
+MIN_WARMUP = 10
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
-    # the clock takes about ten 4096^3 steps (some 20 ms of work) to settle
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", default="gemm4096_lognormal")
+    ap.add_argument("--steps", type=int, default=20)
+    # the clock takes some 20 ms of work to settle after the device idles:
+    # fewer warm-up steps than MIN_WARMUP are raised to it
+    ap.add_argument("--warmup", type=int, default=MIN_WARMUP)
+    ap.add_argument("--config", default="gemm16384_wide")
     ap.add_argument("--moduli", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=int, default=2304,
-                    help="sampled rows and columns of the CPU-oracle baseline (about 12 s of "
-                         "oracle work on the GPU hosts at 4096^3)")
+    ap.add_argument("--cpu-sample", type=int, default=None,
+                    help="sampled rows and columns of the CPU-oracle baseline (default: 512 at "
+                         "k = 16384, 2304 at k = 4096; 10-30 s of oracle work on the GPU hosts)")
+    ap.add_argument("--stage-steps", type=int, default=3,
+                    help="extra steps on a stage-timed plan for the six-way split")
     ap.add_argument("--no-probes", action="store_true", help="skip the measured-peak probes")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB copy kernel (rocprofv3 counter calibration)")
@@ -52,6 +60,11 @@ def parse():
                     help="instead of the bench line: max componentwise error of a sampled set "
                          "of outputs against the exact product for r = 8..16")
     return ap.parse_args()
+
+
+def log(msg):
+    """Progress on stderr (the JSON line alone goes to stdout)."""
+    print(f"bench: {msg}", file=sys.stderr, flush=True)
 
 
 def source_sha256(rel):
@@ -116,8 +129,10 @@ def main():
     if cfg["kind"] == "batched":
         batched_line(args, cfg, r, dev)
         return
+    t_in = time.perf_counter()
     drawn = synth.make(args.config)
     A, B = drawn[0], drawn[1]
+    log(f"inputs of {args.config} drawn in {time.perf_counter() - t_in:.1f} s")
     m, k = A.shape
     n = B.shape[1]
     if args.accuracy_sweep:
@@ -136,42 +151,49 @@ def main():
         Cd = oz.colmajor_empty(m, n, device=dev)
     plan = oz.Plan(m, n, k, r, flags, device=dev)
     stream = torch.cuda.current_stream()
+    warmup = max(args.warmup, MIN_WARMUP)
 
-    def step(ev=None):
+    def step(p, ev=None):
+        p.deconstruct(Ad, Bd)
         if ev is not None:
             ev[0].record(stream)
-        plan.deconstruct(Ad, Bd)
+        p.residue_gemm()
         if ev is not None:
             ev[1].record(stream)
-        plan.residue_gemm()
-        if ev is not None:
-            ev[2].record(stream)
-        plan.reconstruct(Cd)
-        if ev is not None:
-            ev[3].record(stream)
+        p.reconstruct(Cd)
 
-    for _ in range(args.warmup):
-        step()
+    for _ in range(warmup):
+        step(plan)
     torch.cuda.synchronize()
+    log(f"{warmup} warm-up steps done")
 
-    # the timed steps carry no instrumentation; the per-stage split comes from
-    # as many further steps with HIP events between the stages (an event
-    # record between two launches costs the stream a few microseconds)
+    # timed steps: HIP events around the residue GEMMs (the dominant kernel,
+    # one launch per step for k <= 32768) on the stream they are launched on
+    gev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step()
+        step(plan, gev[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    for i in range(args.steps):
-        step(events[i])
-    torch.cuda.synchronize()
-
     ms_step = (t1 - t0) * 1e3 / args.steps
-    dec = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
-    gem = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
-    rec = float(np.mean([e[2].elapsed_time(e[3]) for e in events]))
+    gem = float(np.mean([e[0].elapsed_time(e[1]) for e in gev]))
+    slabs = (k + 32767) // 32768
+    log(f"{args.steps} timed steps: {ms_step:.3f} ms per step, residue GEMMs {gem:.3f} ms")
+
+    # six-way split: a stage-timed plan on the same workspace, extra steps
+    split = {}
+    if args.stage_steps > 0:
+        tplan = oz.Plan(m, n, k, r, flags | oz.OZ2_TIME_STAGES, device=dev,
+                        workspace=plan.workspace)
+        acc = []
+        for _ in range(args.stage_steps):
+            step(tplan)
+            acc.append(tplan.query(oz.OZ2_Q_STAGE_TIMES))
+        split = {name: round(float(np.mean([a[name] for a in acc])), 4) for name in acc[0]}
+        del tplan
+    nfb = plan.query(oz.OZ2_Q_FALLBACK_COUNT)
+
     flop = 2.0 * m * n * k
     tflops = flop / (ms_step * 1e-3) / 1e12
     fp8_flop = 3 * r * flop                     # 3 plane products per modulus
@@ -211,23 +233,33 @@ def main():
         del src, dst
 
     cpu = None
-    if not args.no_cpu_baseline and cfg["kind"] != "rankk":
-        cpu = cpu_baseline(A, B, r, Cd, args.cpu_sample)
+    if not args.no_cpu_baseline:
+        nsamp = args.cpu_sample or (512 if k > 8192 else 2304)
+        log(f"CPU oracle on {nsamp} x {nsamp} sampled outputs ...")
+        C_in = None
+        if cfg["kind"] == "rankk":
+            # one step from the drawn C_in, so that C = C_in + A B
+            C_in = drawn[2]
+            Cd.copy_(oz.to_device_colmajor(C_in, dev))
+            step(plan)
+            torch.cuda.synchronize()
+        cpu = cpu_baseline(A, B, r, Cd, nsamp, C_in=C_in)
 
     tag = f"resgemm_{args.config}_r{r}"
     traffic = pmc_traffic("paper_2606_06510_amd/csrc/gemm.hip", tag)
     mfma_pmc = pmc_mfma("paper_2606_06510_amd/csrc/gemm.hip", tag)
-    dec_bytes = (m * k + k * n) * (8 + 1 + plan_pstore(r))    # A, B read once + codes + planes
-    rec_bytes = m * n * (2 * r + 8)                              # residues read + C written
-    dec_gbs = dec_bytes / (dec * 1e-3) / 1e9
-    rec_gbs = rec_bytes / (rec * 1e-3) / 1e9
+    pstore = plan_pstore(r)
+    # algorithmic bytes: A, B read once, code bytes and planes written once;
+    # residues read and C written (C also read when accumulating)
+    dec_bytes = (m * k + k * n) * (8 + 1 + pstore)
+    rec_bytes = m * n * (2 * r + 8 + (8 if flags & oz.OZ2_ACCUMULATE else 0))
     out = {
         "metric": "effective FP64 TFLOPS of emulated DGEMM (Ozaki-II on FP8 MFMA)",
         "value": round(tflops, 3),
         "unit": "TFLOPS",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": warmup,
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -241,25 +273,33 @@ def main():
                      "achieved": round(achieved, 2), "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
                      "traffic": None if traffic is None else round(traffic),
-                     "per_launch": f"{fp8_flop:.4g} FP8 FLOP (3r plane products x 2mnk)"},
-        "stages_ms": {"deconstruct": round(dec, 4), "residue_gemm": round(gem, 4),
-                      "reconstruct": round(rec, 4)},
+                     "per_launch": f"{fp8_flop / slabs:.4g} FP8 FLOP (3r plane products x "
+                                   f"2mnk{'' if slabs == 1 else f' / {slabs} k-slabs'})",
+                     "timing": f"HIP events around the residue GEMMs in each of the {args.steps} "
+                               f"timed steps, mean {gem:.3f} ms"},
+        "stages_ms": split,
+        "fallback_rows_cols": list(nfb),
         "fp8_mfma_util_residue_gemm": round(achieved / FP8_PEAK_TFLOPS, 4),
         "fp8_mfma_rocprof_residue_gemm": mfma_pmc,
-        "deconstruct_gbs_algorithmic": round(dec_gbs, 1),
-        "deconstruct_frac_hbm": round(dec_gbs / HBM_PEAK_GBS, 4),
-        "reconstruct_gbs_algorithmic": round(rec_gbs, 1),
-        "reconstruct_frac_hbm": round(rec_gbs / HBM_PEAK_GBS, 4),
         "measured_peak": peaks,
         "native_fp64_tflops": native if not isinstance(native, float) else round(native, 3),
         "cpu_baseline": cpu,
     }
-    if peaks:
-        out["frac_of_measured_peak"] = {
-            "residue_gemm_fp8": round(achieved / peaks["fp8_mfma_tflops"], 4),
-            "residue_gemm_fp8_digits": round(achieved / peaks["fp8_mfma_digits_tflops"], 4),
-            "deconstruct_hbm": round(dec_gbs / peaks["hbm_copy_gbs"], 4),
-            "reconstruct_hbm": round(rec_gbs / peaks["hbm_copy_gbs"], 4)}
+    if split:
+        dec = split["scan_codes"] + split["maxmag_gemm"] + split["split"]
+        rec = split["reconstruct"]
+        out["deconstruct_gbs_algorithmic"] = round(dec_bytes / (dec * 1e-3) / 1e9, 1)
+        out["deconstruct_frac_hbm"] = round(dec_bytes / (dec * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+        out["deconstruct_streaming_frac_hbm"] = round(
+            dec_bytes / ((split["scan_codes"] + split["split"]) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+        out["reconstruct_gbs_algorithmic"] = round(rec_bytes / (rec * 1e-3) / 1e9, 1)
+        out["reconstruct_frac_hbm"] = round(rec_bytes / (rec * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+        if peaks:
+            out["frac_of_measured_peak"] = {
+                "residue_gemm_fp8": round(achieved / peaks["fp8_mfma_tflops"], 4),
+                "residue_gemm_fp8_digits": round(achieved / peaks["fp8_mfma_digits_tflops"], 4),
+                "deconstruct_hbm": round(out["deconstruct_gbs_algorithmic"] / peaks["hbm_copy_gbs"], 4),
+                "reconstruct_hbm": round(out["reconstruct_gbs_algorithmic"] / peaks["hbm_copy_gbs"], 4)}
     print(json.dumps(out))
 
 
@@ -293,18 +333,19 @@ def stationary_line(args, cfg, r, dev, A, B):
         if ev is not None:
             ev[3].record(stream)
 
-    for i in range(args.warmup):
+    warmup = max(args.warmup, MIN_WARMUP)
+    for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i)
+        step(warmup + i)
     torch.cuda.synchronize()
     ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
     # per-stage split from as many further, instrumented steps
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     for i in range(args.steps):
-        step(args.warmup + args.steps + i, events[i])
+        step(warmup + args.steps + i, events[i])
     torch.cuda.synchronize()
     dec = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
     gem = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
@@ -312,15 +353,15 @@ def stationary_line(args, cfg, r, dev, A, B):
     flop = 2.0 * m * n * k
     fp8_flop = 3 * r * flop
     achieved = fp8_flop / (gem * 1e-3) / 1e12
-    Blast = B if ((args.warmup + 2 * args.steps - 1) & 1) == 0 else B2
+    Blast = B if ((warmup + 2 * args.steps - 1) & 1) == 0 else B2
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(A, Blast, r, Cd, min(args.cpu_sample, 256), mode="fixed")
+        cpu = cpu_baseline(A, Blast, r, Cd, min(args.cpu_sample or 256, 256), mode="fixed")
     print(json.dumps({
         "metric": "effective FP64 TFLOPS of emulated DGEMM, operand-stationary "
                   "(A's planes kept, fixed scaling)",
         "value": round(flop / (ms_step * 1e-3) / 1e12, 3), "unit": "TFLOPS", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "steps": args.steps, "warmup": warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "fp8-e4m3 MFMA -> exact int -> f64", "data": "synthetic (seeded numpy PCG64)",
         "config": {"workload": f"{args.config} operand-stationary: C = A B_t, m={m} n={n} k={k}, "
@@ -415,10 +456,12 @@ def plan_pstore(r):
     return sum(2 if int(round(x ** 0.5)) ** 2 == x else 3 for x in ms)
 
 
-def cpu_baseline(A, B, r, Cd, nsamp, mode="bound"):
+def cpu_baseline(A, B, r, Cd, nsamp, mode="bound", C_in=None):
     """The oracle, as it stands, on a bounded sample: nsamp sampled rows x nsamp
     sampled columns of the same workload (the scales of a sampled row need its
-    code product against all of B, as the method does)."""
+    code product against all of B, as the method does).  With C_in (C += A B)
+    the device C must hold C_in + A B of one step."""
+    import torch
     import oracle
     from oracle import refgemm
     import paper_2606_06510_amd as oz
@@ -433,14 +476,16 @@ def cpu_baseline(A, B, r, Cd, nsamp, mode="bound"):
     rows = np.sort(rng.choice(m, size=min(nsamp, m), replace=False))
     cols = np.sort(rng.choice(n, size=min(nsamp, n), replace=False))
     t = time.perf_counter()
-    res = oracle.dgemm(A, B, r, rows=rows, cols=cols, mode=mode)
+    res = oracle.dgemm(A, B, r, rows=rows, cols=cols, mode=mode, C_in=C_in)
     dt = time.perf_counter() - t
-    C = oz.from_device_colmajor(Cd)[np.ix_(rows, cols)]
+    C = Cd.index_select(0, torch.as_tensor(rows, device=Cd.device)).index_select(
+        1, torch.as_tensor(cols, device=Cd.device)).cpu().numpy()
     same = int(np.sum(C.view(np.uint64) == res.C.view(np.uint64)))
     rr, cc = np.meshgrid(rows, cols, indexing="ij")
-    # exact componentwise error on the first 1024 sampled entries (fsum per entry)
-    ratio = refgemm.componentwise_ratio(C.ravel()[:1024], A, B, rr.ravel()[:1024],
-                                        cc.ravel()[:1024])
+    # exact componentwise error on the first 1024 sampled entries (fsum per
+    # entry) of the product itself (not defined for C_in + A B)
+    ratio = None if C_in is not None else refgemm.componentwise_ratio(
+        C.ravel()[:1024], A, B, rr.ravel()[:1024], cc.ravel()[:1024])
     return {"value": round(2.0 * k * len(rows) * len(cols) / dt / 1e12, 9), "unit": "TFLOPS",
             "cores": cores, "kind": "oracle",
             "sample": f"{len(rows)}x{len(cols)} output entries (sampled rows x cols) of the same "

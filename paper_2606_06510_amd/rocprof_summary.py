@@ -4,9 +4,9 @@
     python -m paper_2606_06510_amd.rocprof_summary trace TRACE_CSV OUT_MD TITLE COMMAND SKIP COUNT
     python -m paper_2606_06510_amd.rocprof_summary traffic FETCH_CSV WRITE_CSV OUT_TXT \\
         KERNEL COPY_BYTES SOURCE CMD_FETCH CMD_WRITE
-    python -m paper_2606_06510_amd.rocprof_summary mfma COUNTER_CSV OUT_TXT SOURCE CMD
+    python -m paper_2606_06510_amd.rocprof_summary mfma COUNTER_CSV OUT_TXT SOURCE CMD [SKIP]
     python -m paper_2606_06510_amd.rocprof_summary hbm STATS_CSV FETCH_CSV WRITE_CSV OUT_MD \
-        COPY_BYTES M N K R PSTORE CMD_TRACE CMD_FETCH CMD_WRITE
+        COPY_BYTES M N K R PSTORE CMD_TRACE CMD_FETCH CMD_WRITE [SKIP COUNT]
 
 ``stats`` turns a ``--kernel-trace --stats`` kernel_stats.csv into a markdown
 table.  ``trace`` does the same from the per-dispatch kernel_trace.csv, keeping
@@ -23,6 +23,10 @@ GRBM_GUI_ACTIVE`` counter_collection.csv and reports, per FP8-MFMA kernel,
 the FP8 operations per launch (MOPS x 512), the share of SIMD cycles the MFMA
 unit was busy and the shader clock the launch ran at (GRBM_GUI_ACTIVE is
 summed over the XCDs: cycles = sum / XCDs, clock = cycles / duration).
+With SKIP, ``mfma`` leaves out the first SKIP dispatches of each kernel (the
+warm-up launches, which run while the clock settles); with SKIP COUNT,
+``hbm`` takes its mean durations from a kernel_trace.csv given in place of
+STATS_CSV, over dispatches SKIP .. SKIP+COUNT-1 as ``trace`` does.
 ``hbm`` puts the memory-bound kernels of an m x n x k product at r moduli
 (PSTORE plane bytes per input element) side by side: mean duration from the
 kernel trace, algorithmic bytes, the copy-scaled FETCH_SIZE + WRITE_SIZE
@@ -67,25 +71,12 @@ def trace(src, dst, title, cmd, skip, count):
     tot = sum(r[5] for r in rows) or 1.0
     rows.sort(key=lambda r: -r[5])
     with open(dst, "w") as f:
-        f.write(f"# {title}
-
-Command (from the repository root, on one MI355X):
-
-```
-{cmd}
-```
-
-")
+        f.write(f"# {title}\n\nCommand (from the repository root, on one MI355X):\n\n```\n{cmd}\n```\n\n")
         f.write(f"Dispatches {skip} .. {skip + count - 1} of each kernel (launch order), i.e. the "
-                f"timed steps only; warm-up launches excluded.
-
-")
-        f.write("| kernel | calls | avg (us) | min (us) | max (us) | share |
-|---|---|---|---|---|---|
-")
+                f"timed steps only; warm-up launches excluded.\n\n")
+        f.write("| kernel | calls | avg (us) | min (us) | max (us) | share |\n|---|---|---|---|---|---|\n")
         for name, n, avg, lo, hi, t in rows:
-            f.write(f"| {name} | {n} | {avg:.1f} | {lo:.1f} | {hi:.1f} | {100 * t / tot:.1f}% |
-")
+            f.write(f"| {name} | {n} | {avg:.1f} | {lo:.1f} | {hi:.1f} | {100 * t / tot:.1f}% |\n")
 
 
 def _per_launch(path, counter):
@@ -128,16 +119,25 @@ def traffic(fetch_csv, write_csv, dst, kernel, copy_bytes, source, cmd_fetch, cm
             f.write(f"#   {k}: {fetch[k]:.1f} / {write.get(k, float('nan')):.1f}\n")
 
 
-def mfma(src, dst, source, cmd, xcds=8, simds=1024):
+def mfma(src, dst, source, cmd, skip=0, xcds=8, simds=1024):
     per = collections.defaultdict(lambda: collections.defaultdict(float))
-    names, dur = {}, {}
+    names, dur, start = {}, {}, {}
     for r in csv.DictReader(open(src)):
         key = r["Dispatch_Id"]
         per[key][r["Counter_Name"]] += float(r["Counter_Value"])
         names[key] = _short(r["Kernel_Name"])
         dur[key] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+        start[key] = int(r["Start_Timestamp"])
+    order = collections.defaultdict(list)
+    for key in per:
+        order[names[key]].append((start[key], key))
+    keep = set()
+    for name, ks in order.items():
+        keep.update(key for _, key in sorted(ks)[skip:])
     by = collections.defaultdict(list)
     for key, v in per.items():
+        if key not in keep:
+            continue
         if v.get("SQ_INSTS_VALU_MFMA_MOPS_F8", 0.0) <= 0.0:
             continue
         cycles = v["GRBM_GUI_ACTIVE"] / xcds
@@ -149,6 +149,8 @@ def mfma(src, dst, source, cmd, xcds=8, simds=1024):
                 "# operations), SQ_VALU_MFMA_BUSY_CYCLES over the SIMD cycles, GRBM_GUI_ACTIVE over\n"
                 f"# the {xcds} XCDs for the clock.\n")
         f.write(f"command: {cmd}\nkernel_source: {source}\nkernel_source_sha256: {sha}\n")
+        if skip:
+            f.write(f"# the first {skip} launches of each kernel (warm-up) are left out\n")
         f.write("| kernel | launches | avg (us) | FP8 ops per launch | TFLOP/s | MFMA busy | clock (GHz) |\n")
         f.write("|---|---|---|---|---|---|---|\n")
         for k in sorted(by):
@@ -173,9 +175,25 @@ def _algorithmic(m, n, k, r, pstore):
     }
 
 
+def _trace_avg(path, skip, count):
+    by = collections.defaultdict(list)
+    for r in csv.DictReader(open(path)):
+        by[_short(r["Kernel_Name"])].append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    out = {}
+    for name, ds in by.items():
+        sel = [(e - b) * 1e-9 for b, e in sorted(ds)[skip:skip + count]]
+        if sel:
+            out[name] = sum(sel) / len(sel)
+    return out
+
+
 def hbm(stats_csv, fetch_csv, write_csv, dst, copy_bytes, m, n, k, r, pstore, cmd_t, cmd_f, cmd_w,
-        peak=8.0e12):
-    avg = {_short(x["Name"]): float(x["AverageNs"]) * 1e-9 for x in csv.DictReader(open(stats_csv))}
+        skip=None, count=None, peak=8.0e12):
+    if skip is None:
+        avg = {_short(x["Name"]): float(x["AverageNs"]) * 1e-9
+               for x in csv.DictReader(open(stats_csv))}
+    else:
+        avg = _trace_avg(stats_csv, skip, count)
     fetch = _per_launch(fetch_csv, "FETCH_SIZE")
     write = _per_launch(write_csv, "WRITE_SIZE")
     copy = next(x for x in fetch if x.startswith("k_copy"))
@@ -214,10 +232,10 @@ def main(argv):
     elif argv[0] == "traffic":
         traffic(argv[1], argv[2], argv[3], argv[4], int(argv[5]), argv[6], argv[7], argv[8])
     elif argv[0] == "mfma":
-        mfma(*argv[1:5])
+        mfma(*argv[1:5], *(int(x) for x in argv[5:6]))
     elif argv[0] == "hbm":
         hbm(argv[1], argv[2], argv[3], argv[4], int(argv[5]), *map(int, argv[6:11]),
-            argv[11], argv[12], argv[13])
+            argv[11], argv[12], argv[13], *(int(x) for x in argv[14:16]))
     else:
         raise SystemExit(__doc__)
 
