@@ -91,6 +91,22 @@ int ozaki2_dgemm_ex(int m, int n, int k, const double* A, int lda,
                     int num_moduli, unsigned flags, void* workspace,
                     size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): C = A*B as
+ * ozaki2_dgemm, with the workspace taken from a device array of
+ * OZ2_STATIC_SCRATCH_BYTES (64 MiB) that the library holds on every GPU it
+ * runs on until the process ends.  No hipMalloc, hipFree or other allocating
+ * call is made (the first call on a device looks the array's address up once).
+ * Products whose workspace (ozaki2_workspace_bytes(m, n, k, r, 0)) exceeds
+ * the array -- e.g. beyond about 768^3 at r = 12 or 640^3 at r = 16 -- return
+ * OZ2_E_WORKSPACE before any launch.  Every call on a GPU uses that GPU's one
+ * array: calls that overlap in time on one GPU (different streams or host
+ * threads without ordering) race and give undefined results; calls ordered on
+ * one stream are safe.  Same results as ozaki2_dgemm. */
+#define OZ2_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+int ozaki2_dgemm_static(int m, int n, int k, const double* A, int lda, const double* B,
+                        int ldb, double* C, int ldc, int num_moduli, void* stream);
+
 /* batch independent products C_b = A_b * B_b, A_b = A + b*strideA (elements),
  * likewise B_b, C_b; each with the layout rules above.  Strides must keep the
  * output matrices disjoint. Internal workspace as for ozaki2_dgemm. */

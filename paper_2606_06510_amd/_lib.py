@@ -45,7 +45,7 @@ OZ2_Q_STAGE_TIMES = 10
 STAGE_NAMES = ["scan_codes", "maxmag_gemm", "split", "residue_gemm", "reconstruct", "fallback"]
 
 EXPORTS = [
-    "ozaki2_dgemm", "ozaki2_dgemm_ex", "ozaki2_dgemm_strided_batched",
+    "ozaki2_dgemm", "ozaki2_dgemm_ex", "ozaki2_dgemm_static", "ozaki2_dgemm_strided_batched",
     "ozaki2_workspace_bytes", "ozaki2_moduli", "ozaki2_plan_create",
     "ozaki2_plan_destroy", "ozaki2_deconstruct", "ozaki2_deconstruct_a", "ozaki2_deconstruct_b",
     "ozaki2_residue_gemm",
@@ -83,6 +83,7 @@ def load():
     sig = {
         "ozaki2_dgemm": (i, [i, i, i, p, i, p, i, p, i, i, p]),
         "ozaki2_dgemm_ex": (i, [i, i, i, p, i, p, i, p, i, i, u, p, sz, p]),
+        "ozaki2_dgemm_static": (i, [i, i, i, p, i, p, i, p, i, i, p]),
         "ozaki2_dgemm_strided_batched": (i, [i, i, i, p, i, ll, p, i, ll, p, i, ll, i, i, p]),
         "ozaki2_workspace_bytes": (sz, [i, i, i, i, u]),
         "ozaki2_moduli": (i, [i, ctypes.POINTER(ctypes.c_int)]),
@@ -160,6 +161,14 @@ def ozaki2_dgemm_ex(m, n, k, A, lda, B, ldb, C, ldc, num_moduli, flags, workspac
     return _check("ozaki2_dgemm_ex", load().ozaki2_dgemm_ex(
         m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, num_moduli, flags, _ptr(workspace),
         ws_bytes, _stream(stream)))
+
+
+OZ2_STATIC_SCRATCH_BYTES = 64 << 20
+
+
+def ozaki2_dgemm_static(m, n, k, A, lda, B, ldb, C, ldc, num_moduli, stream=None):
+    return _check("ozaki2_dgemm_static", load().ozaki2_dgemm_static(
+        m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, num_moduli, _stream(stream)))
 
 
 def ozaki2_dgemm_strided_batched(m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC,

@@ -308,6 +308,14 @@ int hip_status(hipError_t e) { return e == hipSuccess ? OZ2_OK : OZ2_E_DEVICE; }
 
 }  // namespace
 
+// ---------------------------------------------------------------- static scratch
+// The workspace of ozaki2_dgemm_static: a file-scope device array, one copy on
+// every GPU the library runs on, held until the process ends.  Host code never
+// uses the array's name as an address (on the host it is only a stand-in for
+// the device symbol): the device address of each GPU's copy comes from
+// hipGetSymbolAddress, once per device, and is kept in g_scratch_ptr.
+static __device__ __align__(256) uint8_t scratch[OZ2_STATIC_SCRATCH_BYTES];
+
 // ------------------------------------------------------------------ plans
 // Stage events of an OZ2_TIME_STAGES plan: 0 deconstruct start, 1 after scan +
 // codes, 2 after the max-magnitude GEMM, 3 after the split, 4 / 5 around the
@@ -412,6 +420,25 @@ int pool_get(size_t need, void** out) {   // g_pool_mu held by the caller
     P.bytes = grow;
   }
   *out = P.ptr;
+  return OZ2_OK;
+}
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64];
+
+int scratch_address(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return OZ2_E_DEVICE;
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+      (void)hipGetLastError();
+      return OZ2_E_DEVICE;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
   return OZ2_OK;
 }
 
@@ -597,6 +624,25 @@ int ozaki2_dgemm(int m, int n, int k, const double* A, int lda, const double* B,
   void* ws = nullptr;
   st = pool_get(need, &ws);
   if (st != OZ2_OK) return st;
+  return ozaki2_dgemm_ex(m, n, k, A, lda, B, ldb, C, ldc, num_moduli, 0, ws, need, stream);
+}
+
+int ozaki2_dgemm_static(int m, int n, int k, const double* A, int lda, const double* B, int ldb,
+                        double* C, int ldc, int num_moduli, void* stream) {
+  if (num_moduli < 8 || num_moduli > OZ2_MAXR) return OZ2_E_INVALID;
+  int st = check_mats(m, n, k, A, lda, B, ldb, C, ldc);
+  if (st != OZ2_OK) return st;
+  if (m == 0 || n == 0) return OZ2_OK;
+  const size_t need = ozaki2_workspace_bytes(m, n, k, num_moduli, 0);
+  if (need == 0) return OZ2_E_INVALID;
+  if (need > OZ2_STATIC_SCRATCH_BYTES) return OZ2_E_WORKSPACE;
+  st = device_ok();
+  if (st != OZ2_OK) return st;
+  void* ws = nullptr;
+  st = scratch_address(&ws);
+  if (st != OZ2_OK) return st;
+  // every kernel of the staged path clears what it accumulates into (k_init)
+  // and rebuilds the plane tables, so the previous call's contents do not matter
   return ozaki2_dgemm_ex(m, n, k, A, lda, B, ldb, C, ldc, num_moduli, 0, ws, need, stream);
 }
 

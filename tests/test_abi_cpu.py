@@ -21,7 +21,7 @@ def _declared(header):
 def test_library_exports_every_declared_symbol():
     L = oz.load()
     names = _declared("ozaki2.h")
-    assert len(names) == 16
+    assert len(names) == 17
     for n in names:
         assert hasattr(L, n), n
     assert sorted(_lib.EXPORTS) == names
@@ -146,3 +146,18 @@ def test_plan_create_validation():
     assert L.ozaki2_plan_create(ctypes.byref(h), 8, 8, 8, 5, 0, FAKE, need) == _lib.OZ2_E_INVALID
     assert L.ozaki2_residue_gemm(None, None) == _lib.OZ2_E_INVALID
     assert L.ozaki2_reconstruct(None, FAKE, 8, None) == _lib.OZ2_E_INVALID
+
+
+def test_static_entry_point_validation():
+    """ozaki2_dgemm_static checks its arguments, and refuses a product whose
+    workspace exceeds its static array, before touching the device."""
+    L = oz.load()
+    assert L.ozaki2_dgemm_static(4, 5, 6, FAKE, 3, FAKE + (1 << 20), 6, FAKE + (2 << 20), 4, 12,
+                                 None) == _lib.OZ2_E_INVALID
+    assert L.ozaki2_dgemm_static(4, 5, 6, FAKE, 4, FAKE + (1 << 20), 6, FAKE + (2 << 20), 4, 7,
+                                 None) == _lib.OZ2_E_INVALID
+    n = 1024
+    assert oz.ozaki2_workspace_bytes(n, n, n, 12) > oz.OZ2_STATIC_SCRATCH_BYTES
+    assert L.ozaki2_dgemm_static(n, n, n, FAKE, n, FAKE + (1 << 30), n, FAKE + (2 << 30), n, 12,
+                                 None) == _lib.OZ2_E_WORKSPACE
+    assert L.ozaki2_dgemm_static(0, 5, 6, None, 1, None, 6, None, 1, 12, None) == 0
