@@ -116,6 +116,29 @@ int ozaki2_dgemm_strided_batched(int m, int n, int k, const double* A, int lda,
                                  long long strideC, int batch, int num_moduli,
                                  void* stream);
 
+/* Batched GEMV, the paper's fused Ozaki-II GEMV (Alg. 2, section "Strategy
+ * 1: Batched GEMV"): Y = A X for A (m x k, lda), X (k x nrhs, ldx) with
+ * 1 <= nrhs <= 16 right-hand sides, Y (m x nrhs, ldy), all column-major FP64
+ * device memory.  A is read twice in FP64 -- once for its row exponents,
+ * once by the fused kernel that quantises, reduces and splits it into E4M3
+ * digit planes on the fly and multiplies them on FP8 MFMA against X's planes
+ * with all r moduli's accumulators in registers -- and never written in any
+ * other form.  The scaling is the fixed rule (Alg. 1's mu = k max|A~| max|X~|,
+ * as OZ2_SCALE_FIXED): entries of unflagged rows and columns are the IEEE
+ * RN-even value of D^-1 (A~ X~) E^-1 exactly as ozaki2_dgemm_ex with
+ * OZ2_SCALE_FIXED computes it; flagged rows of A / columns of X (T1, T2) are
+ * recomputed natively.  flags: OZ2_QUANT_TZ, OZ2_NO_FALLBACK,
+ * OZ2_FORCE_FALLBACK (others: OZ2_E_INVALID).  workspace: device memory of
+ * ozaki2_gemv_workspace_bytes(m, k, nrhs, r) bytes, 256-byte aligned.  k = 0
+ * gives Y = 0; m = 0 or nrhs = 0 is a no-op.  Validation as for
+ * ozaki2_dgemm_ex (nrhs > 16: OZ2_E_INVALID). */
+int ozaki2_gemv_batched(int m, int k, int nrhs, const double* A, int lda, const double* X,
+                        int ldx, double* Y, int ldy, int num_moduli, unsigned flags,
+                        void* workspace, size_t ws_bytes, void* stream);
+
+/* Workspace bytes of ozaki2_gemv_batched (0 on invalid arguments). */
+size_t ozaki2_gemv_workspace_bytes(int m, int k, int nrhs, int num_moduli);
+
 /* Workspace bytes ozaki2_dgemm_ex / ozaki2_plan_create need (0 on invalid
  * arguments). */
 size_t ozaki2_workspace_bytes(int m, int n, int k, int num_moduli, unsigned flags);

@@ -6,4 +6,4 @@ streams."""
 from ._lib import *  # noqa: F401,F403
 from ._lib import load, Ozaki2Error, LIB_PATH  # noqa: F401
 from .tensor import (colmajor_empty, to_device_colmajor, from_device_colmajor,  # noqa: F401
-                     matmul, Plan, words_to_ints)
+                     matmul, gemv, Plan, words_to_ints)

@@ -50,7 +50,7 @@ EXPORTS = [
     "ozaki2_plan_destroy", "ozaki2_deconstruct", "ozaki2_deconstruct_a", "ozaki2_deconstruct_b",
     "ozaki2_residue_gemm",
     "ozaki2_reconstruct", "ozaki2_plan_query_bytes", "ozaki2_plan_query",
-    "ozaki2_status_string", "ozaki2_finalize",
+    "ozaki2_status_string", "ozaki2_finalize", "ozaki2_gemv_batched", "ozaki2_gemv_workspace_bytes",
 ]
 
 # include/ozaki2_probes.h
@@ -98,6 +98,8 @@ def load():
         "ozaki2_plan_query": (i, [p, i, p, sz]),
         "ozaki2_status_string": (ctypes.c_char_p, [i]),
         "ozaki2_finalize": (None, []),
+        "ozaki2_gemv_batched": (i, [i, i, i, p, i, p, i, p, i, i, u, p, sz, p]),
+        "ozaki2_gemv_workspace_bytes": (sz, [i, i, i, i]),
         "ozaki2_probe_e4m3": (i, [p, p, i, p]),
         "ozaki2_probe_accum": (i, [p, p, i, p, p]),
         "ozaki2_probe_copy": (i, [p, p, sz, p]),
@@ -180,6 +182,17 @@ def ozaki2_dgemm_strided_batched(m, n, k, A, lda, strideA, B, ldb, strideB, C, l
 
 def ozaki2_workspace_bytes(m, n, k, num_moduli, flags=0):
     return load().ozaki2_workspace_bytes(m, n, k, num_moduli, flags)
+
+
+def ozaki2_gemv_batched(m, k, nrhs, A, lda, X, ldx, Y, ldy, num_moduli, flags, workspace,
+                        ws_bytes, stream=None):
+    return _check("ozaki2_gemv_batched", load().ozaki2_gemv_batched(
+        m, k, nrhs, _ptr(A), lda, _ptr(X), ldx, _ptr(Y), ldy, num_moduli, flags, _ptr(workspace),
+        ws_bytes, _stream(stream)))
+
+
+def ozaki2_gemv_workspace_bytes(m, k, nrhs, num_moduli):
+    return load().ozaki2_gemv_workspace_bytes(m, k, nrhs, num_moduli)
 
 
 def ozaki2_moduli(num_moduli):

@@ -14,7 +14,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(os.path.dirname(HERE), "_build")
 LIB = os.path.join(HERE, "libozaki2.so")
-SOURCES = ["api.cpp", "deconstruct.hip", "gemm.hip", "reconstruct.hip", "batched.hip", "probes.hip"]
+SOURCES = ["api.cpp", "deconstruct.hip", "gemm.hip", "reconstruct.hip", "batched.hip", "gemv.hip",
+           "probes.hip"]
 
 
 def hipcc():
@@ -45,7 +46,7 @@ def _compile(src):
 
 def build(verbose=False):
     os.makedirs(BUILD, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=min(4, len(SOURCES))) as ex:
+    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
     cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]

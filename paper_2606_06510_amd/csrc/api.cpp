@@ -213,7 +213,7 @@ bool make_dims(int m, int n, int k, unsigned flags, Oz2Dims& d) {
 }
 
 Oz2Layout make_layout(const Oz2Dims& d, const Oz2Const& c) {
-  Oz2Layout L;
+  Oz2Layout L{};
   size_t o = 0;
   auto take = [&o](size_t bytes) { size_t at = o; o = align256(o + bytes); return at; };
   L.rowbits = take((size_t)d.mp * 8);
@@ -241,6 +241,65 @@ Oz2Layout make_layout(const Oz2Dims& d, const Oz2Const& c) {
   L.total = o;
   return L;
 }
+
+// ------------------------------------------------------------ batched GEMV
+// Y = A X with X of nrhs <= 16 columns (the fused kernel of gemv.hip): k in
+// chunks of 128, 64 rows of A per workgroup, and enough k-splits that every
+// split spans at most 32768 k (exact FP32 accumulation) and the row blocks
+// times the splits cover about 256 workgroups.
+constexpr int kGemvRhs = 16, kGemvK = 128, kGemvRows = 64;
+
+struct GemvShape {
+  Oz2Dims d;          // n = nrhs, np = 16, mp = rows padded to 64, kp to 128
+  int chunks, splits;
+};
+
+bool gemv_shape(int m, int k, int nrhs, unsigned flags, GemvShape& g) {
+  if (m < 0 || k < 0 || nrhs < 0 || nrhs > kGemvRhs) return false;
+  Oz2Dims& d = g.d;
+  d.m = m;
+  d.n = nrhs;
+  d.k = k;
+  d.mp = round_up(std::max(m, 1), kGemvRows);
+  d.np = kGemvRhs;
+  d.kp = round_up(std::max(k, 1), kGemvK);
+  d.cslabs = 1;
+  d.flags = flags | OZ2_SCALE_FIXED;
+  if ((double)d.mp * d.kp >= 1099511627776.0) return false;
+  g.chunks = d.kp / kGemvK;
+  const int need = (g.chunks + 255) / 256;
+  const int blocks = d.mp / kGemvRows;
+  const int fill = std::min(g.chunks, (256 + blocks - 1) / blocks);
+  g.splits = std::max(need, fill);
+  return true;
+}
+
+Oz2Layout make_gemv_layout(const GemvShape& g, const Oz2Const& c) {
+  const Oz2Dims& d = g.d;
+  Oz2Layout L{};
+  size_t o = 0;
+  auto take = [&o](size_t bytes) { size_t at = o; o = align256(o + bytes); return at; };
+  L.rowbits = take((size_t)d.mp * 8);
+  L.colbits = take((size_t)d.np * 8);
+  L.flagsA = take((size_t)d.mp * 4);
+  L.flagsB = take((size_t)d.np * 4);
+  L.Rmax = take((size_t)d.mp * 4);
+  L.Kmax = take((size_t)d.np * 4);
+  L.sA = take((size_t)d.mp * 4);
+  L.tB = take((size_t)d.np * 4);
+  L.eA = take((size_t)d.mp * 4);
+  L.eB = take((size_t)d.np * 4);
+  L.counters = take(64);
+  L.listA = take((size_t)d.mp * 4);
+  L.listB = take((size_t)d.np * 4);
+  L.tabs = take((size_t)c.tabsz * 4);
+  L.xfrag = take((size_t)g.chunks * c.P * 2048);
+  L.part = take((size_t)g.splits * c.r * d.mp * kGemvRhs * 2);
+  L.total = o;
+  return L;
+}
+
+const unsigned kGemvFlags = OZ2_QUANT_TZ | OZ2_NO_FALLBACK | OZ2_FORCE_FALLBACK;
 
 const unsigned kKnownFlags = OZ2_ACCUMULATE | OZ2_SCALE_FIXED | OZ2_QUANT_TZ | OZ2_NO_FALLBACK |
                              OZ2_FORCE_FALLBACK | OZ2_KEEP_RESIDUES | OZ2_TIME_STAGES;
@@ -688,6 +747,65 @@ int ozaki2_dgemm_strided_batched(int m, int n, int k, const double* A, int lda, 
     if (st != OZ2_OK) return st;
   }
   return OZ2_OK;
+}
+
+size_t ozaki2_gemv_workspace_bytes(int m, int k, int nrhs, int num_moduli) {
+  Oz2Const c;
+  GemvShape g;
+  if (!make_const(num_moduli, c) || !gemv_shape(m, k, nrhs, 0, g)) return 0;
+  return make_gemv_layout(g, c).total;
+}
+
+int ozaki2_gemv_batched(int m, int k, int nrhs, const double* A, int lda, const double* X, int ldx,
+                        double* Y, int ldy, int num_moduli, unsigned flags, void* workspace,
+                        size_t ws_bytes, void* stream) {
+  if (flags & ~kGemvFlags) return OZ2_E_INVALID;
+  if (num_moduli < 8 || num_moduli > OZ2_MAXR || nrhs > kGemvRhs) return OZ2_E_INVALID;
+  int st = check_mats(m, nrhs, k, A, lda, X, ldx, Y, ldy);
+  if (st != OZ2_OK) return st;
+  if (m == 0 || nrhs == 0) return OZ2_OK;
+  hipStream_t s = (hipStream_t)stream;
+  if (k == 0) {
+    st = device_ok();
+    return st != OZ2_OK ? st : hip_status(oz2_launch_fill(Y, m, nrhs, ldy, s));
+  }
+  Oz2Const c;
+  GemvShape g;
+  if (!make_const(num_moduli, c) || !gemv_shape(m, k, nrhs, flags, g)) return OZ2_E_INVALID;
+  // the fused kernel treats moduli r-6 .. r-1 (the six squares) as square
+  for (int i = 0; i < c.r; ++i)
+    if ((c.sq[i] != 0) != (i >= c.r - 6)) return OZ2_E_UNSUPPORTED;
+  const Oz2Layout L = make_gemv_layout(g, c);
+  if (!workspace || ws_bytes < L.total || ((uintptr_t)workspace & 255)) return OZ2_E_WORKSPACE;
+  st = device_ok();
+  if (st != OZ2_OK) return st;
+  uint8_t* ws = (uint8_t*)workspace;
+  const Oz2Dims& d = g.d;
+  const unsigned tz = (flags & OZ2_QUANT_TZ) ? 1u : 0u;
+  const int listed = (flags & OZ2_FORCE_FALLBACK) ? 1 : 0;
+  const int both = OZ2_SIDE_A | OZ2_SIDE_B;
+  hipError_t e = oz2_launch_init(d, L, ws, both, s);
+  if (e == hipSuccess) e = oz2_launch_scan(d, L, ws, A, lda, X, ldx, both, s);
+  if (e == hipSuccess) e = oz2_launch_scales(d, L, c, ws, both, s);
+  if (e == hipSuccess) e = oz2_launch_tables(L, c, ws, s);
+  if (e == hipSuccess)
+    e = oz2_launch_gemv_xplanes(c, X, ldx, k, nrhs, (const int32_t*)(ws + L.tB),
+                                (uint32_t*)(ws + L.flagsB), (int*)(ws + L.counters) + 1,
+                                (int*)(ws + L.listB), listed, (const uint32_t*)(ws + L.tabs), tz,
+                                ws + L.xfrag, s);
+  if (e == hipSuccess)
+    e = oz2_launch_gemv(c, A, lda, m, k, g.splits, (const int32_t*)(ws + L.sA),
+                        (uint32_t*)(ws + L.flagsA), (int*)(ws + L.counters), (int*)(ws + L.listA),
+                        listed, ws + L.xfrag, (const uint32_t*)(ws + L.tabs), tz,
+                        (int16_t*)(ws + L.part), d.mp, s);
+  const int nofb = (flags & OZ2_NO_FALLBACK) ? 1 : 0;
+  if (e == hipSuccess)
+    e = oz2_launch_gemv_crt(c, (const int16_t*)(ws + L.part), g.splits, d.mp, m, nrhs,
+                            (const int32_t*)(ws + L.sA), (const int32_t*)(ws + L.tB),
+                            (const uint32_t*)(ws + L.flagsA), (const uint32_t*)(ws + L.flagsB),
+                            nofb, Y, ldy, s);
+  if (e == hipSuccess && !nofb) e = oz2_launch_fallback_direct(d, L, ws, A, lda, X, ldx, Y, ldy, s);
+  return hip_status(e);
 }
 
 void ozaki2_finalize(void) {

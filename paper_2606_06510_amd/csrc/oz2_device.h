@@ -322,21 +322,29 @@ __device__ __forceinline__ void crt38_fix(const Oz2Const& c, double& S0, double&
 // quotient estimate, and the exact range check where the estimate is
 // ambiguous.  (The reconstruction rounds these limbs; the integer query of
 // the staged API exports them.)
-template <int R, int I>
-__device__ __forceinline__ void crt38_limbs(const Oz2Const& c, const uint4 (&x)[R], double& S0,
-                                            double& S1, double& S2) {
+template <int R>
+__device__ __forceinline__ void crt38_sum(const Oz2Const& c, const double (&xi)[R], double& S0,
+                                          double& S1, double& S2) {
   static_assert(R <= 12, "three radix-2^38 limbs hold [-M/2, M/2) only for r <= 12");
   S0 = 0.0;
   S1 = 0.0;
   S2 = 0.0;
 #pragma unroll
   for (int i = 0; i < R; ++i) {
-    const double xi = res_at<I>(x[i]);
-    S0 = fma(xi, c.W38[i][0], S0);
-    S1 = fma(xi, c.W38[i][1], S1);
-    S2 = fma(xi, c.W38[i][2], S2);
+    S0 = fma(xi[i], c.W38[i][0], S0);
+    S1 = fma(xi[i], c.W38[i][1], S1);
+    S2 = fma(xi[i], c.W38[i][2], S2);
   }
   if (crt38_reduce(c, S0, S1, S2)) crt38_fix(c, S0, S1, S2);
+}
+
+template <int R, int I>
+__device__ __forceinline__ void crt38_limbs(const Oz2Const& c, const uint4 (&x)[R], double& S0,
+                                            double& S1, double& S2) {
+  double xi[R];
+#pragma unroll
+  for (int i = 0; i < R; ++i) xi[i] = res_at<I>(x[i]);
+  crt38_sum<R>(c, xi, S0, S1, S2);
 }
 
 template <int R, int I>

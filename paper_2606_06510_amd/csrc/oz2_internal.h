@@ -78,6 +78,8 @@ struct Oz2Layout {
   size_t listA, listB;        // int32 [mp] / [np]: flagged row / column indices
   size_t panel;               // double [k][min(mp, OZ2_FBCAP)]: the first flagged rows of A,
                               //   gathered for the native fallback (absent with NO_FALLBACK)
+  size_t xfrag;               // batched GEMV: uint8 [chunks][P][2][64][16] operand fragments of X
+  size_t part;                // batched GEMV: int16 [splits][r][mp/16][64][4] partial residues
   size_t total;
 };
 
@@ -125,6 +127,23 @@ hipError_t oz2_launch_integers(const Oz2Dims& d, const Oz2Layout& L, const Oz2Co
 hipError_t oz2_launch_crt_probe(const Oz2Const& c, const int16_t* res, const int* e, int n,
                                 uint32_t* words, double* rounded, hipStream_t s);
 hipError_t oz2_launch_fill(double* C, int m, int n, int ldc, hipStream_t s);
+// the native fallback reading A directly (no gathered panel)
+hipError_t oz2_launch_fallback_direct(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
+                                      const double* A, int lda, const double* B, int ldb,
+                                      double* C, int ldc, hipStream_t s);
+// batched GEMV (gemv.hip): X's operand fragments; the fused GEMV over
+// `splits` k-ranges into partial residues; their reconstruction into Y
+hipError_t oz2_launch_gemv_xplanes(const Oz2Const& c, const double* X, int ldx, int k, int nrhs,
+                                   const int32_t* tB, uint32_t* flagsB, int* countB, int* listB,
+                                   int listed, const uint32_t* tab, unsigned tz, uint8_t* xf,
+                                   hipStream_t s);
+hipError_t oz2_launch_gemv(const Oz2Const& c, const double* A, int lda, int m, int k, int splits,
+                           const int32_t* sA, uint32_t* flagsA, int* countA, int* listA,
+                           int listed, const uint8_t* xf, const uint32_t* tab, unsigned tz,
+                           int16_t* part, int mp, hipStream_t s);
+hipError_t oz2_launch_gemv_crt(const Oz2Const& c, const int16_t* part, int splits, int mp, int m,
+                               int nrhs, const int32_t* sA, const int32_t* tB, const uint32_t* fA,
+                               const uint32_t* fB, int nofb, double* Y, int ldy, hipStream_t s);
 // all of Alg. 1 for `batch` problems of m, n, k <= 64 in one launch; tab = the
 // residue -> plane-byte tables (oz2_launch_tables); iout (normally null, a
 // diagnostic): write the exact integers of the unflagged outputs there,

@@ -427,6 +427,16 @@ hipError_t oz2_launch_fallback(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws
   return hipGetLastError();
 }
 
+hipError_t oz2_launch_fallback_direct(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
+                                      const double* A, int lda, const double* B, int ldb,
+                                      double* C, int ldc, hipStream_t s) {
+  hipLaunchKernelGGL(k_fallback, dim3(1024), dim3(256), 0, s, d, A, lda, B, ldb, C, ldc,
+                     (const int*)(ws + L.counters), (const int*)(ws + L.listA),
+                     (const int*)(ws + L.listB), (const uint32_t*)(ws + L.flagsA),
+                     (const double*)nullptr, 0);
+  return hipGetLastError();
+}
+
 hipError_t oz2_launch_fill(double* C, int m, int n, int ldc, hipStream_t s) {
   const size_t total = (size_t)m * n;
   hipLaunchKernelGGL(k_fill, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, C, m, n, ldc);

@@ -84,6 +84,32 @@ def matmul(A, B, num_moduli=12, flags=0, C=None, workspace=None, stream=None):
     return C
 
 
+def gemv(A, X, num_moduli=13, flags=0, Y=None, workspace=None, stream=None):
+    """Y = A X for a column-major float64 A (m x k) and X (k x nrhs), nrhs <= 16,
+    through the fused batched GEMV (fixed scaling); returns Y."""
+    import torch
+    if A.dim() != 2 or X.dim() != 2:
+        raise ValueError("A and X must be matrices")
+    m, k = A.shape
+    k2, nrhs = X.shape
+    if k != k2:
+        raise ValueError("inner dimensions differ")
+    dev = A.device
+    items = [("A", A, (m, k)), ("X", X, (k, nrhs))] + ([("Y", Y, (m, nrhs))] if Y is not None else [])
+    _check_matrices(dev, *items)
+    if Y is None:
+        Y = colmajor_empty(m, nrhs, device=dev)
+    lda, ldx, ldy = _check_matrices(dev, ("A", A, (m, k)), ("X", X, (k, nrhs)), ("Y", Y, (m, nrhs)))
+    need = _lib.ozaki2_gemv_workspace_bytes(m, k, nrhs, num_moduli)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    elif workspace.device != dev or workspace.numel() * workspace.element_size() < need:
+        raise ValueError("workspace: too small or on another device")
+    _lib.ozaki2_gemv_batched(m, k, nrhs, A, lda, X, ldx, Y, ldy, num_moduli, flags, workspace,
+                             workspace.numel() * workspace.element_size(), stream)
+    return Y
+
+
 def words_to_ints(w):
     """uint32 [..., 5] little-endian two's complement words -> Python ints
     (object array of shape w.shape[:-1])."""

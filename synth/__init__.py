@@ -19,6 +19,8 @@ any extra draws):
   spans ~2^664 and cannot be certified by per-row scaling.
 * ``rankk`` (rank-k update): A m x k, B k x n, C_in m x n, all
   ``(u-0.5)*exp(0.5*g)``; C_in drawn after A and B.
+* ``gemv16384x8`` (batched GEMV): A 16384 x 16384 and X 16384 x 8, entries
+  as ``lognormal05`` (seed 6).
 * ``batched``: ``batch`` independent problems; A_b, B_b iid U(-1,1), each
   multiplied by its own scale ``10**rng.uniform(-8, 8)``; all A entries are
   drawn first, then all B entries, then the A scales, then the B scales.
@@ -106,6 +108,8 @@ CONFIGS = {
     "gemm16384_wide_span": dict(kind="wide_span", m=16384, n=16384, k=16384, seed=31, r=15),
     "rankk32768x256": dict(kind="rankk", m=32768, n=32768, k=256, seed=4, r=12),
     "batched8192x64": dict(kind="batched", batch=8192, m=64, n=64, k=64, seed=5, r=12),
+    # batched GEMV Y = A X (n = right-hand sides): A as the 4096^3 case's entries
+    "gemv16384x8": dict(kind="lognormal", m=16384, n=8, k=16384, seed=6, r=13),
 }
 
 

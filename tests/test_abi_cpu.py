@@ -21,7 +21,7 @@ def _declared(header):
 def test_library_exports_every_declared_symbol():
     L = oz.load()
     names = _declared("ozaki2.h")
-    assert len(names) == 17
+    assert len(names) == 19
     for n in names:
         assert hasattr(L, n), n
     assert sorted(_lib.EXPORTS) == names
@@ -161,3 +161,35 @@ def test_static_entry_point_validation():
     assert L.ozaki2_dgemm_static(n, n, n, FAKE, n, FAKE + (1 << 30), n, FAKE + (2 << 30), n, 12,
                                  None) == _lib.OZ2_E_WORKSPACE
     assert L.ozaki2_dgemm_static(0, 5, 6, None, 1, None, 6, None, 1, 12, None) == 0
+
+
+@pytest.mark.parametrize("args", [
+    dict(m=-1), dict(k=-1), dict(nrhs=17), dict(nrhs=-1), dict(lda=3), dict(ldx=5), dict(ldy=3),
+    dict(r=7), dict(r=17), dict(A=0), dict(X=0), dict(Y=0), dict(flags=oz.OZ2_ACCUMULATE),
+    dict(flags=oz.OZ2_SCALE_FIXED), dict(flags=1 << 9),
+])
+def test_gemv_invalid_arguments_rejected(args):
+    p = dict(m=4, k=6, nrhs=3, A=FAKE, lda=4, X=FAKE + (1 << 20), ldx=6, Y=FAKE + (2 << 20), ldy=4,
+             r=12, flags=0)
+    p.update(args)
+    L = oz.load()
+    st = L.ozaki2_gemv_batched(p["m"], p["k"], p["nrhs"], p["A"] or None, p["lda"],
+                               p["X"] or None, p["ldx"], p["Y"] or None, p["ldy"], p["r"],
+                               p["flags"], FAKE + (3 << 20), 1 << 30, None)
+    assert st == _lib.OZ2_E_INVALID
+
+
+def test_gemv_workspace_bytes():
+    # X's operand fragments (P planes x 2 KiB per 128 k) and the partial
+    # residues (splits x r x rows padded to 64 x 16 x 2 bytes) dominate
+    for m, k, nrhs, r in [(16384, 16384, 8, 13), (100, 70000, 3, 12), (1, 1, 1, 8)]:
+        b = oz.ozaki2_gemv_workspace_bytes(m, k, nrhs, r)
+        P = sum(2 if int(round(x ** 0.5)) ** 2 == x else 3 for x in oz.ozaki2_moduli(r))
+        chunks = (k + 127) // 128
+        assert b >= chunks * P * 2048 + r * ((m + 63) // 64 * 64) * 32, (m, k, b)
+    assert oz.ozaki2_gemv_workspace_bytes(10, 10, 17, 12) == 0
+    assert oz.ozaki2_gemv_workspace_bytes(10, 10, 4, 7) == 0
+    L = oz.load()
+    assert L.ozaki2_gemv_batched(0, 5, 3, None, 1, None, 5, None, 1, 12, 0, None, 0, None) == 0
+    assert L.ozaki2_gemv_batched(4, 5, 3, FAKE, 4, FAKE + (1 << 20), 5, FAKE + (2 << 20), 4, 12, 0,
+                                 None, 0, None) == _lib.OZ2_E_WORKSPACE
