@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--cpu-sample", type=int, default=None,
                     help="sampled rows and columns of the CPU-oracle baseline (default: 512 at "
                          "k = 16384, 2304 at k = 4096; 10-30 s of oracle work on the GPU hosts)")
+    ap.add_argument("--route", choices=["staged", "fused"], default="staged",
+                    help="residue GEMMs and reconstruction as separate stages (the library's "
+                         "default), or fused into one kernel (OZ2_FUSED: r <= 12, k <= 32768)")
     ap.add_argument("--stage-steps", type=int, default=3,
                     help="extra steps on a stage-timed plan for the six-way split")
     ap.add_argument("--no-probes", action="store_true", help="skip the measured-peak probes")
@@ -105,7 +108,7 @@ def pmc_mfma(kernel_src, tag):
         return None
     for x in lines:
         cells = [c.strip() for c in x.strip("|").split("|")]
-        if len(cells) == 7 and "k_resgemm" in cells[0]:
+        if len(cells) == 7 and ("k_resgemm" in cells[0]):
             return {"mfma_busy": cells[5], "clock_ghz": float(cells[6]),
                     "fp8_ops_per_launch": float(cells[3]), "source": os.path.relpath(path, ROOT)}
     return None
@@ -152,6 +155,8 @@ def main():
         flags = oz.OZ2_ACCUMULATE
     else:
         Cd = oz.colmajor_empty(m, n, device=dev)
+    if args.route == "fused":
+        flags |= oz.OZ2_FUSED
     plan = oz.Plan(m, n, k, r, flags, device=dev)
     stream = torch.cuda.current_stream()
     warmup = max(args.warmup, MIN_WARMUP)
@@ -164,6 +169,8 @@ def main():
         if ev is not None:
             ev[1].record(stream)
         p.reconstruct(Cd)
+        if ev is not None:
+            ev[2].record(stream)
 
     for _ in range(warmup):
         step(plan)
@@ -172,7 +179,7 @@ def main():
 
     # timed steps: HIP events around the residue GEMMs (the dominant kernel,
     # one launch per step for k <= 32768) on the stream they are launched on
-    gev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    gev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -180,7 +187,11 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
-    gem = float(np.mean([e[0].elapsed_time(e[1]) for e in gev]))
+    fused = bool(flags & oz.OZ2_FUSED)
+    # the dominant kernel: the residue GEMMs, or the fused kernel that runs
+    # them inside the reconstruction
+    gem = float(np.mean([(e[1].elapsed_time(e[2]) if fused else e[0].elapsed_time(e[1]))
+                         for e in gev]))
     slabs = (k + 32767) // 32768
     log(f"{args.steps} timed steps: {ms_step:.3f} ms per step, residue GEMMs {gem:.3f} ms")
 
@@ -248,9 +259,10 @@ def main():
             torch.cuda.synchronize()
         cpu = cpu_baseline(A, B, r, Cd, nsamp, C_in=C_in)
 
-    tag = f"resgemm_{args.config}_r{r}"
-    traffic = pmc_traffic("paper_2606_06510_amd/csrc/gemm.hip", tag)
-    mfma_pmc = pmc_mfma("paper_2606_06510_amd/csrc/gemm.hip", tag)
+    tag = f"{'fused' if fused else 'resgemm'}_{args.config}_r{r}"
+    ksrc = "paper_2606_06510_amd/csrc/" + ("fused.hip" if fused else "gemm.hip")
+    traffic = pmc_traffic(ksrc, tag)
+    mfma_pmc = pmc_mfma(ksrc, tag)
     pstore = plan_pstore(r)
     # algorithmic bytes: A, B read once, code bytes and planes written once;
     # residues read and C written (C also read when accumulating)
@@ -269,17 +281,21 @@ def main():
         "vs_baseline": None,
         "dtype": "fp8-e4m3 MFMA -> exact int -> f64",
         "data": "synthetic (seeded numpy PCG64)",
-        "config": {"workload": f"{args.config}: C = A B, m={m} n={n} k={k}, "
-                               f"{cfg['kind']} entries, r={r} moduli (alpha={3 * r + 1})",
+        "config": {"workload": f"{args.config}: C {'+' if flags & oz.OZ2_ACCUMULATE else ''}= "
+                               f"A B, m={m} n={n} k={k}, {cfg['kind']} entries, r={r} moduli "
+                               f"(alpha={3 * r + 1})"
+                               f"{', residue GEMMs fused with the reconstruction' if flags & oz.OZ2_FUSED else ''}",
                    "m": m, "n": n, "k": k, "num_moduli": r},
-        "roofline": {"bound": "mfma", "kernel": "k_resgemm (residue GEMMs, 3r FP8 products)",
+        "roofline": {"bound": "mfma",
+                     "kernel": ("k_resgemm_crt (residue GEMMs fused with the reconstruction)"
+                                if fused else "k_resgemm (residue GEMMs, 3r FP8 products)"),
                      "achieved": round(achieved, 2), "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
                      "traffic": None if traffic is None else round(traffic),
                      "per_launch": f"{fp8_flop / slabs:.4g} FP8 FLOP (3r plane products x "
                                    f"2mnk{'' if slabs == 1 else f' / {slabs} k-slabs'})",
-                     "timing": f"HIP events around the residue GEMMs in each of the {args.steps} "
-                               f"timed steps, mean {gem:.3f} ms"},
+                     "timing": f"HIP events around the {'fused kernel' if fused else 'residue GEMMs'}"
+                               f" in each of the {args.steps} timed steps, mean {gem:.3f} ms"},
         "stages_ms": split,
         "fallback_rows_cols": list(nfb),
         "fp8_mfma_util_residue_gemm": round(achieved / FP8_PEAK_TFLOPS, 4),
@@ -291,6 +307,8 @@ def main():
     if split:
         dec = split["scan_codes"] + split["maxmag_gemm"] + split["split"]
         rec = split["reconstruct"]
+        if fused:   # the reconstruction reads no residues; its kernel is the MFMA-bound one
+            rec_bytes = m * n * (8 + (8 if flags & oz.OZ2_ACCUMULATE else 0))
         out["deconstruct_gbs_algorithmic"] = round(dec_bytes / (dec * 1e-3) / 1e9, 1)
         out["deconstruct_frac_hbm"] = round(dec_bytes / (dec * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
         out["deconstruct_streaming_frac_hbm"] = round(
@@ -370,7 +388,9 @@ def stationary_line(args, cfg, r, dev, A, B):
         "config": {"workload": f"{args.config} operand-stationary: C = A B_t, m={m} n={n} k={k}, "
                                f"r={r} moduli (alpha={3 * r}), new B each step",
                    "m": m, "n": n, "k": k, "num_moduli": r},
-        "roofline": {"bound": "mfma", "kernel": "k_resgemm (residue GEMMs, 3r FP8 products)",
+        "roofline": {"bound": "mfma",
+                     "kernel": ("k_resgemm_crt (residue GEMMs fused with the reconstruction)"
+                                if fused else "k_resgemm (residue GEMMs, 3r FP8 products)"),
                      "achieved": round(achieved, 2), "peak": FP8_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
                      "traffic": None},

@@ -66,12 +66,20 @@ enum {
   OZ2_QUANT_TZ = 4u,       /* quantise by truncation toward zero instead of RN-even */
   OZ2_NO_FALLBACK = 8u,    /* never recompute flagged rows natively */
   OZ2_FORCE_FALLBACK = 16u,/* recompute every row natively (testing aid) */
-  OZ2_KEEP_RESIDUES = 32u, /* materialise the r residues of every output in the workspace:
-                              ozaki2_dgemm_ex then takes the staged route even where its
-                              fused residue-GEMM + reconstruction kernel would serve; a
-                              plan's stages always keep them (implied) */
-  OZ2_TIME_STAGES = 64u    /* plans only: record HIP events between the stages on the
+  OZ2_KEEP_RESIDUES = 32u, /* materialise the r residues of every output in the workspace
+                              (the staged route, which every call takes unless OZ2_FUSED is
+                              given: the flag only forbids OZ2_FUSED alongside it) */
+  OZ2_TIME_STAGES = 64u,   /* plans only: record HIP events between the stages on the
                               stream of each call (OZ2_Q_STAGE_TIMES) */
+  OZ2_FUSED = 128u         /* the residue GEMMs and the reconstruction as one kernel that
+                              keeps every output's residues on chip (r <= 12 and k <= 32768;
+                              OZ2_E_UNSUPPORTED otherwise): nothing of them is written to the
+                              workspace, so ozaki2_workspace_bytes is smaller.  In a plan,
+                              ozaki2_residue_gemm then only marks its stage and
+                              ozaki2_reconstruct runs the fused kernel; OZ2_Q_RESIDUES and
+                              OZ2_Q_INTEGERS are not available.  Results are those of the
+                              staged route bit for bit; on MI355X it is the slower route (see
+                              ozaki2_dgemm_ex), so it is taken only when asked for */
 };
 
 /* C = A*B with the default flags (accumulation: ozaki2_dgemm_ex).

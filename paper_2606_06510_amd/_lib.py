@@ -29,6 +29,7 @@ OZ2_NO_FALLBACK = 8
 OZ2_FORCE_FALLBACK = 16
 OZ2_KEEP_RESIDUES = 32
 OZ2_TIME_STAGES = 64
+OZ2_FUSED = 128
 
 OZ2_Q_EXPONENTS = 1
 OZ2_Q_MAXIMA = 2
@@ -78,6 +79,11 @@ def load():
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
                            "(python paper_2606_06510_amd/build.py)")
+    # torch first: its HIP runtime is then the one the library's
+    # libamdhip64.so.7 dependency resolves to, so device pointers and streams
+    # from torch and the library's launches share one runtime whatever the
+    # caller imported first
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     i, u, p, sz, ll = ctypes.c_int, ctypes.c_uint, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_longlong
     sig = {

@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(os.path.dirname(HERE), "_build")
 LIB = os.path.join(HERE, "libozaki2.so")
 SOURCES = ["api.cpp", "deconstruct.hip", "gemm.hip", "reconstruct.hip", "batched.hip", "gemv.hip",
-           "probes.hip"]
+           "fused.hip", "probes.hip"]
 
 
 def hipcc():

@@ -236,8 +236,12 @@ Oz2Layout make_layout(const Oz2Dims& d, const Oz2Const& c) {
   L.planesA = take((size_t)c.P * d.mp * d.kp);
   L.planesB = take((size_t)c.P * d.np * d.kp);
   L.tabs = take((size_t)c.tabsz * 4);
-  L.res = take((size_t)c.r * d.mp * d.np * 2);
-  L.panel = (d.flags & OZ2_NO_FALLBACK) ? 0 : take((size_t)std::min(d.mp, OZ2_FBCAP) * d.k * 8);
+  // the fused route keeps the residues on chip, and its native fallback reads A
+  // directly (no gathered panel)
+  const bool fused = (d.flags & OZ2_FUSED) != 0;
+  L.res = fused ? 0 : take((size_t)c.r * d.mp * d.np * 2);
+  L.panel = ((d.flags & OZ2_NO_FALLBACK) || fused)
+                ? 0 : take((size_t)std::min(d.mp, OZ2_FBCAP) * d.k * 8);
   L.total = o;
   return L;
 }
@@ -302,7 +306,19 @@ Oz2Layout make_gemv_layout(const GemvShape& g, const Oz2Const& c) {
 const unsigned kGemvFlags = OZ2_QUANT_TZ | OZ2_NO_FALLBACK | OZ2_FORCE_FALLBACK;
 
 const unsigned kKnownFlags = OZ2_ACCUMULATE | OZ2_SCALE_FIXED | OZ2_QUANT_TZ | OZ2_NO_FALLBACK |
-                             OZ2_FORCE_FALLBACK | OZ2_KEEP_RESIDUES | OZ2_TIME_STAGES;
+                             OZ2_FORCE_FALLBACK | OZ2_KEEP_RESIDUES | OZ2_TIME_STAGES | OZ2_FUSED;
+
+// The fused residue-GEMM + reconstruction kernel holds r <= 12 residues per
+// output packed in four words and runs one exact FP32 slab of k.
+bool fused_ok(const Oz2Dims& d, const Oz2Const& c) { return c.r <= 12 && d.kp <= OZ2_KSLAB; }
+
+// The route of ozaki2_dgemm / _ex / _static: the fused kernel only when the
+// caller asks for it.  Measured on MI355X at 8192^2 and 16384^2 with k from
+// 256 to 4096 it is 1.2-1.5x slower than the staged route (its 128 x 128
+// tiles need twice the operand bytes per FLOP from L2, and its CRT epilogue
+// leaves the matrix cores idle), although it moves a fraction of the HBM
+// bytes; the staged route stays the default.
+unsigned route_flags(int, int, int, int, unsigned flags) { return flags; }
 
 }  // namespace
 
@@ -439,11 +455,15 @@ int run_deconstruct(ozaki2_plan_s& p, int side, hipStream_t s) {
 }
 
 int run_reconstruct(ozaki2_plan_s& p, double* C, int ldc, hipStream_t s) {
+  const bool fused = (p.d.flags & OZ2_FUSED) != 0;
   hipError_t e = mark(p, 6, s);
-  if (e == hipSuccess) e = oz2_launch_reconstruct(p.d, p.L, p.c, p.ws, p.A, p.lda, C, ldc, s);
+  if (e == hipSuccess)
+    e = fused ? oz2_launch_fused(p.d, p.L, p.c, p.ws, C, ldc, s)
+              : oz2_launch_reconstruct(p.d, p.L, p.c, p.ws, p.A, p.lda, C, ldc, s);
   if (e == hipSuccess) e = mark(p, 7, s);
   if (e == hipSuccess && !(p.d.flags & OZ2_NO_FALLBACK))
-    e = oz2_launch_fallback(p.d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, C, ldc, s);
+    e = fused ? oz2_launch_fallback_direct(p.d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, C, ldc, s)
+              : oz2_launch_fallback(p.d, p.L, p.ws, p.A, p.lda, p.B, p.ldb, C, ldc, s);
   if (e == hipSuccess) e = mark(p, 8, s);
   return hip_status(e);
 }
@@ -540,9 +560,14 @@ int ozaki2_plan_create(ozaki2_plan_t* out, int m, int n, int k, int num_moduli, 
   if (m <= 0 || n <= 0 || k <= 0) return OZ2_E_INVALID;
   ozaki2_plan_s* p = new (std::nothrow) ozaki2_plan_s();
   if (!p) return OZ2_E_NOMEM;
-  if (!make_const(num_moduli, p->c) || !make_dims(m, n, k, flags, p->d)) {
+  if (!make_const(num_moduli, p->c) || !make_dims(m, n, k, flags, p->d) ||
+      ((flags & OZ2_FUSED) && (flags & OZ2_KEEP_RESIDUES))) {
     delete p;
     return OZ2_E_INVALID;
+  }
+  if ((flags & OZ2_FUSED) && !fused_ok(p->d, p->c)) {
+    delete p;
+    return OZ2_E_UNSUPPORTED;
   }
   p->L = make_layout(p->d, p->c);
   if (!workspace || ws_bytes < p->L.total || ((uintptr_t)workspace & 255)) {
@@ -622,7 +647,9 @@ int ozaki2_residue_gemm(ozaki2_plan_t p, void* stream) {
   if (!p || p->stage < 1) return OZ2_E_INVALID;
   const hipStream_t s = (hipStream_t)stream;
   hipError_t e = mark(*p, 4, s);
-  if (e == hipSuccess) e = oz2_launch_resgemm(p->d, p->L, p->c, p->ws, s);
+  // a fused plan runs its residue GEMMs inside the reconstruction
+  if (e == hipSuccess && !(p->d.flags & OZ2_FUSED))
+    e = oz2_launch_resgemm(p->d, p->L, p->c, p->ws, s);
   if (e == hipSuccess) e = mark(*p, 5, s);
   int st = hip_status(e);
   if (st == OZ2_OK) p->stage = 2;
@@ -654,7 +681,10 @@ int ozaki2_dgemm_ex(int m, int n, int k, const double* A, int lda, const double*
     return hip_status(oz2_launch_fill(C, m, n, ldc, s));
   }
   ozaki2_plan_s p;
+  flags = route_flags(m, n, k, num_moduli, flags);
   if (!make_const(num_moduli, p.c) || !make_dims(m, n, k, flags, p.d)) return OZ2_E_INVALID;
+  if ((flags & OZ2_FUSED) && ((flags & OZ2_KEEP_RESIDUES) || !fused_ok(p.d, p.c)))
+    return (flags & OZ2_KEEP_RESIDUES) ? OZ2_E_INVALID : OZ2_E_UNSUPPORTED;
   p.L = make_layout(p.d, p.c);
   if (!workspace || ws_bytes < p.L.total || ((uintptr_t)workspace & 255)) return OZ2_E_WORKSPACE;
   p.ws = (uint8_t*)workspace;
@@ -664,8 +694,10 @@ int ozaki2_dgemm_ex(int m, int n, int k, const double* A, int lda, const double*
   p.ldb = ldb;
   st = run_deconstruct(p, OZ2_SIDE_A | OZ2_SIDE_B, s);
   if (st != OZ2_OK) return st;
-  st = hip_status(oz2_launch_resgemm(p.d, p.L, p.c, p.ws, s));
-  if (st != OZ2_OK) return st;
+  if (!(flags & OZ2_FUSED)) {
+    st = hip_status(oz2_launch_resgemm(p.d, p.L, p.c, p.ws, s));
+    if (st != OZ2_OK) return st;
+  }
   return run_reconstruct(p, C, ldc, s);
 }
 
@@ -675,7 +707,7 @@ int ozaki2_dgemm(int m, int n, int k, const double* A, int lda, const double* B,
   int st = check_mats(m, n, k, A, lda, B, ldb, C, ldc);
   if (st != OZ2_OK) return st;
   if (m == 0 || n == 0) return OZ2_OK;
-  size_t need = ozaki2_workspace_bytes(m, n, k, num_moduli, 0);
+  size_t need = ozaki2_workspace_bytes(m, n, k, num_moduli, route_flags(m, n, k, num_moduli, 0));
   if (need == 0) return OZ2_E_INVALID;
   st = device_ok();
   if (st != OZ2_OK) return st;
@@ -848,8 +880,9 @@ int ozaki2_plan_query(ozaki2_plan_t p, int what, void* host_out, size_t bytes) {
   if (!p || !host_out) return OZ2_E_INVALID;
   const size_t need = ozaki2_plan_query_bytes(p, what);
   if (need == 0 || bytes < need) return OZ2_E_INVALID;
-  const int needs_stage = (what == OZ2_Q_RESIDUES || what == OZ2_Q_INTEGERS) ? 2 : 1;
-  if (p->stage < needs_stage) return OZ2_E_INVALID;
+  const bool residues = what == OZ2_Q_RESIDUES || what == OZ2_Q_INTEGERS;
+  if (p->stage < (residues ? 2 : 1)) return OZ2_E_INVALID;
+  if (residues && (p->d.flags & OZ2_FUSED)) return OZ2_E_INVALID;   // never materialised
   if (hipDeviceSynchronize() != hipSuccess) return OZ2_E_DEVICE;
   const Oz2Dims& d = p->d;
   const Oz2Layout& L = p->L;

@@ -127,6 +127,11 @@ hipError_t oz2_launch_integers(const Oz2Dims& d, const Oz2Layout& L, const Oz2Co
 hipError_t oz2_launch_crt_probe(const Oz2Const& c, const int16_t* res, const int* e, int n,
                                 uint32_t* words, double* rounded, hipStream_t s);
 hipError_t oz2_launch_fill(double* C, int m, int n, int ldc, hipStream_t s);
+// residue GEMMs and reconstruction in one kernel (fused.hip): r <= 12 and
+// kp <= OZ2_KSLAB; mp, np multiples of 128 (they are of 256); C written
+// (C += with OZ2_ACCUMULATE) except flagged rows / columns
+hipError_t oz2_launch_fused(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, uint8_t* ws,
+                            double* C, int ldc, hipStream_t s);
 // the native fallback reading A directly (no gathered panel)
 hipError_t oz2_launch_fallback_direct(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws,
                                       const double* A, int lda, const double* B, int ldb,

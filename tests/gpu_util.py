@@ -40,18 +40,21 @@ def expected_bytes(vals):
     return enc(np.asarray(vals, dtype=np.int64))
 
 
-def fallback_ok(C, A, B, i, j):
+def fallback_ok(C, A, B, i, j, C_in=None):
     """A fallback entry: native FP64 within the dot-product error bound, or the
-    same IEEE class (NaN / signed Inf) as the oracle's reference."""
+    same IEEE class (NaN / signed Inf) as the oracle's reference.  With C_in
+    (C += A B) the entry is fl(C_in + native dot): one more rounding."""
     ref = oz2o.native_dot(A[i], B[:, j])
     got = C[i, j]
+    cin = 0.0 if C_in is None else float(C_in[i, j])
     if np.isnan(ref):
         return np.isnan(got)
     if np.isinf(ref):
         return got == ref
     k = A.shape[1]
     den = float(np.abs(A[i]) @ np.abs(B[:, j]))
-    return abs(got - ref) <= 1.01 * (k + 1) * 2.0 ** -53 * den + k * 2.0 ** -1074
+    return abs(got - (cin + ref)) <= (1.01 * (k + 1) * 2.0 ** -53 * den + k * 2.0 ** -1074
+                                      + 2.0 ** -53 * abs(got))
 
 
 def compare_all(plan, C, A, B, r, res, check_integers=True):
@@ -96,10 +99,10 @@ def compare_all(plan, C, A, B, r, res, check_integers=True):
     compare_C(C, A, B, res)
 
 
-def compare_C(C, A, B, res):
+def compare_C(C, A, B, res, C_in=None):
     fr = np.isin(res.rows, res.fallback_rows)
     fc = np.isin(res.cols, res.fallback_cols)
     emu = ~fr[:, None] & ~fc[None, :]
     assert np.array_equal(bits(C)[emu], bits(res.C)[emu]), "emulated entries differ"
     for ii, jj in zip(*np.nonzero(~emu)):
-        assert fallback_ok(C, A, B, res.rows[ii], res.cols[jj]), (ii, jj)
+        assert fallback_ok(C, A, B, res.rows[ii], res.cols[jj], C_in), (ii, jj)
