@@ -24,10 +24,12 @@ constexpr int PP = 80;   // bytes per plane row (64 + 16: spreads the LDS banks)
 constexpr int NTB = 512;
 
 struct Smem {
-  // the quantised A and B (row or column, k): a = h 2^32 + l, one int2 (h, l)
-  // per element, written once per problem and read for every modulus
-  int2 qa[64][64];
-  int2 qb[64][64];
+  // the quantised chunks of A and B: a = h 2^32 + l; elements j, j + 1 of
+  // thread t's chunk as one int4 (h_j, l_j, h_j+1, l_j+1) at [j / 2][t], so
+  // that a wave's 16-byte accesses are contiguous (no bank conflicts);
+  // written once per problem and read for every modulus
+  int4 qa[4][NTB];
+  int4 qb[4][NTB];
   uint8_t pa[3][64][PP];
   uint8_t pb[4][64][PP];     // B: d0, d1, d0 + d1 and, for nonsquare moduli, -16 d1
   unsigned long long rbits[64], cbits[64];
@@ -73,8 +75,10 @@ __device__ __forceinline__ v4f mfma(v8i a, v8i b, v4f c) {
 
 // Quantise (Eq. (scale)) the thread's chunk (8 consecutive k of one row,
 // already zero for T1 rows) once per problem: a = rint(x 2^s) = h 2^32 + l
-// with |h| <= 2^30 (|a| <= 2^62) and 0 <= l < 2^32, stored as (h, l) in LDS.
-__device__ __forceinline__ void quantise8(const double (&x)[8], int sc, bool& t2, int2* q) {
+// with |h| <= 2^30 (|a| <= 2^62) and 0 <= l < 2^32, stored as (h, l) in LDS
+// (q[j / 2][thread]).
+__device__ __forceinline__ void quantise8(const double (&x)[8], int sc, bool& t2,
+                                          int4 (*q)[NTB]) {
 #pragma unroll
   for (int j = 0; j < 8; j += 2) {
     int2 v[2];
@@ -85,7 +89,7 @@ __device__ __forceinline__ void quantise8(const double (&x)[8], int sc, bool& t2
       const double hd = floor(a * 0x1p-32);
       v[u] = make_int2((int)hd, (int)(uint32_t)fma(-hd, 0x1p32, a));
     }
-    *reinterpret_cast<int4*>(q + j) = make_int4(v[0].x, v[0].y, v[1].x, v[1].y);
+    q[j >> 1][threadIdx.x] = make_int4(v[0].x, v[0].y, v[1].x, v[1].y);
   }
 }
 
@@ -93,13 +97,14 @@ __device__ __forceinline__ void quantise8(const double (&x)[8], int sc, bool& t2
 // (FOUR: also the -16 d1 plane of a nonsquare modulus, for B)
 template <bool FOUR>
 __device__ __forceinline__ void split8(const Oz2Const& c, int i, const uint32_t* tab,
-                                       const int2* q, uint8_t (*pl)[64][PP], int row, int ch) {
+                                       const int4 (*q)[NTB], uint8_t (*pl)[64][PP], int row,
+                                       int ch) {
   const double m = (double)c.m[i], c32 = (double)c.c32[i], dinv = c.dinv[i];
   const int to = c.toff[i];
   uint32_t e[8];
 #pragma unroll
   for (int j = 0; j < 8; j += 2) {
-    const int4 hl = *reinterpret_cast<const int4*>(q + j);
+    const int4 hl = q[j >> 1][threadIdx.x];
     e[j] = tab[to + centred_residue((double)hl.x, (double)(uint32_t)hl.y, m, c32, dinv)];
     e[j + 1] = tab[to + centred_residue((double)hl.z, (double)(uint32_t)hl.w, m, c32, dinv)];
   }
@@ -407,8 +412,8 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
       xa[j] = t1a ? 0.0 : xa[j];
       xb[j] = t1b ? 0.0 : xb[j];
     }
-    quantise8(xa, S.sS[row], t2a, &S.qa[row][ch]);
-    quantise8(xb, S.sT[row], t2b, &S.qb[row][ch]);
+    quantise8(xa, S.sS[row], t2a, S.qa);
+    quantise8(xb, S.sT[row], t2b, S.qb);
     if constexpr (R <= 12) {
       // each modulus's residues go straight into the CRT sums (three
       // radix-2^38 limbs per output)
@@ -417,8 +422,8 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
       for (int I = 0; I < 8; ++I) S0[I] = S1[I] = S2[I] = 0.0;
 #pragma nounroll
       for (int i = 0; i < R; ++i) {
-        split8<false>(c, i, tab, &S.qa[row][ch], S.pa, row, ch);
-        split8<true>(c, i, tab, &S.qb[row][ch], S.pb, row, ch);
+        split8<false>(c, i, tab, S.qa, S.pa, row, ch);
+        split8<true>(c, i, tab, S.qb, S.pb, row, ch);
         __syncthreads();
         v4f acc[2];
         modulus_chain(c, i, S, rb0, cb0, acc);
@@ -434,8 +439,8 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
       uint4 res[R];
 #pragma nounroll
       for (int i = 0; i < R; ++i) {
-        split8<false>(c, i, tab, &S.qa[row][ch], S.pa, row, ch);
-        split8<true>(c, i, tab, &S.qb[row][ch], S.pb, row, ch);
+        split8<false>(c, i, tab, S.qa, S.pa, row, ch);
+        split8<true>(c, i, tab, S.qb, S.pb, row, ch);
         __syncthreads();
         put_res<R>(res, i, modulus_products(c, i, S, rb0, cb0));
         __syncthreads();

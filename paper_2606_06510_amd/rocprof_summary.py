@@ -7,6 +7,8 @@
     python -m paper_2606_06510_amd.rocprof_summary mfma COUNTER_CSV OUT_TXT SOURCE CMD [SKIP]
     python -m paper_2606_06510_amd.rocprof_summary hbm STATS_CSV FETCH_CSV WRITE_CSV OUT_MD \
         COPY_BYTES M N K R PSTORE CMD_TRACE CMD_FETCH CMD_WRITE [SKIP COUNT]
+    python -m paper_2606_06510_amd.rocprof_summary counters OUT_TXT KERNEL SOURCE SKIP UNITS \
+        CSV CMD [CSV CMD ...]
 
 ``stats`` turns a ``--kernel-trace --stats`` kernel_stats.csv into a markdown
 table.  ``trace`` does the same from the per-dispatch kernel_trace.csv, keeping
@@ -32,6 +34,15 @@ STATS_CSV, over dispatches SKIP .. SKIP+COUNT-1 as ``trace`` does.
 kernel trace, algorithmic bytes, the copy-scaled FETCH_SIZE + WRITE_SIZE
 bytes, and the achieved rate (algorithmic bytes / mean duration) against
 the 8 TB/s HBM peak.
+``counters`` gathers the SQ counters of KERNEL from one or more ``--pmc``
+passes (each a counter_collection.csv with the command that made it; every
+pass also collects GRBM_GUI_ACTIVE for the clock), leaves out the first SKIP
+dispatches of the kernel, and writes the mean per launch of each counter,
+per unit of work (UNITS per launch, e.g. problems of a batch), and the
+ratios that read directly against the chip: VALU instructions x 4 cycles
+(a wave64 VALU instruction occupies its SIMD's 16 lanes for 4 cycles) over
+the SIMD cycles, LDS bank-conflict cycles over the CU cycles, and the
+resident waves per SIMD (SQ_WAVE_CYCLES, counted in 4-cycle units).
 """
 from __future__ import annotations
 
@@ -224,6 +235,58 @@ def hbm(stats_csv, fetch_csv, write_csv, dst, copy_bytes, m, n, k, r, pstore, cm
                 f"{tot_a / tot_t / 1e12:.2f} TB/s | {100 * tot_a / tot_t / peak:.0f}% |\n")
 
 
+def counters(dst, kernel, source, skip, units, passes, xcds=8, cus=256, simds=1024):
+    vals = collections.defaultdict(list)
+    cyc, dur = [], []
+    for path, _ in passes:
+        per = collections.defaultdict(lambda: collections.defaultdict(float))
+        meta = {}
+        for r in csv.DictReader(open(path)):
+            if _short(r["Kernel_Name"]) != kernel:
+                continue
+            key = r["Dispatch_Id"]
+            per[key][r["Counter_Name"]] += float(r["Counter_Value"])
+            meta[key] = (int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
+        keys = [k for _, k in sorted((meta[k][0], k) for k in per)][skip:]
+        for key in keys:
+            for name, v in per[key].items():
+                if name == "GRBM_GUI_ACTIVE":
+                    cyc.append(v / xcds)
+                    dur.append((meta[key][1] - meta[key][0]) * 1e-9)
+                else:
+                    vals[name].append(v)
+    mean = {k: sum(v) / len(v) for k, v in vals.items()}
+    cycles = sum(cyc) / len(cyc)
+    d = sum(dur) / len(dur)
+    sha = hashlib.sha256(open(source, "rb").read()).hexdigest()
+    with open(dst, "w") as f:
+        f.write(f"# SQ counters of {kernel} per launch (mean over launches after the first {skip}"
+                f" of each pass)\n")
+        for _, cmd in passes:
+            f.write(f"command: {cmd}\n")
+        f.write(f"kernel_source: {source}\nkernel_source_sha256: {sha}\n")
+        f.write(f"launch_us: {d * 1e6:.1f}\ncycles_per_launch: {cycles:.0f}\n"
+                f"clock_ghz: {cycles / d / 1e9:.2f}\nunits_per_launch: {units}\n")
+        f.write("| counter | per launch | per unit |\n|---|---|---|\n")
+        for k in sorted(mean):
+            f.write(f"| {k} | {mean[k]:.4g} | {mean[k] / units:.4g} |\n")
+        simd_cycles = cycles * simds
+        if "SQ_INSTS_VALU" in mean:
+            f.write(f"valu_issue_share: {4 * mean['SQ_INSTS_VALU'] / simd_cycles:.3f}"
+                    "  (VALU instructions x 4 cycles / SIMD cycles)\n")
+        if "SQ_INSTS_LDS" in mean:
+            f.write(f"lds_insts_per_cu_cycle: {mean['SQ_INSTS_LDS'] / (cycles * cus):.3f}\n")
+        if "SQ_LDS_BANK_CONFLICT" in mean:
+            f.write(f"lds_bank_conflict_share: {mean['SQ_LDS_BANK_CONFLICT'] / (cycles * cus):.3f}"
+                    "  (bank-conflict cycles / CU cycles)\n")
+        if "SQ_WAVE_CYCLES" in mean:
+            f.write(f"waves_per_simd: {4 * mean['SQ_WAVE_CYCLES'] / simd_cycles:.2f}\n")
+        for k in ("SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_LDS", "SQ_WAIT_INST_LDS",
+                  "SQ_WAIT_INST_ANY", "SQ_WAIT_ANY", "SQ_ACTIVE_INST_ANY"):
+            if k in mean and "SQ_WAVE_CYCLES" in mean:
+                f.write(f"{k.lower()}_over_wave_cycles: {mean[k] / mean['SQ_WAVE_CYCLES']:.3f}\n")
+
+
 def main(argv):
     if argv[0] == "stats":
         stats(*argv[1:5])
@@ -236,6 +299,10 @@ def main(argv):
     elif argv[0] == "hbm":
         hbm(argv[1], argv[2], argv[3], argv[4], int(argv[5]), *map(int, argv[6:11]),
             argv[11], argv[12], argv[13], *(int(x) for x in argv[14:16]))
+    elif argv[0] == "counters":
+        rest = argv[6:]
+        counters(argv[1], argv[2], argv[3], int(argv[4]), int(argv[5]),
+                 [(rest[i], rest[i + 1]) for i in range(0, len(rest), 2)])
     else:
         raise SystemExit(__doc__)
 
