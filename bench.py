@@ -265,9 +265,10 @@ def main():
     mfma_pmc = pmc_mfma(ksrc, tag)
     pstore = plan_pstore(r)
     # algorithmic bytes: A, B read once, code bytes and planes written once;
-    # residues read and C written (C also read when accumulating)
+    # residues (12 bits per output and modulus) read and C written (C also
+    # read when accumulating)
     dec_bytes = (m * k + k * n) * (8 + 1 + pstore)
-    rec_bytes = m * n * (2 * r + 8 + (8 if flags & oz.OZ2_ACCUMULATE else 0))
+    rec_bytes = m * n * (1.5 * r + 8 + (8 if flags & oz.OZ2_ACCUMULATE else 0))
     out = {
         "metric": "effective FP64 TFLOPS of emulated DGEMM (Ozaki-II on FP8 MFMA)",
         "value": round(tflops, 3),

@@ -106,7 +106,7 @@ int ozaki2_dgemm_ex(int m, int n, int k, const double* A, int lda,
  * runs on until the process ends.  No hipMalloc, hipFree or other allocating
  * call is made (the first call on a device looks the array's address up once).
  * Products whose workspace (ozaki2_workspace_bytes(m, n, k, r, 0)) exceeds
- * the array -- e.g. beyond about 768^3 at r = 12 or 640^3 at r = 16 -- return
+ * the array -- e.g. beyond about 768^3 at r = 12 or 704^3 at r = 16 -- return
  * OZ2_E_WORKSPACE before any launch.  Every call on a GPU uses that GPU's one
  * array: calls that overlap in time on one GPU (different streams or host
  * threads without ordering) race and give undefined results; calls ordered on

@@ -61,10 +61,13 @@ int ozaki2_probe_copy_peak(size_t bytes, int reps, double* gbs);
  * 32-bit words above; one RN-even rounding) applied to n given residue
  * vectors, for tests that reach the rare branches -- integers next to +-M/2,
  * where the quotient estimate needs the exact range check -- which random
- * products almost never produce.  residues: int16 [num_moduli][n] (modulus i
- * in ascending order; any representative with |x| <= 577, the bound the
- * residue GEMMs guarantee; larger values give undefined results but no
- * out-of-bounds access), shifts: int [n]; words: uint32 [n][5] (the integer
+ * products almost never produce.  The residues go through the stored form
+ * the reconstruction reads (x + floor(m_i/2) + 32 in a 12-bit slot) exactly
+ * as the residue GEMMs write it.  residues: int16 [num_moduli][n] (modulus i
+ * in ascending order; any representative x with -(floor(m_i/2) + 32) <= x <=
+ * m_i/2 + 32, the range the residue GEMMs guarantee; other values give
+ * undefined results but no out-of-bounds access), shifts: int [n]; words:
+ * uint32 [n][5] (the integer
  * in [-M/2, M/2), two's complement, little endian), rounded: double [n]
  * (the integer times 2^-shift, rounded once).  Device pointers; asynchronous.
  * OZ2_E_INVALID for n < 0, num_moduli outside [8, 16] or a null pointer. */

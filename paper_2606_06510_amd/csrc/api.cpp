@@ -171,6 +171,18 @@ bool build_const(int r, Oz2Const& c) {
   // 114 bits, and with |x_i| <= 545 every limb sum stays below 2^52
   if (r <= 12 && M.bitlen() + 1 > 114) return false;
   c.mtop38 = std::ldexp(1.0, 76) / Md;
+  // the offsets of the stored residues, folded into the CRT sums
+  // (integer sums: W38 limbs < 2^38 and W words < 2^32, offsets <= 576)
+  for (int j = 0; j < 3; ++j) {
+    int64_t k = 0;
+    for (int i = 0; i < r; ++i) k += (int64_t)(ms[i] / 2 + 32) * (int64_t)c.W38[i][j];
+    c.K38[j] = (double)k;   // < 2^52: exact
+  }
+  for (int j = 0; j < OZ2_NLIMB; ++j) {
+    int64_t k = 0;
+    for (int i = 0; i < r; ++i) k += (int64_t)(ms[i] / 2 + 32) * (int64_t)c.W[i][j];
+    c.Kw[j] = (double)k;    // < 2^46: exact
+  }
   const int cc = (M.bitlen() - 1) + 6;     // floor(log2 M) + 6
   c.cA = cc / 2;
   c.cB = cc - c.cA;
@@ -239,7 +251,7 @@ Oz2Layout make_layout(const Oz2Dims& d, const Oz2Const& c) {
   // the fused route keeps the residues on chip, and its native fallback reads A
   // directly (no gathered panel)
   const bool fused = (d.flags & OZ2_FUSED) != 0;
-  L.res = fused ? 0 : take((size_t)c.r * d.mp * d.np * 2);
+  L.res = fused ? 0 : take((size_t)c.r * d.mp * d.np / 8 * 12);   // 12 bits per output
   L.panel = ((d.flags & OZ2_NO_FALLBACK) || fused)
                 ? 0 : take((size_t)std::min(d.mp, OZ2_FBCAP) * d.k * 8);
   L.total = o;
@@ -944,14 +956,16 @@ int ozaki2_plan_query(ozaki2_plan_t p, int what, void* host_out, size_t bytes) {
       return OZ2_OK;
     }
     case OZ2_Q_RESIDUES: {
-      // [tile][wave 8][x 4][y 2][lane 64][16] per modulus -> [r][n][m]
-      const size_t plane = (size_t)d.mp * d.np;
-      std::vector<int16_t> raw((size_t)p->c.r * plane);
-      if (!cp(raw.data(), ws + L.res, raw.size() * 2)) return OZ2_E_DEVICE;
+      // [tile][wave 8][x 4][y 2][lane 64][2 records of 3 words] per modulus,
+      // output 8h + e of a lane in slot e of record h, as x + floor(m/2) + 32
+      // -> the representative x itself, [r][n][m]
+      const size_t plane = (size_t)d.mp * d.np / 8 * 3;
+      std::vector<uint32_t> raw((size_t)p->c.r * plane);
+      if (!cp(raw.data(), ws + L.res, raw.size() * 4)) return OZ2_E_DEVICE;
       int16_t* o = (int16_t*)out;
       const int ntm = d.mp / OZ2_TILE;
       for (int i = 0; i < p->c.r; ++i)
-        for (size_t t = 0; t < plane / 16; ++t) {
+        for (size_t t = 0; t < (size_t)d.mp * d.np / 16; ++t) {
           const size_t tile = t >> 12;
           const int q = (int)(t & 4095), lane = q & 63, blk = q >> 6;
           const int y = blk & 1, x = (blk >> 1) & 3, w = blk >> 3;
@@ -959,11 +973,15 @@ int ozaki2_plan_query(ozaki2_plan_t p, int what, void* host_out, size_t bytes) {
           const int row = tm * OZ2_TILE + (w >> 2) * 128 + 32 * x + 4 * (lane >> 5);
           const int col = tn * OZ2_TILE + (w & 3) * 64 + 32 * y + (lane & 31);
           if (col >= d.n) continue;
+          const uint32_t* rec = raw.data() + (size_t)i * plane + t * 6;
           for (int e = 0; e < 16; ++e) {
             const int rr = row + 8 * (e >> 2) + (e & 3);
-            if (rr < d.m)   // the stored representative itself (|x| <= m_i/2 + 32)
-              o[((size_t)i * d.n + col) * d.m + rr] =
-                  raw[(size_t)i * plane + tile * (OZ2_TILE * OZ2_TILE) + (size_t)q * 16 + e];
+            if (rr >= d.m) continue;
+            const int bit = 96 * (e >> 3) + 12 * (e & 7);
+            const uint64_t two = (uint64_t)rec[bit >> 5] |
+                                 ((bit >> 5) + 1 < 6 ? (uint64_t)rec[(bit >> 5) + 1] << 32 : 0);
+            const int u = (int)((two >> (bit & 31)) & 0xFFFu);
+            o[((size_t)i * d.n + col) * d.m + rr] = (int16_t)(u - (p->c.m[i] / 2 + 32));
           }
         }
       return OZ2_OK;

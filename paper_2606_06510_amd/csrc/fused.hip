@@ -1,7 +1,7 @@
 // The residue GEMMs of Phase 2 and the reconstruction of Phase 3 in one
 // kernel, for r <= 12 moduli and k within one exact FP32 slab: the fused
 // reconstruction epilogue.  The staged path writes every output's r residues
-// to HBM (2r bytes per output) and reads them back in the reconstruction;
+// to HBM (1.5 r bytes per output) and reads them back in the reconstruction;
 // here a workgroup walks all r moduli of its 128 x 128 output tile, keeps
 // each output's residues packed in registers, and at the end forms the exact
 // CRT integer (the reconstruction's own routine), rounds it once with the

@@ -33,6 +33,7 @@ namespace {
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
 constexpr int TILE = OZ2_TILE;   // 256
@@ -376,7 +377,7 @@ __device__ __forceinline__ void chain_scale(v16f (&acc)[4][2], float f) {
 template <int CH>
 __global__ void __launch_bounds__(NT, 1)
 k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, int mp,
-          int np, int kp, int kbeg, int kend, int accumulate, int mpw, int16_t* __restrict__ res) {
+          int np, int kp, int kbeg, int kend, int accumulate, int mpw, uint32_t* __restrict__ res) {
   __shared__ __attribute__((aligned(16))) uint8_t LB[NB * STB];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)LB;
   const int ntm = mp / TILE, ntn = np / TILE;
@@ -439,17 +440,20 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
     // in fp32 throughout.  acc is an integer with |acc| <= 2^24 and fin is 1
     // or 16, so v = fin * acc is exact.  v * RN(1/m) is within
     // 2 * 2^-24 |v| / m <= 32 / m of v / m (the relative errors of RN(1/m)
-    // and of the product), so v - m rint(.) is an exact integer of magnitude
-    // <= m/2 + 32: stored as it is.  The reconstruction's exact CRT sum takes
-    // any representative of that size (its limb sums stay below 2^53 for
-    // |x| <= 1365), so the canonical centring (one more rounding per output)
-    // is left to the diagnostic residue query.  With a previous slab, the sum
-    // (|.| <= m + 64) is reduced once more: its quotient estimate is then
-    // within 2^-22 of the exact one, so the result lies in [-m/2, m/2].
+    // and of the product), so x = v - m rint(.) is an exact integer of
+    // magnitude <= m/2 + 32.  The reconstruction's exact CRT sum takes any
+    // representative of that size (the canonical centring is left to the
+    // diagnostic residue query).  With a previous slab, the sum (|.| <= m +
+    // 64) is reduced once more: its quotient estimate is then within 2^-22
+    // of the exact one, so the result lies in [-m/2, m/2].
+    // Stored: u = x + floor(m/2) + 32 (0 <= u <= m + 64 < 2^12) in 12-bit
+    // slots, the lane's 16 outputs of a 32x32 block as two 96-bit records
+    // (outputs 8h .. 8h+7 in record h, output 8h + e at bits 12 e).
     const float ffin = (float)c.fin[mi];
-    int16_t* dst = res + (size_t)mi * mp * np + (size_t)tile * (TILE * TILE) + (size_t)w * 8192 +
-                   lane * 16;
-    uint32_t pk[4][2][8];
+    const int offi = m / 2 + 32;
+    uint32_t* dst = res + ((size_t)mi * mp * np + (size_t)tile * (TILE * TILE) +
+                           (size_t)w * 8192) / 8 * 3 + lane * 6;
+    uint32_t pk[4][2][6];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -461,20 +465,29 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
           r16[e] = __builtin_fmaf(-rintf(v * inv), fm, v);
         }
         if (accumulate) {
-          const uint4* p = reinterpret_cast<const uint4*>(dst + (i * 2 + j) * 1024);
-          const uint4 o0 = p[0], o1 = p[1];
-          const uint32_t ow[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
+          const uint2* p = reinterpret_cast<const uint2*>(dst + (i * 2 + j) * 384);
+          const uint2 o0 = p[0], o1 = p[1], o2 = p[2];
+          const uint32_t ow[7] = {o0.x, o0.y, o1.x, o1.y, o2.x, o2.y, 0u};
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
-            const int old = (int)(int16_t)((ow[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
-            const float t = r16[e] + (float)old;
+            // slot e % 8 of record e / 8 (words 3 (e / 8) ..)
+            const int bit = 96 * (e >> 3) + 12 * (e & 7), wi = bit >> 5, sh = bit & 31;
+            const uint32_t u = (sh + 12 <= 32 ? (ow[wi] >> sh)
+                                              : __builtin_amdgcn_alignbit(ow[wi + 1], ow[wi], sh)) &
+                               0xFFFu;
+            const float t = r16[e] + (float)((int)u - offi);
             r16[e] = __builtin_fmaf(-rintf(t * inv), fm, t);
           }
         }
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          pk[i][j][e] = __builtin_bit_cast(
-              uint32_t, __builtin_amdgcn_cvt_pk_i16((int)r16[2 * e], (int)r16[2 * e + 1]));
+        for (int h = 0; h < 2; ++h) {
+          uint32_t u[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) u[e] = (uint32_t)((int)r16[8 * h + e] + offi);
+          pk[i][j][3 * h] = u[0] | (u[1] << 12) | (u[2] << 24);
+          pk[i][j][3 * h + 1] = (u[2] >> 8) | (u[3] << 4) | (u[4] << 16) | (u[5] << 28);
+          pk[i][j][3 * h + 2] = (u[5] >> 4) | (u[6] << 8) | (u[7] << 20);
+        }
       }
     // Every DMA issued so far (the next modulus's first stages, up to three)
     // has landed before the stores go out; those stages then skip their wait,
@@ -487,9 +500,10 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        u32x4* p = reinterpret_cast<u32x4*>(dst + (i * 2 + j) * 1024);
-        __builtin_nontemporal_store(u32x4{pk[i][j][0], pk[i][j][1], pk[i][j][2], pk[i][j][3]}, p);
-        __builtin_nontemporal_store(u32x4{pk[i][j][4], pk[i][j][5], pk[i][j][6], pk[i][j][7]}, p + 1);
+        u32x2* p = reinterpret_cast<u32x2*>(dst + (i * 2 + j) * 384);
+#pragma unroll
+        for (int q = 0; q < 3; ++q)
+          __builtin_nontemporal_store(u32x2{pk[i][j][2 * q], pk[i][j][2 * q + 1]}, p + q);
       }
   }
   if (!g) bar();
@@ -533,10 +547,10 @@ hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Con
     }
     const int ch = (sq_cheap ? 1 : 0) | (ns_cheap ? 2 : 0);
     void (*kern)(Oz2Const, const uint8_t*, const uint8_t*, int, int, int, int, int, int, int,
-                 int16_t*) = ch == 3 ? k_resgemm<3> : ch == 2 ? k_resgemm<2>
+                 uint32_t*) = ch == 3 ? k_resgemm<3> : ch == 2 ? k_resgemm<2>
                                                     : ch == 1 ? k_resgemm<1> : k_resgemm<0>;
     hipLaunchKernelGGL(kern, grid, dim3(NT), 0, s, c, ws + L.planesA, ws + L.planesB, d.mp, d.np,
-                       d.kp, kb, ke, sl > 0 ? 1 : 0, mpw, (int16_t*)(ws + L.res));
+                       d.kp, kb, ke, sl > 0 ? 1 : 0, mpw, (uint32_t*)(ws + L.res));
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

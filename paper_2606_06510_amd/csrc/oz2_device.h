@@ -92,13 +92,31 @@ __device__ __forceinline__ void normalise(double (&S)[NW]) {
   }
 }
 
-// Exact integer of output I of a thread from its R residues (any
-// representatives of magnitude <= 577):
-// NW words, two's complement, little endian.
+// The staged residue format: 8 outputs of a thread per modulus in a 96-bit
+// record of three 32-bit words, output I in bits 12 I .. 12 I + 11, as
+// u = x + floor(m/2) + 32 (0 <= u <= m + 64 < 2^12 for |x| <= m/2 + 32).
+template <int I>
+__device__ __forceinline__ uint32_t slot_bits(const uint3& v) {
+  constexpr int b = 12 * I, wi = b >> 5, sh = b & 31;
+  const uint32_t lo = wi == 0 ? v.x : (wi == 1 ? v.y : v.z);
+  if constexpr (sh + 12 <= 32) {
+    return (lo >> sh) & 0xFFFu;
+  } else {
+    const uint32_t hi = wi == 0 ? v.y : v.z;
+    return __builtin_amdgcn_alignbit(hi, lo, sh) & 0xFFFu;
+  }
+}
+template <int I>
+__device__ __forceinline__ double slot_at(const uint3& v) {
+  return (double)slot_bits<I>(v);
+}
+
+// The sums S_j = sum_i x_i W_i[j] of the direct CRT sum, from int16
+// representatives (|x_i| <= 577) or from stored records (S_j starts at
+// -sum_i (floor(m_i/2) + 32) W_i[j] and adds u_i W_i[j]: the same integers,
+// exact at every step, every partial sum below 2^47).
 template <int R, int NW, int I>
-__device__ __forceinline__ void crt_words(const Oz2Const& c, const uint4 (&x)[R],
-                                          uint32_t (&w)[NW]) {
-  double S[NW];
+__device__ __forceinline__ void crt_sums(const Oz2Const& c, const uint4 (&x)[R], double (&S)[NW]) {
 #pragma unroll
   for (int j = 0; j < NW; ++j) S[j] = 0.0;
 #pragma unroll
@@ -107,6 +125,26 @@ __device__ __forceinline__ void crt_words(const Oz2Const& c, const uint4 (&x)[R]
 #pragma unroll
     for (int j = 0; j < NW; ++j) S[j] = fma(xi, c.W[i][j], S[j]);
   }
+}
+template <int R, int NW, int I>
+__device__ __forceinline__ void crt_sums(const Oz2Const& c, const uint3 (&x)[R], double (&S)[NW]) {
+#pragma unroll
+  for (int j = 0; j < NW; ++j) S[j] = -c.Kw[j];
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const double ui = slot_at<I>(x[i]);
+#pragma unroll
+    for (int j = 0; j < NW; ++j) S[j] = fma(ui, c.W[i][j], S[j]);
+  }
+}
+
+// Exact integer of output I of a thread from its R residues (int16
+// representatives of magnitude <= 577, or stored records):
+// NW words, two's complement, little endian.
+template <int R, int NW, int I, class X>
+__device__ __forceinline__ void crt_words(const Oz2Const& c, const X (&x)[R], uint32_t (&w)[NW]) {
+  double S[NW];
+  crt_sums<R, NW, I>(c, x, S);
   // quotient estimate q = rint(X / M) from the three top (unnormalised)
   // limbs: |S_j| < 2^46, |X/M| <= sum |x_i| < 2^14, so the estimate of X/M
   // is within 2^-36 of the true value; only within that of +-1/2 can q be
@@ -323,18 +361,23 @@ __device__ __forceinline__ void crt38_fix(const Oz2Const& c, double& S0, double&
 // ambiguous.  (The reconstruction rounds these limbs; the integer query of
 // the staged API exports them.)
 template <int R>
-__device__ __forceinline__ void crt38_sum(const Oz2Const& c, const double (&xi)[R], double& S0,
+__device__ __forceinline__ void crt38_acc(const Oz2Const& c, const double (&xi)[R], double& S0,
                                           double& S1, double& S2) {
   static_assert(R <= 12, "three radix-2^38 limbs hold [-M/2, M/2) only for r <= 12");
-  S0 = 0.0;
-  S1 = 0.0;
-  S2 = 0.0;
 #pragma unroll
   for (int i = 0; i < R; ++i) {
     S0 = fma(xi[i], c.W38[i][0], S0);
     S1 = fma(xi[i], c.W38[i][1], S1);
     S2 = fma(xi[i], c.W38[i][2], S2);
   }
+}
+template <int R>
+__device__ __forceinline__ void crt38_sum(const Oz2Const& c, const double (&xi)[R], double& S0,
+                                          double& S1, double& S2) {
+  S0 = 0.0;
+  S1 = 0.0;
+  S2 = 0.0;
+  crt38_acc<R>(c, xi, S0, S1, S2);
   if (crt38_reduce(c, S0, S1, S2)) crt38_fix(c, S0, S1, S2);
 }
 
@@ -346,9 +389,24 @@ __device__ __forceinline__ void crt38_limbs(const Oz2Const& c, const uint4 (&x)[
   for (int i = 0; i < R; ++i) xi[i] = res_at<I>(x[i]);
   crt38_sum<R>(c, xi, S0, S1, S2);
 }
-
+// from stored records: the limb sums start at -K38 (the offsets' share) and
+// add u_i W38[i]: the same exact integers as from the representatives
+// (partial sums below 2^52)
 template <int R, int I>
-__device__ __forceinline__ double crt38_rounded(const Oz2Const& c, const uint4 (&x)[R], int e) {
+__device__ __forceinline__ void crt38_limbs(const Oz2Const& c, const uint3 (&x)[R], double& S0,
+                                            double& S1, double& S2) {
+  double ui[R];
+#pragma unroll
+  for (int i = 0; i < R; ++i) ui[i] = slot_at<I>(x[i]);
+  S0 = -c.K38[0];
+  S1 = -c.K38[1];
+  S2 = -c.K38[2];
+  crt38_acc<R>(c, ui, S0, S1, S2);
+  if (crt38_reduce(c, S0, S1, S2)) crt38_fix(c, S0, S1, S2);
+}
+
+template <int R, int I, class X>
+__device__ __forceinline__ double crt38_rounded(const Oz2Const& c, const X (&x)[R], int e) {
   double S0, S1, S2;
   crt38_limbs<R, I>(c, x, S0, S1, S2);
   return round38(S0, S1, S2, e);

@@ -43,6 +43,10 @@ struct Oz2Const {
   double W38[OZ2_MAXR][3];
   double M38[3], Mhalf38[3];
   double mtop38;                  // 2^76 / M, rounded
+  // the staged residues are stored as u_i = x_i + floor(m_i/2) + 32 >= 0:
+  // sum_i u_i W_i limb by limb minus these gives sum_i x_i W_i exactly
+  double K38[3];                  // sum_i (floor(m_i/2) + 32) W38[i][l] (exact: < 2^51)
+  double Kw[OZ2_NLIMB];           // sum_i (floor(m_i/2) + 32) W[i][j] (exact: < 2^46)
   int cA, cB;                     // width budgets of the scaling rule
   // residue -> plane-bytes tables: entry toff[i] + d for the centred residue d
   int toff[OZ2_MAXR];             // (sum of the earlier moduli) + floor(m_i/2)
@@ -71,8 +75,10 @@ struct Oz2Layout {
   size_t etA, etB;            // int16 [kp/64][mp] / [kp/64][np]: exponents of the tile-row maxima
   size_t planesA, planesB;    // uint8 [P][kp/64][mp][64] / [P][kp/64][np][64] (K-blocked)
   size_t tabs;                // uint32 [tabsz]: E4M3 plane bytes of every centred residue
-  size_t res;                 // int16 [r][tile][wave 8][x 4][y 2][lane 64][16]: per modulus a
-                              //   representative of C~ mod m_i of magnitude <= m_i/2 + 32
+  size_t res;                 // uint32 [r][tile][wave 8][x 4][y 2][lane 64][2][3]: per modulus
+                              //   a representative x of C~ mod m_i with |x| <= m_i/2 + 32,
+                              //   stored as x + floor(m_i/2) + 32 in a 12-bit slot; the 16
+                              //   outputs of a lane as two 96-bit records of 8 slots
                               //   (the GEMM's accumulator order, see gemm.hip)
   size_t counters;            // int32 [4]: fallback row / column counts
   size_t listA, listB;        // int32 [mp] / [np]: flagged row / column indices

@@ -14,7 +14,10 @@
 // x_i are any representatives of the residues with |x_i| <= m_i/2 + 32 <= 577
 // (what the residue GEMM stores): every partial word sum is then an integer
 // below 2^46 (32-bit words) or 2^51 (radix-2^38 limbs), and the quotient
-// estimate is as good for them as for centred residues.
+// estimate is as good for them as for centred residues.  The residue GEMMs
+// store them offset (u = x + floor(m/2) + 32, 12 bits per output): the sums
+// start at minus the offsets' share and add the u_i, which gives the same
+// integers.
 // The limbs are normalised to five 32-bit words (two's complement), and
 // rounded once to binary64 with the exponent shift -(s_i + t_j), including
 // gradual underflow and overflow.
@@ -24,13 +27,13 @@ namespace {
 
 // Thread mapping shared by the reconstruction kernels.  The residue GEMM
 // leaves, per modulus, each 32x32 output block (wave w of a 256x256 tile,
-// sub-block x, y) as 1024 int16 in its accumulator order: lane L holds 16
-// outputs of column L%32, rows 4(L/32) + 8(e/4) + e%4, e = 0..15.  Here two
-// threads share a lane's 16 (t = 2L + h takes e = 8h..8h+7), so the 128
-// threads of a block read 2 KiB contiguous per modulus; a workgroup of 256
-// takes two blocks.
+// sub-block x, y) as 1024 12-bit slots in its accumulator order: lane L holds
+// 16 outputs of column L%32, rows 4(L/32) + 8(e/4) + e%4, e = 0..15, as two
+// 96-bit records (e = 0..7, e = 8..15).  Here two threads share a lane's 16
+// (t = 2L + h takes record h), so the 128 threads of a block read 1.5 KiB
+// contiguous per modulus; a workgroup of 256 takes two blocks.
 struct BlockMap {
-  size_t roff;      // int16 offset of the thread's 8 residues in a modulus plane
+  size_t roff;      // word offset of the thread's record in a modulus plane
   int row0, col0;   // block origin in C
   int cl;           // column within the block
   int rb;           // row within the block of output i: rb + 8(i/4) + i%4
@@ -53,22 +56,23 @@ __device__ __forceinline__ BlockMap block_map(int mp) {
   const int lane = b.tt >> 1, h = b.tt & 1;
   b.cl = lane & 31;
   b.rb = 4 * (lane >> 5) + 16 * h;
-  b.roff = tile * (OZ2_TILE * OZ2_TILE) + (size_t)blk * 1024 + (size_t)b.tt * 8;
+  b.roff = tile * (OZ2_TILE * OZ2_TILE / 8 * 3) + (size_t)blk * 384 + (size_t)b.tt * 3;
   return b;
 }
 
+// the thread's record of each modulus (plane: words per modulus)
 template <int R>
-__device__ __forceinline__ void load_residues(const int16_t* __restrict__ res, size_t plane,
-                                              size_t roff, uint4 (&x)[R]) {
+__device__ __forceinline__ void load_residues(const uint32_t* __restrict__ res, size_t plane,
+                                              size_t roff, uint3 (&x)[R]) {
 #pragma unroll
   for (int i = 0; i < R; ++i)
-    x[i] = *reinterpret_cast<const uint4*>(res + (size_t)i * plane + roff);
+    x[i] = *reinterpret_cast<const uint3*>(res + (size_t)i * plane + roff);
 }
 
 template <int R, int I>
 struct Outputs {
   __device__ __forceinline__ static void run(const Oz2Const& c, const Oz2Dims& d,
-                                             const uint4 (&x)[R], const BlockMap& b, int tj,
+                                             const uint3 (&x)[R], const BlockMap& b, int tj,
                                              const int32_t* __restrict__ sA, double (*tr)[33]) {
     constexpr int NW = NWords<R>::value;
     const int rr = b.rb + 8 * (I >> 2) + (I & 3);
@@ -86,7 +90,7 @@ struct Outputs {
 };
 template <int R>
 struct Outputs<R, 8> {
-  __device__ __forceinline__ static void run(const Oz2Const&, const Oz2Dims&, const uint4 (&)[R],
+  __device__ __forceinline__ static void run(const Oz2Const&, const Oz2Dims&, const uint3 (&)[R],
                                              const BlockMap&, int, const int32_t* __restrict__,
                                              double (*)[33]) {}
 };
@@ -100,7 +104,7 @@ struct Outputs<R, 8> {
 // without flagged rows).
 template <int R>
 __global__ void __launch_bounds__(256)
-k_reconstruct(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res,
+k_reconstruct(Oz2Const c, Oz2Dims d, const uint32_t* __restrict__ res,
               const int32_t* __restrict__ sA, const int32_t* __restrict__ tB,
               const uint32_t* __restrict__ fA, const uint32_t* __restrict__ fB, double* C, int ldc,
               const double* __restrict__ A, int lda, const int* __restrict__ counters,
@@ -109,8 +113,8 @@ k_reconstruct(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res,
   const int nflag = panel ? counters[0] : 0;   // used at the end; loaded early
   const BlockMap b = block_map(d.mp);
   {
-    uint4 x[R];
-    load_residues<R>(res, (size_t)d.mp * d.np, b.roff, x);
+    uint3 x[R];
+    load_residues<R>(res, (size_t)d.mp * d.np / 8 * 3, b.roff, x);
     const int col = b.col0 + b.cl;
     const int tj = col < d.n ? tB[col] : 0;
     Outputs<R, 0>::run(c, d, x, b, tj, sA, tr[b.hb]);
@@ -146,8 +150,8 @@ k_reconstruct(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res,
 // The exact integer of output I of a thread as NL 32-bit words (two's
 // complement, little endian), formed by the routine the reconstruction
 // itself uses: radix-2^38 limbs for R <= 12, 32-bit words above.
-template <int R, int I>
-__device__ __forceinline__ void store_integer(const Oz2Const& c, const uint4 (&x)[R], uint32_t* o) {
+template <int R, int I, class X>
+__device__ __forceinline__ void store_integer(const Oz2Const& c, const X (&x)[R], uint32_t* o) {
   constexpr int NW = R <= 12 ? 4 : NWords<R>::value;
   uint32_t w[NW];
   if constexpr (R <= 12) {
@@ -163,8 +167,8 @@ __device__ __forceinline__ void store_integer(const Oz2Const& c, const uint4 (&x
 }
 
 // The rounded value of output I exactly as the reconstruction forms it.
-template <int R, int I>
-__device__ __forceinline__ double rounded_value(const Oz2Const& c, const uint4 (&x)[R], int e) {
+template <int R, int I, class X>
+__device__ __forceinline__ double rounded_value(const Oz2Const& c, const X (&x)[R], int e) {
   if constexpr (R <= 12) {
     return crt38_rounded<R, I>(c, x, e);
   } else {
@@ -178,7 +182,7 @@ __device__ __forceinline__ double rounded_value(const Oz2Const& c, const uint4 (
 template <int R, int I>
 struct IntOut {
   __device__ __forceinline__ static void run(const Oz2Const& c, const Oz2Dims& d,
-                                             const uint4 (&x)[R], const BlockMap& b,
+                                             const uint3 (&x)[R], const BlockMap& b,
                                              uint32_t* out) {
     constexpr int NW = NWords<R>::value;
     const int row = b.row0 + b.rb + 8 * (I >> 2) + (I & 3);
@@ -192,33 +196,37 @@ struct IntOut {
 };
 template <int R>
 struct IntOut<R, 8> {
-  __device__ __forceinline__ static void run(const Oz2Const&, const Oz2Dims&, const uint4 (&)[R],
+  __device__ __forceinline__ static void run(const Oz2Const&, const Oz2Dims&, const uint3 (&)[R],
                                              const BlockMap&, uint32_t*) {}
 };
 
 // the exact integers themselves, [n][m][5] words (a diagnostic query)
 template <int R>
 __global__ void __launch_bounds__(256)
-k_integers(Oz2Const c, Oz2Dims d, const int16_t* __restrict__ res, uint32_t* out) {
+k_integers(Oz2Const c, Oz2Dims d, const uint32_t* __restrict__ res, uint32_t* out) {
   const BlockMap b = block_map(d.mp);
-  uint4 x[R];
-  load_residues<R>(res, (size_t)d.mp * d.np, b.roff, x);
+  uint3 x[R];
+  load_residues<R>(res, (size_t)d.mp * d.np / 8 * 3, b.roff, x);
   IntOut<R, 0>::run(c, d, x, b, out);
 }
 
 // The reconstruction's integer and rounding routines on given residues (a
 // probe): thread t takes residue t of each modulus (res[i n + t], any
-// representative with |x| <= 577) and writes the exact integer as 5 words and
-// its value rounded with the shift e[t].
+// representative x with -(floor(m/2) + 32) <= x <= m/2 + 32, what the residue
+// GEMMs store), puts it into a stored record as the residue GEMMs do, and
+// writes the exact integer as 5 words and its value rounded with the shift e[t].
 template <int R>
 __global__ void __launch_bounds__(256)
 k_crt_probe(Oz2Const c, const int16_t* __restrict__ res, const int* __restrict__ e, int n,
             uint32_t* __restrict__ words, double* __restrict__ rounded) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= n) return;
-  uint4 x[R];
+  uint3 x[R];
 #pragma unroll
-  for (int i = 0; i < R; ++i) x[i] = make_uint4((uint32_t)(uint16_t)res[(size_t)i * n + t], 0u, 0u, 0u);
+  for (int i = 0; i < R; ++i) {
+    const int u = (int)res[(size_t)i * n + t] + c.m[i] / 2 + 32;   // slot 0 of the record
+    x[i] = make_uint3((uint32_t)u & 0xFFFu, 0u, 0u);
+  }
   store_integer<R, 0>(c, x, words + (size_t)t * NL);
   rounded[t] = rounded_value<R, 0>(c, x, e[t]);
 }
@@ -356,7 +364,7 @@ void launch_reconstruct_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& 
   const size_t blocks = (size_t)d.mp * d.np / 2048;
   const bool gather = !(d.flags & 8u);   // OZ2_NO_FALLBACK: no fallback, no panel
   hipLaunchKernelGGL(k_reconstruct<R>, dim3((unsigned)blocks), dim3(256), 0, s, c, d,
-                     (const int16_t*)(ws + L.res), (const int32_t*)(ws + L.sA),
+                     (const uint32_t*)(ws + L.res), (const int32_t*)(ws + L.sA),
                      (const int32_t*)(ws + L.tB), (const uint32_t*)(ws + L.flagsA),
                      (const uint32_t*)(ws + L.flagsB), C, ldc, A, lda,
                      (const int*)(ws + L.counters), (const int*)(ws + L.listA),
@@ -368,7 +376,7 @@ void launch_integers_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c, 
                        uint32_t* out, hipStream_t s) {
   const size_t blocks = (size_t)d.mp * d.np / 2048;
   hipLaunchKernelGGL(k_integers<R>, dim3((unsigned)blocks), dim3(256), 0, s, c, d,
-                     (const int16_t*)(ws + L.res), out);
+                     (const uint32_t*)(ws + L.res), out);
 }
 
 template <int R>

@@ -182,7 +182,7 @@ def _algorithmic(m, n, k, r, pstore):
         "k_scan_codes_cols": 9 * eb,
         "k_rebase": 2 * (ea + eb),                # code bytes read and rewritten in place
         "k_split": (8 + pstore) * (ea + eb),      # operand read, plane bytes written
-        f"void k_reconstruct<{r}>": (2 * r + 8) * m * n,   # int16 residues read, FP64 written
+        f"void k_reconstruct<{r}>": 3 * r * m * n // 2 + 8 * m * n,   # 12-bit residues read, FP64 written
     }
 
 

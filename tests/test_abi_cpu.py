@@ -76,10 +76,18 @@ def test_moduli_table():
 
 
 def test_workspace_bytes():
-    # planes 30 B per padded element of A and B, residues 24 B per padded output
+    # planes 30 B per padded element of A and B, residues 12 bits per padded
+    # output and modulus (18 B at r = 12)
     b = oz.ozaki2_workspace_bytes(4096, 4096, 4096, 12)
-    assert b >= 30 * 2 * 4096 * 4096 + 24 * 4096 * 4096
-    assert b < 1.05 * (31 * 2 * 4096 * 4096 + 24 * 4096 * 4096) + (1 << 20)
+    assert b >= 30 * 2 * 4096 * 4096 + 18 * 4096 * 4096
+    assert b < 1.05 * (31 * 2 * 4096 * 4096 + 18 * 4096 * 4096) + (1 << 20)
+    # the fused route keeps no residues (nor a fallback panel: compared
+    # without one): 1.5 r B per padded output less
+    mp = np_ = 512
+    nf = oz.OZ2_NO_FALLBACK
+    assert oz.ozaki2_workspace_bytes(300, 400, 500, 12, nf) - \
+        oz.ozaki2_workspace_bytes(300, 400, 500, 12, nf | oz.OZ2_FUSED) in \
+        range(18 * mp * np_, 18 * mp * np_ + 256 * 4)
     # the native fallback's panel of gathered rows: min(mp, 1024) x k doubles,
     # absent with OZ2_NO_FALLBACK
     for m, k in [(4096, 4096), (300, 200), (32768, 256)]:
