@@ -6,7 +6,7 @@
         KERNEL COPY_BYTES SOURCE CMD_FETCH CMD_WRITE
     python -m paper_2606_06510_amd.rocprof_summary mfma COUNTER_CSV OUT_TXT SOURCE CMD [SKIP]
     python -m paper_2606_06510_amd.rocprof_summary hbm STATS_CSV FETCH_CSV WRITE_CSV OUT_MD \
-        COPY_BYTES M N K R PSTORE CMD_TRACE CMD_FETCH CMD_WRITE [SKIP COUNT]
+        COPY_BYTES M N K R PSTORE CMD_TRACE CMD_FETCH CMD_WRITE [SKIP COUNT [ACC]]
     python -m paper_2606_06510_amd.rocprof_summary counters OUT_TXT KERNEL SOURCE SKIP UNITS \
         CSV CMD [CSV CMD ...]
 
@@ -173,16 +173,17 @@ def mfma(src, dst, source, cmd, skip=0, xcds=8, simds=1024):
                     f"{100 * sum(x[2] for x in xs) / n:.1f}% | {sum(x[3] for x in xs) / n / 1e9:.2f} |\n")
 
 
-def _algorithmic(m, n, k, r, pstore):
+def _algorithmic(m, n, k, r, pstore, acc=False):
     """Algorithmic bytes per launch of the memory-bound kernels: each operand
-    read once per pass, each code, plane, residue and output written once."""
+    read once per pass, each code, plane, residue and output written once
+    (and C read once more when accumulating)."""
     ea, eb = m * k, k * n
     return {
         "k_scan_codes_rows": 9 * ea,              # A read (8 B), code byte written (1 B)
         "k_scan_codes_cols": 9 * eb,
         "k_rebase": 2 * (ea + eb),                # code bytes read and rewritten in place
         "k_split": (8 + pstore) * (ea + eb),      # operand read, plane bytes written
-        f"void k_reconstruct<{r}>": 3 * r * m * n // 2 + 8 * m * n,   # 12-bit residues read, FP64 written
+        f"void k_reconstruct<{r}>": 3 * r * m * n // 2 + (16 if acc else 8) * m * n,  # 12-bit residues read, FP64 written
     }
 
 
@@ -199,7 +200,7 @@ def _trace_avg(path, skip, count):
 
 
 def hbm(stats_csv, fetch_csv, write_csv, dst, copy_bytes, m, n, k, r, pstore, cmd_t, cmd_f, cmd_w,
-        skip=None, count=None, peak=8.0e12):
+        skip=None, count=None, acc=False, peak=8.0e12):
     if skip is None:
         avg = {_short(x["Name"]): float(x["AverageNs"]) * 1e-9
                for x in csv.DictReader(open(stats_csv))}
@@ -210,7 +211,7 @@ def hbm(stats_csv, fetch_csv, write_csv, dst, copy_bytes, m, n, k, r, pstore, cm
     copy = next(x for x in fetch if x.startswith("k_copy"))
     sf = copy_bytes / (fetch[copy] * 1024.0)
     sw = copy_bytes / (write[copy] * 1024.0)
-    alg = _algorithmic(m, n, k, r, pstore)
+    alg = _algorithmic(m, n, k, r, pstore, acc)
     with open(dst, "w") as f:
         f.write(f"# Memory-bound kernels of the emulated DGEMM {m}x{n}x{k}, r = {r}: achieved HBM "
                 f"rate against the {peak / 1e12:.0f} TB/s peak\n\n")
@@ -298,7 +299,8 @@ def main(argv):
         mfma(*argv[1:5], *(int(x) for x in argv[5:6]))
     elif argv[0] == "hbm":
         hbm(argv[1], argv[2], argv[3], argv[4], int(argv[5]), *map(int, argv[6:11]),
-            argv[11], argv[12], argv[13], *(int(x) for x in argv[14:16]))
+            argv[11], argv[12], argv[13], *(int(x) for x in argv[14:16]),
+            *(bool(int(x)) for x in argv[16:17]))
     elif argv[0] == "counters":
         rest = argv[6:]
         counters(argv[1], argv[2], argv[3], int(argv[4]), int(argv[5]),
