@@ -101,8 +101,9 @@ struct Outputs<R, 8> {
 // follows on the same stream; for it the grid also gathers the first `cap`
 // flagged rows of A into a contiguous panel (row r at panel[r + l cap]), read
 // once here instead of once per column tile there (nothing to do on inputs
-// without flagged rows).
-template <int R>
+// without flagged rows).  ACC (OZ2_ACCUMULATE): C_in is loaded before the
+// CRT work, so that its latency hides behind it.
+template <int R, bool ACC>
 __global__ void __launch_bounds__(256)
 k_reconstruct(Oz2Const c, Oz2Dims d, const uint32_t* __restrict__ res,
               const int32_t* __restrict__ sA, const int32_t* __restrict__ tB,
@@ -112,6 +113,17 @@ k_reconstruct(Oz2Const c, Oz2Dims d, const uint32_t* __restrict__ res,
   __shared__ double tr[2][32][33];
   const int nflag = panel ? counters[0] : 0;   // used at the end; loaded early
   const BlockMap b = block_map(d.mp);
+  const int rr = b.tt & 31;
+  const int row = b.row0 + rr;
+  // the thread's outputs in the store phase: row, columns col0 + 4 j + tt/32
+  double cin[8];
+  if constexpr (ACC) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int col = b.col0 + j * 4 + (b.tt >> 5);
+      cin[j] = (row < d.m && col < d.n) ? C[(size_t)col * ldc + row] : 0.0;
+    }
+  }
   {
     uint3 x[R];
     load_residues<R>(res, (size_t)d.mp * d.np / 8 * 3, b.roff, x);
@@ -120,20 +132,16 @@ k_reconstruct(Oz2Const c, Oz2Dims d, const uint32_t* __restrict__ res,
     Outputs<R, 0>::run(c, d, x, b, tj, sA, tr[b.hb]);
   }
   __syncthreads();
-  const bool acc = (d.flags & 1u) != 0;        // OZ2_ACCUMULATE
   const bool nofb = (d.flags & 8u) != 0;       // OZ2_NO_FALLBACK
   const bool force = (d.flags & 16u) != 0;     // OZ2_FORCE_FALLBACK
-  const int rr = b.tt & 31;
-  const int row = b.row0 + rr;
   if (row < d.m && !(!nofb && (force || (fA[row] & (OZ2_T1 | OZ2_T2))))) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int cc = j * 4 + (b.tt >> 5);
       const int col = b.col0 + cc;
       if (col < d.n && (nofb || !(fB[col] & (OZ2_T1 | OZ2_T2)))) {
-        double* o = C + (size_t)col * ldc + row;
         const double v = tr[b.hb][cc][rr];
-        *o = acc ? *o + v : v;
+        C[(size_t)col * ldc + row] = ACC ? cin[j] + v : v;
       }
     }
   }
@@ -363,7 +371,8 @@ void launch_reconstruct_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& 
                           const double* A, int lda, double* C, int ldc, hipStream_t s) {
   const size_t blocks = (size_t)d.mp * d.np / 2048;
   const bool gather = !(d.flags & 8u);   // OZ2_NO_FALLBACK: no fallback, no panel
-  hipLaunchKernelGGL(k_reconstruct<R>, dim3((unsigned)blocks), dim3(256), 0, s, c, d,
+  auto kern = (d.flags & 1u) ? k_reconstruct<R, true> : k_reconstruct<R, false>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), 0, s, c, d,
                      (const uint32_t*)(ws + L.res), (const int32_t*)(ws + L.sA),
                      (const int32_t*)(ws + L.tB), (const uint32_t*)(ws + L.flagsA),
                      (const uint32_t*)(ws + L.flagsB), C, ldc, A, lda,
