@@ -46,16 +46,19 @@ def _sample_C(Cd, rows, cols):
     return Cd.index_select(0, ri).index_select(1, ci).cpu().numpy()
 
 
-def _check(C, res, A, B, rows, cols, bound=1e-15):
+def _check(C, res, A, B, rows, cols, bound=1e-15, err_entries=768):
     """Sampled entries without fallback: bit-exact against the oracle, and the
-    componentwise error of the sample within `bound`; returns their count."""
+    componentwise error within `bound` on up to `err_entries` of them (the
+    exact error takes an exactly rounded sum of 2k + 1 terms per entry);
+    returns the number of bit-exact entries."""
     fr = set(res.fallback_rows.tolist())
     fc = set(res.fallback_cols.tolist())
-    mask = np.array([[(i not in fr and j not in fc) for j in cols] for i in rows])
+    mask = ~np.isin(rows, list(fr))[:, None] & ~np.isin(cols, list(fc))[None, :]
     assert np.array_equal(bits(C[mask]), bits(res.C[mask]))
     rr, cc = np.meshgrid(rows, cols, indexing="ij")
     if mask.any():
-        ratio = refgemm.componentwise_ratio(C[mask], A, B, rr[mask], cc[mask])
+        pick = np.random.default_rng(0).permutation(int(mask.sum()))[:err_entries]
+        ratio = refgemm.componentwise_ratio(C[mask][pick], A, B, rr[mask][pick], cc[mask][pick])
         assert ratio <= bound, ratio
     return int(mask.sum())
 
@@ -63,12 +66,12 @@ def _check(C, res, A, B, rows, cols, bound=1e-15):
 def test_gemm4096_lognormal_r12_sampled():
     A, B = synth.make("gemm4096_lognormal")
     rng = np.random.default_rng(7)
-    rows = np.sort(rng.choice(4096, 24, replace=False))
-    cols = np.sort(rng.choice(4096, 24, replace=False))
+    rows = np.sort(rng.choice(4096, 256, replace=False))
+    cols = np.sort(rng.choice(4096, 256, replace=False))
     plan, Cd = _run(A, B, 12)
     C = _sample_C(Cd, rows, cols)
     res = oracle.dgemm(A, B, 12, rows=rows, cols=cols)
-    assert _check(C, res, A, B, rows, cols) == 24 * 24
+    assert _check(C, res, A, B, rows, cols) == 256 * 256
     del plan, Cd
     _free()
 
@@ -77,9 +80,9 @@ def test_gemm16384_wide_r15_sampled():
     A, B, big = synth.make("gemm16384_wide")
     assert len(big) > 100
     rng = np.random.default_rng(8)
-    rows = np.sort(np.concatenate([rng.choice(big, 4, replace=False),
-                                   rng.choice(16384, 6, replace=False)]))
-    cols = np.sort(rng.choice(16384, 8, replace=False))
+    rows = np.unique(np.concatenate([rng.choice(big, 16, replace=False),
+                                     rng.choice(16384, 112, replace=False)]))
+    cols = np.sort(rng.choice(16384, 96, replace=False))
     plan, Cd = _run(A, B, 15)
     C = _sample_C(Cd, rows, cols)
     res = oracle.dgemm(A, B, 15, rows=rows, cols=cols)
@@ -94,9 +97,9 @@ def test_gemm16384_wide_span_fallback_r15_sampled():
     import paper_2606_06510_amd as oz
     A, B, big = synth.make("gemm16384_wide_span")
     rng = np.random.default_rng(9)
-    rows = np.sort(np.concatenate([rng.choice(big, 3, replace=False),
-                                   rng.choice(16384, 5, replace=False)]))
-    cols = np.sort(rng.choice(16384, 8, replace=False))
+    rows = np.unique(np.concatenate([rng.choice(big, 6, replace=False),
+                                     rng.choice(16384, 42, replace=False)]))
+    cols = np.sort(rng.choice(16384, 48, replace=False))
     plan, Cd = _run(A, B, 15)
     count = plan.query(oz.OZ2_Q_FALLBACK_COUNT)
     C = _sample_C(Cd, rows, cols)
@@ -120,25 +123,25 @@ def test_rankk32768x256_accumulate_sampled():
     import paper_2606_06510_amd as oz
     A, B, C0 = synth.make("rankk32768x256")
     rng = np.random.default_rng(10)
-    rows = np.sort(rng.choice(32768, 12, replace=False))
-    cols = np.sort(rng.choice(32768, 12, replace=False))
+    rows = np.sort(rng.choice(32768, 256, replace=False))
+    cols = np.sort(rng.choice(32768, 256, replace=False))
     plan, Cd = _run(A, B, 12, flags=oz.OZ2_ACCUMULATE, C_in=C0)
     C = _sample_C(Cd, rows, cols)
     res = oracle.dgemm(A, B, 12, rows=rows, cols=cols, C_in=C0)
-    for a in range(len(rows)):
-        for b in range(len(cols)):
-            assert bits(C[a, b]) == bits(res.C[a, b])
+    assert np.array_equal(bits(C), bits(res.C))
     # error of the product part (C_out - C_in is not exact; compare A B alone)
     prod = oracle.dgemm(A, B, 12, rows=rows, cols=cols)
     rr, cc = np.meshgrid(rows, cols, indexing="ij")
-    assert refgemm.componentwise_ratio(prod.C.ravel(), A, B, rr.ravel(), cc.ravel()) <= 1e-15
+    pick = np.random.default_rng(0).permutation(rr.size)[:768]
+    assert refgemm.componentwise_ratio(prod.C.ravel()[pick], A, B, rr.ravel()[pick],
+                                       cc.ravel()[pick]) <= 1e-15
     del plan, Cd
     _free()
 
 
 def test_outputs_beyond_2_pow_31():
     """65536 x 40000 outputs (2.6e9, above 2^31) at k = 64: C, the staged
-    residues (12 x 2.6e9 int16, 63 GB) and the launch grids all need 64-bit
+    residues (12 x 2.6e9 12-bit slots, 47 GB) and the launch grids all need 64-bit
     indexing; sampled entries, including the last row and columns whose
     column-major offsets exceed 2^31, are bit-exact."""
     m, n, k = 65536, 40000, 64
@@ -168,7 +171,7 @@ def test_batched8192x64_sampled():
                                     nb, 12)
     torch.cuda.synchronize()
     rng = np.random.default_rng(12)
-    for b in np.sort(rng.choice(nb, 12, replace=False)):
+    for b in np.sort(rng.choice(nb, 64, replace=False)):
         Cb = Cd[b].cpu().numpy().T
         rb = oracle.dgemm(Ab[b], Bb[b], 12)
         assert np.array_equal(bits(Cb), bits(rb.C)), b
