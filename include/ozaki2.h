@@ -68,7 +68,8 @@ enum {
   OZ2_FORCE_FALLBACK = 16u,/* recompute every row natively (testing aid) */
   OZ2_KEEP_RESIDUES = 32u, /* materialise the r residues of every output in the workspace
                               (the staged route, which every call takes unless OZ2_FUSED is
-                              given: the flag only forbids OZ2_FUSED alongside it) */
+                              given or ozaki2_dgemm_ex takes its tall-skinny route: the flag
+                              forbids OZ2_FUSED alongside it and keeps that route off) */
   OZ2_TIME_STAGES = 64u,   /* plans only: record HIP events between the stages on the
                               stream of each call (OZ2_Q_STAGE_TIMES) */
   OZ2_FUSED = 128u         /* the residue GEMMs and the reconstruction as one kernel that
@@ -93,7 +94,12 @@ int ozaki2_dgemm(int m, int n, int k, const double* A, int lda, const double* B,
 
 /* C = A*B, or C = C + A*B with OZ2_ACCUMULATE, using the caller's workspace
  * (device memory of at least ozaki2_workspace_bytes(m, n, k, r, flags) bytes,
- * 256-byte aligned; contents on entry are ignored and on exit undefined). */
+ * 256-byte aligned; contents on entry are ignored and on exit undefined).
+ * With OZ2_SCALE_FIXED, n <= 16 and none of OZ2_ACCUMULATE, OZ2_FUSED,
+ * OZ2_KEEP_RESIDUES, the product runs as the fused GEMV of ozaki2_gemv_batched
+ * (A deconstructed on the fly, the fused mode for tall-skinny products of
+ * Section "On-Chip Tile Fusion"): the same results as the staged path, bit for
+ * bit, without A's digit planes. */
 int ozaki2_dgemm_ex(int m, int n, int k, const double* A, int lda,
                     const double* B, int ldb, double* C, int ldc,
                     int num_moduli, unsigned flags, void* workspace,
@@ -148,7 +154,8 @@ int ozaki2_gemv_batched(int m, int k, int nrhs, const double* A, int lda, const 
 size_t ozaki2_gemv_workspace_bytes(int m, int k, int nrhs, int num_moduli);
 
 /* Workspace bytes ozaki2_dgemm_ex / ozaki2_plan_create need (0 on invalid
- * arguments). */
+ * arguments; for the tall-skinny fixed-scale route of ozaki2_dgemm_ex, enough
+ * for both it and a plan). */
 size_t ozaki2_workspace_bytes(int m, int n, int k, int num_moduli, unsigned flags);
 
 /* The r moduli in ascending (reconstruction) order into host_out[0..r-1]. */

@@ -556,12 +556,24 @@ int ozaki2_moduli(int num_moduli, int* host_out) {
   return OZ2_OK;
 }
 
+// C = A B with at most 16 columns under the fixed scaling: ozaki2_dgemm_ex
+// runs the fused GEMV of Alg. 2 (A deconstructed on the fly, fused mode F for
+// tall-skinny products), whose results equal the staged fixed-scale path's
+// bit for bit; plans always take the staged path.
+static bool skinny_route(int n, unsigned flags) {
+  return (flags & OZ2_SCALE_FIXED) && n <= kGemvRhs &&
+         !(flags & (OZ2_ACCUMULATE | OZ2_FUSED | OZ2_KEEP_RESIDUES | OZ2_TIME_STAGES));
+}
+
 size_t ozaki2_workspace_bytes(int m, int n, int k, int num_moduli, unsigned flags) {
   Oz2Const c;
   Oz2Dims d;
   if ((flags & ~kKnownFlags) || !make_const(num_moduli, c) || !make_dims(m, n, k, flags, d))
     return 0;
-  return make_layout(d, c).total;
+  const size_t staged = make_layout(d, c).total;
+  if (!skinny_route(n, flags)) return staged;
+  // enough for either route: the same size serves ozaki2_plan_create
+  return std::max(staged, ozaki2_gemv_workspace_bytes(m, k, n, num_moduli));
 }
 
 int ozaki2_plan_create(ozaki2_plan_t* out, int m, int n, int k, int num_moduli, unsigned flags,
@@ -692,6 +704,9 @@ int ozaki2_dgemm_ex(int m, int n, int k, const double* A, int lda, const double*
     if (flags & OZ2_ACCUMULATE) return OZ2_OK;
     return hip_status(oz2_launch_fill(C, m, n, ldc, s));
   }
+  if (skinny_route(n, flags))
+    return ozaki2_gemv_batched(m, k, n, A, lda, B, ldb, C, ldc, num_moduli, flags & kGemvFlags,
+                               workspace, ws_bytes, stream);
   ozaki2_plan_s p;
   flags = route_flags(m, n, k, num_moduli, flags);
   if (!make_const(num_moduli, p.c) || !make_dims(m, n, k, flags, p.d)) return OZ2_E_INVALID;

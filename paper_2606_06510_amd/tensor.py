@@ -29,8 +29,17 @@ def from_device_colmajor(T):
 
 
 def _ld(T):
-    if T.dim() != 2 or T.stride(0) != 1:
+    """Leading dimension of a column-major (m, n) view.  A dimension of size
+    1 carries no stride information (numpy and torch normalise it), so a
+    single column has leading dimension max(m, 1) and a single row any
+    stride."""
+    if T.dim() != 2:
         raise ValueError("expected a column-major (m, n) view with stride (1, ld)")
+    m, n = T.shape
+    if m > 1 and T.stride(0) != 1:
+        raise ValueError("expected a column-major (m, n) view with stride (1, ld)")
+    if n <= 1:
+        return max(m, 1)
     return max(T.stride(1), 1)
 
 

@@ -132,6 +132,21 @@ def test_zero_sized_output_is_a_noop():
     assert L.ozaki2_dgemm(4, 0, 6, None, 4, None, 6, None, 4, 12, None) == 0
 
 
+def test_skinny_route_workspace_serves_both_routes():
+    """With OZ2_SCALE_FIXED and n <= 16 ozaki2_dgemm_ex takes the fused GEMV;
+    the workspace size covers that route and a plan of the same shape."""
+    f = oz.OZ2_SCALE_FIXED
+    for m, n, k in [(300, 8, 500), (5000, 16, 20000), (64, 1, 1)]:
+        both = oz.ozaki2_workspace_bytes(m, n, k, 12, f)
+        assert both == max(oz.ozaki2_gemv_workspace_bytes(m, k, n, 12),
+                           oz.ozaki2_workspace_bytes(m, n, k, 12, f | oz.OZ2_KEEP_RESIDUES))
+    # n = 17, or accumulation: the staged path alone
+    assert oz.ozaki2_workspace_bytes(300, 17, 500, 12, f) == \
+        oz.ozaki2_workspace_bytes(300, 17, 500, 12, f | oz.OZ2_KEEP_RESIDUES)
+    assert oz.ozaki2_workspace_bytes(300, 8, 500, 12, f | oz.OZ2_ACCUMULATE) == \
+        oz.ozaki2_workspace_bytes(300, 8, 500, 12, f | oz.OZ2_KEEP_RESIDUES)
+
+
 def test_stage_timing_flag_is_for_plans_only():
     L = oz.load()
     st = L.ozaki2_dgemm_ex(4, 5, 6, FAKE, 4, FAKE + (1 << 20), 6, FAKE + (2 << 20), 4, 12,

@@ -103,3 +103,32 @@ def test_gemv_full_size_sampled():
     del Ad, Xd, Yd
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("m,n,k,r", [(300, 8, 500, 12), (1000, 16, 3000, 13), (129, 1, 70, 8),
+                                     (257, 17, 300, 12)])
+@pytest.mark.parametrize("fallback", [False, True])
+def test_fixed_scale_skinny_route_matches_staged(m, n, k, r, fallback):
+    """ozaki2_dgemm_ex with OZ2_SCALE_FIXED and n <= 16 runs the fused GEMV
+    kernel; its C equals the staged fixed-scale plan's bit for bit (and the
+    oracle's on unflagged entries).  n = 17 takes the staged path itself."""
+    import paper_2606_06510_amd as oz
+    import torch
+    from tests.gpu_util import run_staged
+    A, B = synth.lognormal(m, n, k, seed=m + 3 * n + k)
+    if fallback:
+        A[min(5, m - 1), k // 2] = np.nan           # a T1 row of A
+        B[k // 3, n - 1] *= 1e300                    # a huge entry: T2 in its column's span
+    dev = device()
+    Ad, Bd = oz.to_device_colmajor(A, dev), oz.to_device_colmajor(B, dev)
+    Cd = oz.to_device_colmajor(np.full((m, n), np.nan), dev)
+    oz.matmul(Ad, Bd, r, flags=oz.OZ2_SCALE_FIXED, C=Cd)
+    torch.cuda.synchronize()
+    got = oz.from_device_colmajor(Cd)
+    _, staged = run_staged(A, B, r, oz.OZ2_SCALE_FIXED)
+    assert np.array_equal(bits(got), bits(staged))
+    res = oracle.dgemm(A, B, r, mode="fixed")
+    emu = ~np.isin(np.arange(m), res.fallback_rows)[:, None] & \
+        ~np.isin(np.arange(n), res.fallback_cols)[None, :]
+    assert np.array_equal(bits(got[emu]), bits(res.C[emu]))
+    assert fallback == (not emu.all())

@@ -87,3 +87,17 @@ def test_words_to_ints_roundtrip():
     w = np.array([[(v >> (32 * q)) & 0xFFFFFFFF for q in range(5)] for v in vals], dtype=np.uint32)
     back = oz.words_to_ints(w)
     assert [int(x) for x in back] == vals
+
+
+def test_leading_dimension_of_single_columns_and_rows():
+    """numpy and torch normalise the stride of a size-1 dimension (a single
+    column made by to_device_colmajor has strides (1, 1)): the leading
+    dimension handed to the C ABI is then max(m, 1), never below m."""
+    for m, n in [(70, 1), (1, 70), (1, 1), (5, 3)]:
+        X = np.asfortranarray(np.arange(m * n, dtype=np.float64).reshape(m, n))
+        T = oz.to_device_colmajor(X, "cpu")
+        assert tensor._ld(T) >= max(m, 1)
+        assert tensor._ld(T) == (max(m, 1) if n == 1 else T.stride(1))
+        assert np.array_equal(oz.from_device_colmajor(T), X)
+    with pytest.raises(ValueError):
+        tensor._ld(torch.zeros(4, 3))                 # row-major (stride (3, 1))
