@@ -260,13 +260,13 @@ Oz2Layout make_layout(const Oz2Dims& d, const Oz2Const& c) {
 
 // ------------------------------------------------------------ batched GEMV
 // Y = A X with X of nrhs <= 16 columns (the fused kernel of gemv.hip): k in
-// chunks of 128, 64 rows of A per workgroup, and enough k-splits that every
+// chunks of 128, 128 rows of A per workgroup, and enough k-splits that every
 // split spans at most 32768 k (exact FP32 accumulation) and the row blocks
 // times the splits cover about 256 workgroups.
-constexpr int kGemvRhs = 16, kGemvK = 128, kGemvRows = 64;
+constexpr int kGemvRhs = 16, kGemvK = 128, kGemvRows = 128;
 
 struct GemvShape {
-  Oz2Dims d;          // n = nrhs, np = 16, mp = rows padded to 64, kp to 128
+  Oz2Dims d;          // n = nrhs, np = 16, mp = rows padded to 128, kp to 128
   int chunks, splits;
 };
 

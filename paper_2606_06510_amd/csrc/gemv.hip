@@ -12,13 +12,14 @@
 // Kernels (after the scan and scale kernels and the plane tables):
 //  * k_gemv_xplanes: X quantised, reduced and split once into MFMA operand
 //    fragments [chunk][plane][half][lane][16 B] (k in chunks of 128);
-//  * k_gemv<R>: a workgroup of 4 waves owns 64 rows of A (wave w rows
-//    16w..16w+15) and a range of chunks (split-K); per chunk each lane loads
-//    32 elements of its row (row L%16, k 32(L/16)..+31: exactly its operand
-//    bytes of v_mfma_f32_16x16x128_f8f6f4), quantises them once, then per
-//    modulus forms their residues (exact fp64), looks the E4M3 plane bytes up
-//    in an LDS table and issues the modulus's three plane products against
-//    the X fragments (staged in LDS, shared by the 4 waves).  Square m = s^2:
+//  * k_gemv<R>: a workgroup of 8 waves (2 per SIMD) owns 128 rows of A (wave
+//    w rows 16w..16w+15) and a range of chunks (split-K); per 32-k quarter of
+//    a chunk each lane loads 8 elements of its row (row L%16, k 8(L/16)..+7:
+//    exactly its operand bytes of v_mfma_f32_16x16x32_fp8_fp8), the next
+//    quarter's loads in flight, quantises them once, then per modulus forms
+//    their residues (exact fp64), looks the E4M3 plane bytes up in an LDS
+//    table and issues the modulus's three plane products against the X
+//    fragments (staged in LDS, shared by the 8 waves).  Square m = s^2:
 //    acc0 += d0 e0, acc1 += d1 e0 + d0 e1; nonsquare (Eq. (kar), b = 4):
 //    acc0 += (d0+d1)(e0+e1), acc1 += d0 e0, acc2 += d1 e1.  Every partial
 //    sum is an integer below 2^24 while a split spans at most 32768 k
@@ -36,13 +37,15 @@ namespace {
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-constexpr int GV_ROWS = 64;    // rows of A per workgroup
-constexpr int GV_K = 128;      // k per chunk (one 16x16x128 MFMA)
-constexpr int GV_NT = 256;     // threads per workgroup
+constexpr int GV_ROWS = 128;   // rows of A per workgroup
+constexpr int GV_K = 128;      // k per chunk (X's fragments are staged per chunk)
+constexpr int GV_NT = 512;     // threads per workgroup (8 waves)
 constexpr int GV_FRAG = 2048;  // bytes of one plane's operand fragments per chunk
 
-__device__ __forceinline__ v4f mfma16(v8i a, v8i b, v4f c) {
-  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+// 16 x 16 x 32 E4M3 product: lane L holds row (A) / column (B) L%16,
+// k 8(L/16) .. +7; the result lane L column L%16, rows 4(L/16) .. +3
+__device__ __forceinline__ v4f mfma16k32(long a, long b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_fp8_fp8(a, b, c, 0, 0, 0);
 }
 
 // Quantise 32 elements with the power-of-two scale sc (Eq. (scale)): a =
@@ -81,13 +84,46 @@ __device__ __forceinline__ void planes32(const Oz2Const& c, int i, const uint32_
   }
 }
 
-// fragment of plane p (of the chunk staged in LDS) for this lane: the two
-// 16-byte halves are stored [half][lane] so that consecutive lanes read
-// consecutive 16 bytes
-__device__ __forceinline__ v8i xfrag_lds(const uint8_t* xs, int p, int lane) {
-  const uint4 lo = *reinterpret_cast<const uint4*>(xs + (size_t)p * GV_FRAG + 16 * lane);
-  const uint4 hi = *reinterpret_cast<const uint4*>(xs + (size_t)p * GV_FRAG + 1024 + 16 * lane);
-  return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+// Quantise 8 elements (as quantise32).
+__device__ __forceinline__ void quantise8(const double (&x)[8], int sc, unsigned tz, bool& t2,
+                                          double (&ah)[8], double (&al)[8]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const double y = ldexp(x[j], sc);
+    const double a = tz ? trunc(y) : rint(y);
+    t2 |= (x[j] != 0.0) && (a == 0.0);
+    const double h = floor(a * 0x1p-32);
+    ah[j] = h;
+    al[j] = fma(-h, 0x1p32, a);
+  }
+}
+
+// Operand bytes of the planes of modulus i for 8 quantised elements (byte j
+// of plane p: table entry byte p of element j: d0, d1, d0 + d1).
+template <bool SQ>
+__device__ __forceinline__ void planes8(const Oz2Const& c, int i, const uint32_t* tab,
+                                        const double (&ah)[8], const double (&al)[8], long& p0,
+                                        long& p1, long& p2) {
+  const double m = (double)c.m[i], c32 = (double)c.c32[i], dinv = c.dinv[i];
+  const int to = c.toff[i];
+  uint32_t e[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) e[j] = tab[to + centred_residue(ah[j], al[j], m, c32, dinv)];
+  auto word = [&](int g, uint32_t sel) { return gather_byte(e[4 * g], e[4 * g + 1], e[4 * g + 2], e[4 * g + 3], sel); };
+  p0 = (long)(((uint64_t)word(1, 0x05010400u) << 32) | word(0, 0x05010400u));
+  p1 = (long)(((uint64_t)word(1, 0x05010501u) << 32) | word(0, 0x05010501u));
+  if (!SQ) p2 = (long)(((uint64_t)word(1, 0x05010602u) << 32) | word(0, 0x05010602u));
+}
+
+// X's operand bytes of plane p for quarter q of the chunk staged in LDS:
+// lane L needs column L%16, k 32 q + 8 (L/16) .. +7, which the chunk's
+// fragment layout ([half][lane'][16 B], lane' holding column lane'%16, k
+// 32 (lane'/16) .. +31) keeps in lane' = 16 q + L%16, byte 8 (L/16); a
+// wave's 8-byte reads cover 2 x 256 contiguous bytes
+__device__ __forceinline__ long xfrag8(const uint8_t* xs, int p, int q, int lane) {
+  const int u = lane >> 4;
+  const uint8_t* a = xs + (size_t)p * GV_FRAG + (u >> 1) * 1024 + 16 * (16 * q + (lane & 15)) + 8 * (u & 1);
+  return *reinterpret_cast<const long*>(a);
 }
 
 // x - m rint(x/m) in fp32: a representative of magnitude <= m/2 + 1 for an
@@ -157,12 +193,13 @@ k_gemv(Oz2Const c, const double* __restrict__ A, int lda, int m, int k, int chun
   const int c0 = split * cps, c1 = min(chunks, c0 + cps);
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = blockIdx.x * GV_ROWS + 16 * w + (lane & 15);
-  const int kq = 32 * (lane >> 4);
+  const int kq = 8 * (lane >> 4);
   const bool rok = row < m;
   const uint32_t f0 = rok ? flagsA[row] : 0u;
   const bool zero = !rok || (f0 & OZ2_T1);
   const int sc = zero ? 0 : sA[row];
   const int fbytes = c.P * GV_FRAG;
+  const double* arow = A + (size_t)row;
 
   v4f acc[R][3];
 #pragma unroll
@@ -170,39 +207,43 @@ k_gemv(Oz2Const c, const double* __restrict__ A, int lda, int m, int k, int chun
 #pragma unroll
     for (int q = 0; q < 3; ++q) acc[i][q] = v4f{0.f, 0.f, 0.f, 0.f};
   bool t2 = false;
-  // (loading the next chunk's elements one chunk ahead measured slower: 3.41
-  // against 3.09 ms at 16384 x 16384 x 8, r = 13 -- the extra 64 registers)
-  for (int ch = c0; ch < c1; ++ch) {
-    double x[32];
-    const int l0 = ch * GV_K + kq;
+  // the lane's 8 elements of quarter q of chunk ch
+  auto load8 = [&](int ch, int q, double (&x)[8]) {
+    const int l0 = ch * GV_K + 32 * q + kq;
 #pragma unroll
-    for (int j = 0; j < 32; ++j) {
+    for (int j = 0; j < 8; ++j) {
       const int l = l0 + j;
-      x[j] = (!zero && l < k) ? A[(size_t)row + (size_t)l * lda] : 0.0;
+      x[j] = (!zero && l < k) ? arow[(size_t)l * lda] : 0.0;
     }
+  };
+  for (int ch = c0; ch < c1; ++ch) {
     __syncthreads();   // every wave is done with the previous chunk's fragments
     const uint4* src = reinterpret_cast<const uint4*>(xf + (size_t)ch * fbytes);
     for (int q = threadIdx.x; q < fbytes / 16; q += GV_NT) reinterpret_cast<uint4*>(xs)[q] = src[q];
-    double ah[32], al[32];
-    quantise32(x, sc, tz, t2, ah, al);
     __syncthreads();   // the fragments (and, at first, the tables) are in LDS
+#pragma unroll 1
+    for (int q = 0; q < 4; ++q) {
+      double xq[8], ah[8], al[8];
+      load8(ch, q, xq);
+      quantise8(xq, sc, tz, t2, ah, al);
 #pragma unroll
-    for (int i = 0; i < R; ++i) {
-      const int pb = c.pbase[i];
-      v8i p0, p1, p2;
-      if (i >= R - 6) {
-        planes32<true>(c, i, tab, ah, al, p0, p1, p2);
-        const v8i x0 = xfrag_lds(xs, pb, lane), x1 = xfrag_lds(xs, pb + 1, lane);
-        acc[i][0] = mfma16(p0, x0, acc[i][0]);
-        acc[i][1] = mfma16(p1, x0, acc[i][1]);
-        acc[i][1] = mfma16(p0, x1, acc[i][1]);
-      } else {
-        planes32<false>(c, i, tab, ah, al, p0, p1, p2);
-        const v8i x0 = xfrag_lds(xs, pb, lane), x1 = xfrag_lds(xs, pb + 1, lane),
-                  x2 = xfrag_lds(xs, pb + 2, lane);
-        acc[i][0] = mfma16(p2, x2, acc[i][0]);
-        acc[i][1] = mfma16(p0, x0, acc[i][1]);
-        acc[i][2] = mfma16(p1, x1, acc[i][2]);
+      for (int i = 0; i < R; ++i) {
+        const int pb = c.pbase[i];
+        long p0, p1, p2;
+        if (i >= R - 6) {
+          planes8<true>(c, i, tab, ah, al, p0, p1, p2);
+          const long x0 = xfrag8(xs, pb, q, lane), x1 = xfrag8(xs, pb + 1, q, lane);
+          acc[i][0] = mfma16k32(p0, x0, acc[i][0]);
+          acc[i][1] = mfma16k32(p1, x0, acc[i][1]);
+          acc[i][1] = mfma16k32(p0, x1, acc[i][1]);
+        } else {
+          planes8<false>(c, i, tab, ah, al, p0, p1, p2);
+          const long x0 = xfrag8(xs, pb, q, lane), x1 = xfrag8(xs, pb + 1, q, lane),
+                     x2 = xfrag8(xs, pb + 2, q, lane);
+          acc[i][0] = mfma16k32(p2, x2, acc[i][0]);
+          acc[i][1] = mfma16k32(p0, x0, acc[i][1]);
+          acc[i][2] = mfma16k32(p1, x1, acc[i][2]);
+        }
       }
     }
   }
@@ -210,7 +251,7 @@ k_gemv(Oz2Const c, const double* __restrict__ A, int lda, int m, int k, int chun
     listA[atomicAdd(countA, 1)] = row;
   // epilogue: lane L holds column L%16, rows 4(L/16) + e of the wave's 16;
   // stored as [split][modulus][row block of 16][lane][4]
-  const size_t tile = (size_t)blockIdx.x * 4 + w;
+  const size_t tile = (size_t)blockIdx.x * (GV_ROWS / 16) + w;
 #pragma unroll
   for (int i = 0; i < R; ++i) {
     const float fm = (float)c.m[i], inv = c.finv[i];
