@@ -80,7 +80,13 @@ enum {
                               ozaki2_reconstruct runs the fused kernel; OZ2_Q_RESIDUES and
                               OZ2_Q_INTEGERS are not available.  Results are those of the
                               staged route bit for bit; on MI355X it is the slower route (see
-                              ozaki2_dgemm_ex), so it is taken only when asked for */
+                              ozaki2_dgemm_ex), so it is taken only when asked for */,
+  OZ2_REUSE_A_SCALES = 256u /* ozaki2_gemv_batched only: the workspace still holds A's row
+                              scales, flags and fallback list from the previous call on it,
+                              made with the same A (contents), lda, m, k, num_moduli and
+                              other flags (the caller's promise: nothing checks it); the
+                              scan of A is skipped, as an operand-stationary A in an
+                              iterative method allows.  Results are those of a full call */
 };
 
 /* C = A*B with the default flags (accumulation: ozaki2_dgemm_ex).
@@ -142,7 +148,7 @@ int ozaki2_dgemm_strided_batched(int m, int n, int k, const double* A, int lda,
  * RN-even value of D^-1 (A~ X~) E^-1 exactly as ozaki2_dgemm_ex with
  * OZ2_SCALE_FIXED computes it; flagged rows of A / columns of X (T1, T2) are
  * recomputed natively.  flags: OZ2_QUANT_TZ, OZ2_NO_FALLBACK,
- * OZ2_FORCE_FALLBACK (others: OZ2_E_INVALID).  workspace: device memory of
+ * OZ2_FORCE_FALLBACK, OZ2_REUSE_A_SCALES (others: OZ2_E_INVALID).  workspace: device memory of
  * ozaki2_gemv_workspace_bytes(m, k, nrhs, r) bytes, 256-byte aligned.  k = 0
  * gives Y = 0; m = 0 or nrhs = 0 is a no-op.  Validation as for
  * ozaki2_dgemm_ex (nrhs > 16: OZ2_E_INVALID). */

@@ -30,6 +30,7 @@ OZ2_FORCE_FALLBACK = 16
 OZ2_KEEP_RESIDUES = 32
 OZ2_TIME_STAGES = 64
 OZ2_FUSED = 128
+OZ2_REUSE_A_SCALES = 256
 
 OZ2_Q_EXPONENTS = 1
 OZ2_Q_MAXIMA = 2

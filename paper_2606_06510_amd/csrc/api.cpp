@@ -315,7 +315,8 @@ Oz2Layout make_gemv_layout(const GemvShape& g, const Oz2Const& c) {
   return L;
 }
 
-const unsigned kGemvFlags = OZ2_QUANT_TZ | OZ2_NO_FALLBACK | OZ2_FORCE_FALLBACK;
+const unsigned kGemvFlags =
+    OZ2_QUANT_TZ | OZ2_NO_FALLBACK | OZ2_FORCE_FALLBACK | OZ2_REUSE_A_SCALES;
 
 const unsigned kKnownFlags = OZ2_ACCUMULATE | OZ2_SCALE_FIXED | OZ2_QUANT_TZ | OZ2_NO_FALLBACK |
                              OZ2_FORCE_FALLBACK | OZ2_KEEP_RESIDUES | OZ2_TIME_STAGES | OZ2_FUSED;
@@ -842,11 +843,14 @@ int ozaki2_gemv_batched(int m, int k, int nrhs, const double* A, int lda, const 
   const Oz2Dims& d = g.d;
   const unsigned tz = (flags & OZ2_QUANT_TZ) ? 1u : 0u;
   const int listed = (flags & OZ2_FORCE_FALLBACK) ? 1 : 0;
-  const int both = OZ2_SIDE_A | OZ2_SIDE_B;
-  hipError_t e = oz2_launch_init(d, L, ws, both, s);
-  if (e == hipSuccess) e = oz2_launch_scan(d, L, ws, A, lda, X, ldx, both, s);
-  if (e == hipSuccess) e = oz2_launch_scales(d, L, c, ws, both, s);
-  if (e == hipSuccess) e = oz2_launch_tables(L, c, ws, s);
+  // with OZ2_REUSE_A_SCALES, A's side (scales, flags, list, counter) and the
+  // plane tables are the previous call's
+  const bool reuse = (flags & OZ2_REUSE_A_SCALES) != 0;
+  const int sides = reuse ? OZ2_SIDE_B : (OZ2_SIDE_A | OZ2_SIDE_B);
+  hipError_t e = oz2_launch_init(d, L, ws, sides, s);
+  if (e == hipSuccess) e = oz2_launch_scan(d, L, ws, A, lda, X, ldx, sides, s);
+  if (e == hipSuccess) e = oz2_launch_scales(d, L, c, ws, sides, s);
+  if (e == hipSuccess && !reuse) e = oz2_launch_tables(L, c, ws, s);
   if (e == hipSuccess)
     e = oz2_launch_gemv_xplanes(c, X, ldx, k, nrhs, (const int32_t*)(ws + L.tB),
                                 (uint32_t*)(ws + L.flagsB), (int*)(ws + L.counters) + 1,

@@ -132,3 +132,31 @@ def test_fixed_scale_skinny_route_matches_staged(m, n, k, r, fallback):
         ~np.isin(np.arange(n), res.fallback_cols)[None, :]
     assert np.array_equal(bits(got[emu]), bits(res.C[emu]))
     assert fallback == (not emu.all())
+
+
+@pytest.mark.parametrize("m,k,n1,n2,r", [(300, 500, 8, 3, 12), (1000, 40000, 16, 16, 13)])
+def test_reuse_a_scales_matches_full_call(m, k, n1, n2, r):
+    """OZ2_REUSE_A_SCALES: a second call on the same A (a T1 row and a T2
+    row in it) with a new X skips A's scan and gives exactly the full call's
+    Y, flagged rows included."""
+    import paper_2606_06510_amd as oz
+    import torch
+    A, X1 = synth.lognormal(m, n1, k, seed=m + k)
+    A[3, k // 2] = np.inf                                # T1 row
+    A[7, 1] *= 1e280                                     # T2 row (the rest quantises to 0)
+    X2 = synth.lognormal(m, n2, k, seed=m + k + 1)[1]
+    dev = device()
+    Ad = oz.to_device_colmajor(A, dev)
+    ws = torch.empty(oz.ozaki2_gemv_workspace_bytes(m, k, 16, r), dtype=torch.uint8, device=dev)
+    Y1 = oz.gemv(Ad, oz.to_device_colmajor(X1, dev), num_moduli=r, workspace=ws)
+    X2d = oz.to_device_colmajor(X2, dev)
+    Y2 = oz.gemv(Ad, X2d, num_moduli=r, flags=oz.OZ2_REUSE_A_SCALES, workspace=ws)
+    Y2ref = oz.gemv(Ad, X2d, num_moduli=r)                # fresh workspace, full call
+    torch.cuda.synchronize()
+    y2, y2ref = oz.from_device_colmajor(Y2), oz.from_device_colmajor(Y2ref)
+    assert np.array_equal(bits(y2), bits(y2ref))
+    res = oracle.dgemm(A, X2, r, mode="fixed")
+    assert {3, 7} <= set(res.fallback_rows.tolist())
+    emu = ~np.isin(np.arange(m), res.fallback_rows)
+    assert np.array_equal(bits(y2[emu]), bits(res.C[emu]))
+    del Y1
