@@ -77,9 +77,10 @@ def source_sha256(rel):
 
 
 def pmc_traffic(kernel_src, tag):
-    """HBM traffic per launch of the dominant kernel from the committed
-    rocprofv3 FETCH_SIZE / WRITE_SIZE summary, scaled by the plain copy kernel's
-    reading; None unless the summary was taken on the current kernel source."""
+    """HBM traffic per step of the dominant kernel (all its launches in one
+    step) from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary, scaled
+    by the plain copy kernel's reading; None unless the summary was taken on
+    the current kernel source."""
     path = os.path.join(ROOT, "profiles", f"{tag}_pmc_traffic.txt")
     if not os.path.exists(path):
         return None
@@ -91,7 +92,7 @@ def pmc_traffic(kernel_src, tag):
     if vals.get("kernel_source_sha256") != source_sha256(kernel_src):
         return None
     try:
-        return float(vals["traffic_bytes_per_launch"])
+        return float(vals.get("traffic_bytes_per_step", vals["traffic_bytes_per_launch"]))
     except (KeyError, ValueError):
         return None
 
@@ -177,8 +178,9 @@ def main():
     torch.cuda.synchronize()
     log(f"{warmup} warm-up steps done")
 
-    # timed steps: HIP events around the residue GEMMs (the dominant kernel,
-    # one launch per step for k <= 32768) on the stream they are launched on
+    # timed steps: HIP events around the residue GEMMs (the dominant kernel:
+    # one launch per modulus group, 1024-tile chunk and k-slab) on the stream
+    # they are launched on
     gev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -293,10 +295,13 @@ def main():
                      "achieved": round(achieved, 2), "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
                      "traffic": None if traffic is None else round(traffic),
-                     "per_launch": f"{fp8_flop / slabs:.4g} FP8 FLOP (3r plane products x "
-                                   f"2mnk{'' if slabs == 1 else f' / {slabs} k-slabs'})",
+                     "per_step": f"{fp8_flop:.4g} FP8 FLOP (3r plane products x 2mnk)"
+                                 + ("" if fused else ", over all residue-GEMM launches of the "
+                                    "step (one per modulus group, 1024-tile chunk and "
+                                    f"k-slab; {slabs} k-slab{'s' if slabs > 1 else ''})"),
                      "timing": f"HIP events around the {'fused kernel' if fused else 'residue GEMMs'}"
-                               f" in each of the {args.steps} timed steps, mean {gem:.3f} ms"},
+                               f" in each of the {args.steps} timed steps (first launch start "
+                               f"to last launch end), mean {gem:.3f} ms per step"},
         "stages_ms": split,
         "fallback_rows_cols": list(nfb),
         "fp8_mfma_util_residue_gemm": round(achieved / FP8_PEAK_TFLOPS, 4),

@@ -256,14 +256,15 @@ __device__ __forceinline__ void halve(float (&u)[64], int lane) {
 }
 
 // ------------------------------------------------------------- code GEMM
-// grid: (tiles, code slabs).  G'[i][j] <= 256 * 65536 = 2^24: exact in FP32.
+// grid: (tiles tbase .. tbase + gridDim.x - 1, code slabs).
+// G'[i][j] <= 256 * 65536 = 2^24: exact in FP32.
 __global__ void __launch_bounds__(NT, 1)
 k_codegemm(const uint8_t* __restrict__ cA, const uint8_t* __restrict__ cB, int mp, int np,
-           int kp, uint32_t* Rmax, uint32_t* Kmax) {
+           int kp, uint32_t* Rmax, uint32_t* Kmax, int tbase) {
   __shared__ __attribute__((aligned(16))) uint8_t LB[NB * STB];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)LB;
   const int ntm = mp / TILE, ntn = np / TILE;
-  const int tile = tile_of(blockIdx.x, ntm, ntn), slab = blockIdx.y;
+  const int tile = tile_of(tbase + blockIdx.x, ntm, ntn), slab = blockIdx.y;
   const int tm = tile % ntm, tn = tile / ntm;
   const int kbeg = slab * OZ2_CSLAB, kend = min(kp, kbeg + OZ2_CSLAB);
   Ctx x;
@@ -369,20 +370,22 @@ __device__ __forceinline__ void chain_scale(v16f (&acc)[4][2], float f) {
 }
 
 // ------------------------------------------------------------- residue GEMM
-// grid: (tiles, ceil(r / mpw)).  Workgroup (t, g) computes moduli
-// g*mpw .. min(r, (g+1)*mpw) - 1 of tile t over k in [kbeg, kend), one after
-// the other on one accumulator set, as one continuous DMA stream.
+// grid: (tiles tbase .. tbase + gridDim.x - 1, 1).  Workgroup t computes
+// moduli mgroup*mpw .. min(r, (mgroup+1)*mpw) - 1 of tile tbase + t over k in
+// [kbeg, kend), one after the other on one accumulator set, as one
+// continuous DMA stream.
 // CH bit 0: square moduli, bit 1: nonsquare moduli take the first chain
 // transition as a plain multiply (every modulus of that kind has k <= kcheap)
 template <int CH>
 __global__ void __launch_bounds__(NT, 1)
 k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, int mp,
-          int np, int kp, int kbeg, int kend, int accumulate, int mpw, uint32_t* __restrict__ res) {
+          int np, int kp, int kbeg, int kend, int accumulate, int mpw, int mgroup, int tbase,
+          uint32_t* __restrict__ res) {
   __shared__ __attribute__((aligned(16))) uint8_t LB[NB * STB];
   const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)LB;
   const int ntm = mp / TILE, ntn = np / TILE;
-  const int tile = tile_of(blockIdx.x, ntm, ntn);
-  const int mi0 = blockIdx.y * mpw, mi1 = min(c.r, mi0 + mpw);
+  const int tile = tile_of(tbase + blockIdx.x, ntm, ntn);
+  const int mi0 = mgroup * mpw, mi1 = min(c.r, mi0 + mpw);
   const int tm = tile % ntm, tn = tile / ntm;
   Ctx x;
   x.psA = (size_t)mp * kp;
@@ -512,11 +515,26 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
 
 }  // namespace
 
+// Launch granularity: at most LAUNCH_TILES tiles (four rounds of one
+// workgroup per CU) and one modulus group per launch.  The workgroups of an
+// XCD that share A or B panels (the 4 x 8 groups of tile_of) run their
+// K-loops in step only while they started together: in one long launch the
+// dispatcher refills each CU as its workgroup ends, their starts drift apart
+// round after round, and the shared panel blocks no longer meet in L2.  A
+// new launch starts them together again (16384^3 at r = 15: 56.2 -> 61.8 TF
+// on one box; one launch per modulus alone gave 61.3).
+constexpr int LAUNCH_TILES = 1024;
+
 hipError_t oz2_launch_codegemm(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, hipStream_t s) {
-  dim3 grid((d.mp / TILE) * (d.np / TILE), d.cslabs);
-  hipLaunchKernelGGL(k_codegemm, grid, dim3(NT), 0, s, ws + L.codesA, ws + L.codesB, d.mp, d.np,
-                     d.kp, (uint32_t*)(ws + L.Rmax), (uint32_t*)(ws + L.Kmax));
-  return hipGetLastError();
+  const int tiles = (d.mp / TILE) * (d.np / TILE);
+  for (int tb = 0; tb < tiles; tb += LAUNCH_TILES) {
+    dim3 grid(std::min(LAUNCH_TILES, tiles - tb), d.cslabs);
+    hipLaunchKernelGGL(k_codegemm, grid, dim3(NT), 0, s, ws + L.codesA, ws + L.codesB, d.mp,
+                       d.np, d.kp, (uint32_t*)(ws + L.Rmax), (uint32_t*)(ws + L.Kmax), tb);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& c,
@@ -534,7 +552,7 @@ hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Con
   const int ksteps = (std::min(d.kp, OZ2_KSLAB) + KS - 1) / KS;
   const int by_work = std::max(1, WG_STEPS / (3 * ksteps));
   const int mpw = std::min((c.r + fill - 1) / fill, by_work);
-  dim3 grid(tiles, (c.r + mpw - 1) / mpw);
+  const int groups = (c.r + mpw - 1) / mpw;
   for (int kb = 0, sl = 0; kb < d.kp; kb += OZ2_KSLAB, ++sl) {
     const int ke = kb + OZ2_KSLAB < d.kp ? kb + OZ2_KSLAB : d.kp;
     // the first chain transition may skip its reduction when every modulus of
@@ -546,13 +564,17 @@ hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Con
       else ns_cheap = ns_cheap && ok;
     }
     const int ch = (sq_cheap ? 1 : 0) | (ns_cheap ? 2 : 0);
-    void (*kern)(Oz2Const, const uint8_t*, const uint8_t*, int, int, int, int, int, int, int,
-                 uint32_t*) = ch == 3 ? k_resgemm<3> : ch == 2 ? k_resgemm<2>
-                                                    : ch == 1 ? k_resgemm<1> : k_resgemm<0>;
-    hipLaunchKernelGGL(kern, grid, dim3(NT), 0, s, c, ws + L.planesA, ws + L.planesB, d.mp, d.np,
-                       d.kp, kb, ke, sl > 0 ? 1 : 0, mpw, (uint32_t*)(ws + L.res));
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    void (*kern)(Oz2Const, const uint8_t*, const uint8_t*, int, int, int, int, int, int, int, int,
+                 int, uint32_t*) = ch == 3 ? k_resgemm<3> : ch == 2 ? k_resgemm<2>
+                                           : ch == 1 ? k_resgemm<1> : k_resgemm<0>;
+    for (int g = 0; g < groups; ++g)
+      for (int tb = 0; tb < tiles; tb += LAUNCH_TILES) {
+        hipLaunchKernelGGL(kern, dim3(std::min(LAUNCH_TILES, tiles - tb)), dim3(NT), 0, s, c,
+                           ws + L.planesA, ws + L.planesB, d.mp, d.np, d.kp, kb, ke,
+                           sl > 0 ? 1 : 0, mpw, g, tb, (uint32_t*)(ws + L.res));
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+      }
   }
   return hipSuccess;
 }

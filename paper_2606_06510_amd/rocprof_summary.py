@@ -1,9 +1,10 @@
 """Render rocprofv3 output into the short text summaries kept under profiles/.
 
     python -m paper_2606_06510_amd.rocprof_summary stats STATS_CSV OUT_MD TITLE COMMAND
-    python -m paper_2606_06510_amd.rocprof_summary trace TRACE_CSV OUT_MD TITLE COMMAND SKIP COUNT
+    python -m paper_2606_06510_amd.rocprof_summary trace TRACE_CSV OUT_MD TITLE COMMAND SKIP COUNT \\
+        [STEPS]
     python -m paper_2606_06510_amd.rocprof_summary traffic FETCH_CSV WRITE_CSV OUT_TXT \\
-        KERNEL COPY_BYTES SOURCE CMD_FETCH CMD_WRITE
+        KERNEL COPY_BYTES SOURCE CMD_FETCH CMD_WRITE [STEPS]
     python -m paper_2606_06510_amd.rocprof_summary mfma COUNTER_CSV OUT_TXT SOURCE CMD [SKIP]
     python -m paper_2606_06510_amd.rocprof_summary hbm STATS_CSV FETCH_CSV WRITE_CSV OUT_MD \
         COPY_BYTES M N K R PSTORE CMD_TRACE CMD_FETCH CMD_WRITE [SKIP COUNT [ACC]]
@@ -15,7 +16,10 @@ table.  ``trace`` does the same from the per-dispatch kernel_trace.csv, keeping
 only dispatches SKIP .. SKIP+COUNT-1 of each kernel (in launch order): with
 SKIP = the bench's warm-up steps and COUNT = its timed steps, the averages
 cover the timed steps alone (kernels launched once per plan, not per step,
-drop out).  ``traffic`` reads two ``--pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE``
+drop out).  With STEPS (every step the traced program ran), a kernel
+dispatched L times per step (L = its dispatches / STEPS, a whole number)
+keeps dispatches L*SKIP .. L*(SKIP+COUNT)-1, and the table adds L and the
+kernel's time per step (the sum of its L launches).  ``traffic`` reads two ``--pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE``
 counter_collection.csv files (KiB per dispatch), takes the mean per launch of
 KERNEL and of the plain copy kernel (COPY_BYTES read and written), and scales
 the kernel's figures by copy_bytes / copy_reading; the result carries the
@@ -69,29 +73,51 @@ def stats(src, dst, title, cmd):
                     f"{float(r['Percentage']):.1f}% |\n")
 
 
-def trace(src, dst, title, cmd, skip, count):
+def _per_step(n, steps):
+    """Launches per step of a kernel dispatched n times in `steps` steps
+    (0 when it is not a whole number: launched per plan, not per step)."""
+    if not steps or n % steps:
+        return 0
+    return n // steps
+
+
+def trace(src, dst, title, cmd, skip, count, steps=None):
     by = collections.defaultdict(list)
     for r in csv.DictReader(open(src)):
         by[_short(r["Kernel_Name"])].append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
     rows = []
     for name, ds in by.items():
         ds.sort()
-        sel = [(e - b) * 1e-3 for b, e in ds[skip:skip + count]]
+        L = _per_step(len(ds), steps) if steps else 1
+        if steps and not L:
+            continue
+        sel = [(e - b) * 1e-3 for b, e in ds[L * skip:L * (skip + count)]]
         if sel:
-            rows.append((name, len(sel), sum(sel) / len(sel), min(sel), max(sel), sum(sel)))
-    tot = sum(r[5] for r in rows) or 1.0
-    rows.sort(key=lambda r: -r[5])
+            rows.append((name, L, len(sel), sum(sel) / len(sel), min(sel), max(sel), sum(sel)))
+    tot = sum(r[6] for r in rows) or 1.0
+    rows.sort(key=lambda r: -r[6])
     with open(dst, "w") as f:
         f.write(f"# {title}\n\nCommand (from the repository root, on one MI355X):\n\n```\n{cmd}\n```\n\n")
+        if steps:
+            f.write(f"The timed steps only ({count} steps after {skip} warm-up steps, of {steps} "
+                    f"steps the program ran): for a kernel launched L times per step, its "
+                    f"dispatches L*{skip} .. L*{skip + count}-1 in launch order.\n\n")
+            f.write("| kernel | launches per step | calls | avg (us) | min (us) | max (us) | "
+                    "per step (us) | share |\n|---|---|---|---|---|---|---|---|\n")
+            for name, L, n, avg, lo, hi, t in rows:
+                f.write(f"| {name} | {L} | {n} | {avg:.1f} | {lo:.1f} | {hi:.1f} | "
+                        f"{t / count:.1f} | {100 * t / tot:.1f}% |\n")
+            return
         f.write(f"Dispatches {skip} .. {skip + count - 1} of each kernel (launch order), i.e. the "
                 f"timed steps only; warm-up launches excluded.\n\n")
         f.write("| kernel | calls | avg (us) | min (us) | max (us) | share |\n|---|---|---|---|---|---|\n")
-        for name, n, avg, lo, hi, t in rows:
+        for name, L, n, avg, lo, hi, t in rows:
             f.write(f"| {name} | {n} | {avg:.1f} | {lo:.1f} | {hi:.1f} | {100 * t / tot:.1f}% |\n")
 
 
-def _per_launch(path, counter):
-    """{kernel short name: mean over dispatches of the summed counter value}."""
+def _per_launch(path, counter, counts=None):
+    """{kernel short name: mean over dispatches of the summed counter value};
+    `counts`, if given, receives the dispatches per kernel."""
     per = collections.defaultdict(float)
     names = {}
     for r in csv.DictReader(open(path)):
@@ -103,11 +129,15 @@ def _per_launch(path, counter):
     by = collections.defaultdict(list)
     for key, v in per.items():
         by[names[key]].append(v)
+    if counts is not None:
+        counts.update({k: len(v) for k, v in by.items()})
     return {k: sum(v) / len(v) for k, v in by.items()}
 
 
-def traffic(fetch_csv, write_csv, dst, kernel, copy_bytes, source, cmd_fetch, cmd_write):
-    fetch = _per_launch(fetch_csv, "FETCH_SIZE")
+def traffic(fetch_csv, write_csv, dst, kernel, copy_bytes, source, cmd_fetch, cmd_write,
+            steps=None):
+    counts = {}
+    fetch = _per_launch(fetch_csv, "FETCH_SIZE", counts)
     write = _per_launch(write_csv, "WRITE_SIZE")
     copy = next(k for k in fetch if k.startswith("k_copy"))
     sf = copy_bytes / (fetch[copy] * 1024.0)
@@ -125,6 +155,9 @@ def traffic(fetch_csv, write_csv, dst, kernel, copy_bytes, source, cmd_fetch, cm
                 f"kernel_write_kib_per_launch: {write[kernel]:.1f}\n")
         f.write(f"fetch_bytes_per_launch: {kf:.0f}\nwrite_bytes_per_launch: {kw:.0f}\n")
         f.write(f"traffic_bytes_per_launch: {kf + kw:.0f}\n")
+        L = _per_step(counts.get(kernel, 0), steps)
+        if L:
+            f.write(f"launches_per_step: {L}\ntraffic_bytes_per_step: {L * (kf + kw):.0f}\n")
         f.write("# all kernels (KiB per launch, unscaled): fetch / write\n")
         for k in sorted(fetch):
             f.write(f"#   {k}: {fetch[k]:.1f} / {write.get(k, float('nan')):.1f}\n")
@@ -293,9 +326,10 @@ def main(argv):
     if argv[0] == "stats":
         stats(*argv[1:5])
     elif argv[0] == "trace":
-        trace(*argv[1:5], int(argv[5]), int(argv[6]))
+        trace(*argv[1:5], int(argv[5]), int(argv[6]), *(int(x) for x in argv[7:8]))
     elif argv[0] == "traffic":
-        traffic(argv[1], argv[2], argv[3], argv[4], int(argv[5]), argv[6], argv[7], argv[8])
+        traffic(argv[1], argv[2], argv[3], argv[4], int(argv[5]), argv[6], argv[7], argv[8],
+                *(int(x) for x in argv[9:10]))
     elif argv[0] == "mfma":
         mfma(*argv[1:5], *(int(x) for x in argv[5:6]))
     elif argv[0] == "hbm":
