@@ -452,8 +452,17 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
     // Stored: u = x + floor(m/2) + 32 (0 <= u <= m + 64 < 2^12) in 12-bit
     // slots, the lane's 16 outputs of a 32x32 block as two 96-bit records
     // (outputs 8h .. 8h+7 in record h, output 8h + e at bits 12 e).
+    // fin is a power of two, so the reduction runs on acc itself:
+    // RN(acc * (fin RN(1/m))) = RN(v * RN(1/m)), the same quotient q;
+    // acc - q (m/fin) = x/fin is exact, and the fma that adds the offset
+    // restores x.  Two neighbouring slots are formed as one integer
+    // u0 + 4096 u1 < 2^24 by two more fmas (exact) and one conversion.
     const float ffin = (float)c.fin[mi];
     const int offi = m / 2 + 32;
+    const float finv = inv * ffin, fmf = fm / ffin;
+    // the scale of r16 at packing time: x/fin, or x after the slab sum
+    const float pf = accumulate ? 1.0f : ffin;
+    const float off1 = (float)offi, off2 = (float)(offi * 4097);
     uint32_t* dst = res + ((size_t)mi * mp * np + (size_t)tile * (TILE * TILE) +
                            (size_t)w * 8192) / 8 * 3 + lane * 6;
     uint32_t pk[4][2][6];
@@ -464,8 +473,8 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
         float r16[16];
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const float v = acc[i][j][e] * ffin;
-          r16[e] = __builtin_fmaf(-rintf(v * inv), fm, v);
+          const float a = acc[i][j][e];
+          r16[e] = __builtin_fmaf(-rintf(a * finv), fmf, a);
         }
         if (accumulate) {
           const uint2* p = reinterpret_cast<const uint2*>(dst + (i * 2 + j) * 384);
@@ -478,18 +487,25 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
             const uint32_t u = (sh + 12 <= 32 ? (ow[wi] >> sh)
                                               : __builtin_amdgcn_alignbit(ow[wi + 1], ow[wi], sh)) &
                                0xFFFu;
-            const float t = r16[e] + (float)((int)u - offi);
+            const float t = r16[e] * ffin + (float)((int)u - offi);
             r16[e] = __builtin_fmaf(-rintf(t * inv), fm, t);
           }
         }
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          uint32_t u[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) u[e] = (uint32_t)((int)r16[8 * h + e] + offi);
-          pk[i][j][3 * h] = u[0] | (u[1] << 12) | (u[2] << 24);
-          pk[i][j][3 * h + 1] = (u[2] >> 8) | (u[3] << 4) | (u[4] << 16) | (u[5] << 28);
-          pk[i][j][3 * h + 2] = (u[5] >> 4) | (u[6] << 8) | (u[7] << 20);
+          const float* x8 = r16 + 8 * h;
+          // u_e = x_e + offi; p_ab = u_a + 4096 u_b
+          const uint32_t p01 = (uint32_t)__builtin_fmaf(x8[1], pf * 4096.0f,
+                                                        __builtin_fmaf(x8[0], pf, off2));
+          const uint32_t p34 = (uint32_t)__builtin_fmaf(x8[4], pf * 4096.0f,
+                                                        __builtin_fmaf(x8[3], pf, off2));
+          const uint32_t p67 = (uint32_t)__builtin_fmaf(x8[7], pf * 4096.0f,
+                                                        __builtin_fmaf(x8[6], pf, off2));
+          const uint32_t u2 = (uint32_t)__builtin_fmaf(x8[2], pf, off1);
+          const uint32_t u5 = (uint32_t)__builtin_fmaf(x8[5], pf, off1);
+          pk[i][j][3 * h] = p01 | (u2 << 24);
+          pk[i][j][3 * h + 1] = (u2 >> 8) | (p34 << 4) | (u5 << 28);
+          pk[i][j][3 * h + 2] = (u5 >> 4) | (p67 << 8);
         }
       }
     // Every DMA issued so far (the next modulus's first stages, up to three)
