@@ -531,20 +531,27 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
 
 }  // namespace
 
-// Launch granularity: at most LAUNCH_TILES tiles (four rounds of one
-// workgroup per CU) and one modulus group per launch.  The workgroups of an
-// XCD that share A or B panels (the 4 x 8 groups of tile_of) run their
-// K-loops in step only while they started together: in one long launch the
-// dispatcher refills each CU as its workgroup ends, their starts drift apart
-// round after round, and the shared panel blocks no longer meet in L2.  A
-// new launch starts them together again (16384^3 at r = 15: 56.2 -> 61.8 TF
-// on one box; one launch per modulus alone gave 61.3).
-constexpr int LAUNCH_TILES = 1024;
+// Launch granularity: one modulus group and a few rounds of tiles per
+// launch.  The workgroups of an XCD that share A or B panels (the 4 x 8
+// groups of tile_of) run their K-loops in step only while they started
+// together: in one long launch the dispatcher refills each CU as its
+// workgroup ends, their starts drift apart round after round, and the shared
+// panel blocks no longer meet in L2.  A new launch starts them together
+// again (16384^3 at r = 15: 56.2 -> 61.8 TF on one box with four rounds per
+// launch; one launch per modulus alone gave 61.3).  Each launch also costs a
+// ramp-up and a tail, so a launch holds one round when a workgroup's run is
+// long (+0.5% at 16384^3) and four when it is short (one round per launch
+// lost 4.6% on 32768^2 x 256).  Chunks are whole multiples of 256 tiles, so
+// that tbase keeps the XCD of every workgroup and the 4 x 8 groups whole.
+static int launch_tiles(int rounds) {
+  return std::max(256, (rounds * oz2_device_cus() + 255) / 256 * 256);
+}
 
 hipError_t oz2_launch_codegemm(const Oz2Dims& d, const Oz2Layout& L, uint8_t* ws, hipStream_t s) {
   const int tiles = (d.mp / TILE) * (d.np / TILE);
-  for (int tb = 0; tb < tiles; tb += LAUNCH_TILES) {
-    dim3 grid(std::min(LAUNCH_TILES, tiles - tb), d.cslabs);
+  const int chunk = launch_tiles(4);
+  for (int tb = 0; tb < tiles; tb += chunk) {
+    dim3 grid(std::min(chunk, tiles - tb), d.cslabs);
     hipLaunchKernelGGL(k_codegemm, grid, dim3(NT), 0, s, ws + L.codesA, ws + L.codesB, d.mp,
                        d.np, d.kp, (uint32_t*)(ws + L.Rmax), (uint32_t*)(ws + L.Kmax), tb);
     const hipError_t e = hipGetLastError();
@@ -569,6 +576,7 @@ hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Con
   const int by_work = std::max(1, WG_STEPS / (3 * ksteps));
   const int mpw = std::min((c.r + fill - 1) / fill, by_work);
   const int groups = (c.r + mpw - 1) / mpw;
+  const int chunk = launch_tiles(3 * ksteps * mpw >= WG_STEPS / 2 ? 1 : 4);
   for (int kb = 0, sl = 0; kb < d.kp; kb += OZ2_KSLAB, ++sl) {
     const int ke = kb + OZ2_KSLAB < d.kp ? kb + OZ2_KSLAB : d.kp;
     // the first chain transition may skip its reduction when every modulus of
@@ -584,8 +592,8 @@ hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Con
                  int, uint32_t*) = ch == 3 ? k_resgemm<3> : ch == 2 ? k_resgemm<2>
                                            : ch == 1 ? k_resgemm<1> : k_resgemm<0>;
     for (int g = 0; g < groups; ++g)
-      for (int tb = 0; tb < tiles; tb += LAUNCH_TILES) {
-        hipLaunchKernelGGL(kern, dim3(std::min(LAUNCH_TILES, tiles - tb)), dim3(NT), 0, s, c,
+      for (int tb = 0; tb < tiles; tb += chunk) {
+        hipLaunchKernelGGL(kern, dim3(std::min(chunk, tiles - tb)), dim3(NT), 0, s, c,
                            ws + L.planesA, ws + L.planesB, d.mp, d.np, d.kp, kb, ke,
                            sl > 0 ? 1 : 0, mpw, g, tb, (uint32_t*)(ws + L.res));
         const hipError_t e = hipGetLastError();
