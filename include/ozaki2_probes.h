@@ -57,8 +57,8 @@ int ozaki2_probe_mfma_digits(int iters, double* tflops);
 int ozaki2_probe_copy_peak(size_t bytes, int reps, double* gbs);
 
 /* The reconstruction's own integer and rounding routines (the direct CRT
- * sum of Eq. (garner)'s unique integer in radix-2^38 limbs for r <= 12, in
- * 32-bit words above; one RN-even rounding) applied to n given residue
+ * sum of Eq. (garner)'s unique integer in radix-2^38 limbs, three for
+ * r <= 12 and four above; one RN-even rounding) applied to n given residue
  * vectors, for tests that reach the rare branches -- integers next to +-M/2,
  * where the quotient estimate needs the exact range check -- which random
  * products almost never produce.  The residues go through the stored form

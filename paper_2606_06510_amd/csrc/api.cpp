@@ -122,7 +122,7 @@ bool build_const(int r, Oz2Const& c) {
     Big Wi = Mi;
     Wi.mul_small((uint32_t)inv);
     for (int j = 0; j < OZ2_NLIMB; ++j) c.W[i][j] = (double)Wi.word(j);
-    for (int j = 0; j < 3; ++j) c.W38[i][j] = (double)Wi.bits(38 * j, 38);
+    for (int j = 0; j < 4; ++j) c.W38[i][j] = (double)Wi.bits(38 * j, 38);
     c.wfrac[i] = (double)inv / (double)m;   // W_i / M exactly = inv_i / m_i
   }
   c.P = pb;
@@ -156,7 +156,7 @@ bool build_const(int r, Oz2Const& c) {
     c.Ml[j] = (double)M.word(j);
     c.Mhalf[j] = (double)Mh.word(j);
   }
-  for (int j = 0; j < 3; ++j) {
+  for (int j = 0; j < 4; ++j) {
     c.M38[j] = (double)M.bits(38 * j, 38);
     c.Mhalf38[j] = (double)Mh.bits(38 * j, 38);
   }
@@ -167,13 +167,14 @@ bool build_const(int r, Oz2Const& c) {
   double Md = 0.0;
   for (int j = OZ2_NLIMB - 1; j >= 0; --j) Md = Md * 4294967296.0 + (double)M.word(j);
   c.mtop = std::ldexp(1.0, 32 * (c.nw - 1)) / Md;
-  // radix-2^38 limbs (the reconstruction of r <= 12): [-M/2, M/2) must fit
-  // 114 bits, and with |x_i| <= 545 every limb sum stays below 2^52
-  if (r <= 12 && M.bitlen() + 1 > 114) return false;
-  c.mtop38 = std::ldexp(1.0, 76) / Md;
+  // radix-2^38 limbs (the reconstruction): [-M/2, M/2) must fit three limbs
+  // (114 bits) for r <= 12 and four (152 bits) above
+  const int nl38 = r <= 12 ? 3 : 4;
+  if (M.bitlen() + 1 > 38 * nl38) return false;
+  c.mtop38 = std::ldexp(1.0, 38 * (nl38 - 1)) / Md;
   // the offsets of the stored residues, folded into the CRT sums
   // (integer sums: W38 limbs < 2^38 and W words < 2^32, offsets <= 576)
-  for (int j = 0; j < 3; ++j) {
+  for (int j = 0; j < 4; ++j) {
     int64_t k = 0;
     for (int i = 0; i < r; ++i) k += (int64_t)(ms[i] / 2 + 32) * (int64_t)c.W38[i][j];
     c.K38[j] = (double)k;   // < 2^52: exact

@@ -233,10 +233,10 @@ __device__ __forceinline__ void emit38(const Oz2Const& c, const double (&S0)[8],
       const bool flagged = ((S.fA[row] | S.fB[col]) & (OZ2_T1 | OZ2_T2)) != 0;
       if (iout) {
         if (!flagged) {
-          double s0 = S0[I], s1 = S1[I], s2 = S2[I];
-          if (crt38_reduce(c, s0, s1, s2)) crt38_fix(c, s0, s1, s2);
+          double s[3] = {S0[I], S1[I], S2[I]};
+          if (crt38_reduce<3>(c, s)) crt38_fix<3>(c, s);
           uint32_t w[4];
-          limbs38_words(s0, s1, s2, w);
+          limbs38_words<3>(s, w);
           uint32_t* o = iout + ((size_t)col * m + row) * NL;
 #pragma unroll
           for (int q = 0; q < 4; ++q) o[q] = w[q];
@@ -250,9 +250,9 @@ __device__ __forceinline__ void emit38(const Oz2Const& c, const double (&S0)[8],
         for (int l = 0; l < k; ++l) sacc = fma(A[row + (size_t)l * lda], B[l + (size_t)col * ldb], sacc);
         v = sacc;
       } else {
-        double s0 = S0[I], s1 = S1[I], s2 = S2[I];
-        if (crt38_reduce(c, s0, s1, s2)) crt38_fix(c, s0, s1, s2);
-        v = round38(s0, s1, s2, S.sS[row] + S.sT[col]);
+        double s[3] = {S0[I], S1[I], S2[I]};
+        if (crt38_reduce<3>(c, s)) crt38_fix<3>(c, s);
+        v = round38<3>(s, S.sS[row] + S.sT[col]);
       }
       C[row + (size_t)col * ldc] = v;
     }

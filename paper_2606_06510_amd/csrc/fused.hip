@@ -330,9 +330,9 @@ k_resgemm_crt(Oz2Const c, Oz2Dims d, const uint8_t* __restrict__ PA, const uint8
         const uint32_t fld = (wd >> P.shift[i]) & field_mask<R>(i);
         x[i] = (double)(int)fld - (double)(kPoolDesc[R - 1 - i] / 2 + 32);
       }
-      double S0, S1, S2;
-      crt38_sum<R>(c, x, S0, S1, S2);
-      T[cl * TRP + rr] = round38(S0, S1, S2, si + tj);
+      double S[3];
+      crt38_sum<R, 3>(c, x, S);
+      T[cl * TRP + rr] = round38<3>(S, si + tj);
       // one output at a time: interleaving several CRTs would need more
       // registers than the packed residues leave
       __builtin_amdgcn_sched_barrier(0);

@@ -288,14 +288,7 @@ struct GvOut {
     if (row < m && b < nrhs && (nofb || !((fA[row] | fB[b]) & (OZ2_T1 | OZ2_T2)))) {
       const int e = sA[row] + tB[b];
       double v;
-      if constexpr (R <= 12) {
-        v = crt38_rounded<R, I>(c, x, e);
-      } else {
-        constexpr int NW = NWords<R>::value;
-        uint32_t wds[NW];
-        crt_words<R, NW, I>(c, x, wds);
-        v = round_scaled<NW>(wds, e);
-      }
+      v = crt38_rounded<R, I>(c, x, e);
       Y[(size_t)row + (size_t)b * ldy] = v;
     }
     GvOut<R, I + 1>::run(c, x, row0, b, m, nrhs, sA, tB, fA, fB, nofb, Y, ldy);

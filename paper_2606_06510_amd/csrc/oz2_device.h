@@ -263,74 +263,117 @@ __device__ __forceinline__ double round_scaled(const uint32_t (&x)[NW], int e) {
   return sm ? -v : v;
 }
 
-// ---- r <= 12: the exact integer in three radix-2^38 fp64 limbs ----------
-// X = S2 2^76 + S1 2^38 + S0 with S0, S1 in [0, 2^38) after normalisation
-// and S2 signed; [-M/2, M/2) fits (log2 M < 113).  Every limb sum is an
-// integer below 2^52 (|x_i| <= 577, limbs of W_i and M below 2^38, at most
-// 12 terms plus the q M correction with |q| <= sum |x_i|), so the fp64
-// arithmetic is exact.
-__device__ __forceinline__ void normalise38(double& S0, double& S1, double& S2) {
-  double cy = floor(S0 * 0x1p-38);
-  S0 = fma(-cy, 0x1p38, S0);
-  S1 += cy;
-  cy = floor(S1 * 0x1p-38);
-  S1 = fma(-cy, 0x1p38, S1);
-  S2 += cy;
+// ---- the exact integer in radix-2^38 fp64 limbs --------------------------
+// X = sum_l S[l] 2^(38 l) with S[l] in [0, 2^38) for l < NB - 1 after
+// normalisation and S[NB - 1] signed; [-M/2, M/2) fits three limbs for
+// r <= 12 (log2 M < 113) and four for r <= 16 (log2 M < 148).  Every limb
+// sum is an integer below 2^53, so the fp64 arithmetic is exact: the limbs of
+// W_i and M are below 2^38, |x_i| <= 577 (or u_i <= m_i + 64 from stored
+// records, whose offsets' share K38 < 2^52 starts the sums), so with at most
+// 16 terms every partial sum stays below 2^52, and the q M correction
+// (|q| <= sum |x_i| + 1 < 2^14) keeps it below 2^53.
+template <int R>
+struct Limbs38 {
+  static constexpr int value = R <= 12 ? 3 : 4;
+};
+
+template <int NB>
+__device__ __forceinline__ void normalise38(double (&S)[NB]) {
+#pragma unroll
+  for (int l = 0; l < NB - 1; ++l) {
+    const double cy = floor(S[l] * 0x1p-38);
+    S[l] = fma(-cy, 0x1p38, S[l]);
+    S[l + 1] += cy;
+  }
 }
 
-// The normalised limbs (S0, S1 in [0, 2^38), S2 signed, |S2| < 2^37) as four
-// 32-bit words of two's complement, little endian: X = b1 2^64 + b0 with
-// b0 = S0 + (S1 mod 2^26) 2^38 and b1 = S2 2^12 + floor(S1 / 2^26).
-__device__ __forceinline__ void limbs38_words(double S0, double S1, double S2, uint32_t (&w)[4]) {
-  const unsigned long long u0 = (unsigned long long)S0, u1 = (unsigned long long)S1;
+// The normalised limbs as NB + 1 32-bit words of two's complement, little
+// endian.  Three limbs: X = b1 2^64 + b0 with b0 = S0 + (S1 mod 2^26) 2^38
+// and b1 = S2 2^12 + floor(S1 / 2^26).  Four limbs: b1 holds bits 64..127
+// (the top 12 bits of S1, S2, the low 14 bits of S3) and the fifth word
+// floor(S3 / 2^14).
+template <int NB>
+__device__ __forceinline__ void limbs38_words(const double (&S)[NB], uint32_t (&w)[NB + 1]) {
+  static_assert(NB == 3 || NB == 4, "three or four limbs");
+  const unsigned long long u0 = (unsigned long long)S[0], u1 = (unsigned long long)S[1];
   const unsigned long long b0 = u0 | (u1 << 38);
-  const long long b1 = (long long)S2 * 4096 + (long long)(u1 >> 26);
   w[0] = (uint32_t)b0;
   w[1] = (uint32_t)(b0 >> 32);
-  w[2] = (uint32_t)b1;
-  w[3] = (uint32_t)((unsigned long long)b1 >> 32);
+  if constexpr (NB == 3) {
+    const long long b1 = (long long)S[2] * 4096 + (long long)(u1 >> 26);
+    w[2] = (uint32_t)b1;
+    w[3] = (uint32_t)((unsigned long long)b1 >> 32);
+  } else {
+    const unsigned long long u2 = (unsigned long long)S[2];
+    const long long t = (long long)S[3];
+    const unsigned long long b1 = (u1 >> 26) | (u2 << 12) | ((unsigned long long)t << 50);
+    w[2] = (uint32_t)b1;
+    w[3] = (uint32_t)(b1 >> 32);
+    w[4] = (uint32_t)(t >> 14);
+  }
 }
 
-// RN-even binary64 value of X 2^-e from normalised limbs.  If S2 is in
-// [-2^15, 2^15), H = S2 2^38 + S1 is exact (|H| <= 2^53) and one fma rounds
-// H 2^38 + S0 once.  Otherwise |S2 2^38 + S1| >= 2^53, where binary64
-// rounding boundaries fall on integers, so S0 / 2^38 (in [0, 1)) can stand
-// in as a sticky half: S2 2^38 + S1 + 0.5 [S0 != 0] rounds like X / 2^38.
-// The power-of-two scaling is exact unless the result overflows (to
-// infinity, the correct rounding) or is subnormal, which takes the 32-bit
-// word routine above.
-__device__ __forceinline__ double round38(double S0, double S1, double S2, int e) {
+// RN-even binary64 value of X 2^-e from normalised limbs.  With T the top
+// limb: if T is in [-2^15, 2^15), H = T 2^38 + S[NB-2] is exact (|H| <= 2^53)
+// and stands in for the top two limbs; with three limbs one fma then rounds
+// H 2^38 + S0 once.  Otherwise |T 2^38 + S[NB-2]| >= 2^53, where binary64
+// rounding boundaries fall on integers, so the limbs below can stand in as a
+// sticky half: + 0.5 when any of them is nonzero rounds like X itself.  Four
+// limbs apply the same test once more, to H.  The power-of-two scaling is
+// exact unless the result overflows (to infinity, the correct rounding) or
+// is subnormal, which takes the 32-bit word routine above.
+template <int NB>
+__device__ __forceinline__ double round38(const double (&S)[NB], int e) {
+  static_assert(NB == 3 || NB == 4, "three or four limbs");
   double v;
   int sh;
-  if (S2 >= -0x1p15 && S2 < 0x1p15) {
-    v = fma(fma(S2, 0x1p38, S1), 0x1p38, S0);
-    sh = 0;
+  const double T = S[NB - 1];
+  if constexpr (NB == 3) {
+    if (T >= -0x1p15 && T < 0x1p15) {
+      v = fma(fma(T, 0x1p38, S[1]), 0x1p38, S[0]);
+      sh = 0;
+    } else {
+      v = fma(T, 0x1p38, S[1] + (S[0] != 0.0 ? 0.5 : 0.0));
+      sh = 38;
+    }
   } else {
-    v = fma(S2, 0x1p38, S1 + (S0 != 0.0 ? 0.5 : 0.0));
-    sh = 38;
+    if (T >= -0x1p15 && T < 0x1p15) {
+      const double H = fma(T, 0x1p38, S[2]);
+      if (H >= -0x1p15 && H < 0x1p15) {
+        v = fma(fma(H, 0x1p38, S[1]), 0x1p38, S[0]);
+        sh = 0;
+      } else {
+        v = fma(H, 0x1p38, S[1] + (S[0] != 0.0 ? 0.5 : 0.0));
+        sh = 38;
+      }
+    } else {
+      v = fma(T, 0x1p38, S[2] + ((S[1] != 0.0 || S[0] != 0.0) ? 0.5 : 0.0));
+      sh = 76;
+    }
   }
   if (v == 0.0) return 0.0;        // exact zero is +0.0
   const int ev = (int)((__double_as_longlong(v) >> 52) & 0x7ff) - 1023;   // |v| >= 1
   if (ev + sh - e < -1022) {
-    // subnormal result: X as four 32-bit words
-    uint32_t w[4];
-    limbs38_words(S0, S1, S2, w);
-    return round_scaled<4>(w, e);
+    // subnormal result: X as 32-bit words
+    uint32_t w[NB + 1];
+    limbs38_words<NB>(S, w);
+    return round_scaled<NB + 1>(w, e);
   }
   return ldexp(v, sh - e);
 }
 
-// X - qM with q = rint(X/M) from the top limbs (within 2^-36 of X/M),
-// normalised.  Returns whether the estimate lay within that of +-1/2, where
-// q may be off by one and crt38_fix settles the range exactly.
-__device__ __forceinline__ bool crt38_reduce(const Oz2Const& c, double& S0, double& S1,
-                                             double& S2) {
-  const double f = fma(S1, 0x1p-38, S2) * c.mtop38;
+// X - qM with q = rint(X/M) estimated from the top two (unnormalised) limbs:
+// the limbs dropped and the roundings move the estimate by less than 2^-24,
+// so q may be off by one only where the estimate lies within that of +-1/2.
+// Normalises, and returns whether the estimate was that close, where
+// crt38_fix settles the range exactly.  mtop38 = 2^(38 (NB - 1)) / M.
+template <int NB>
+__device__ __forceinline__ bool crt38_reduce(const Oz2Const& c, double (&S)[NB]) {
+  const double f = fma(S[NB - 2], 0x1p-38, S[NB - 1]) * c.mtop38;
   const double q = rint(f);
-  S0 = fma(-q, c.M38[0], S0);
-  S1 = fma(-q, c.M38[1], S1);
-  S2 = fma(-q, c.M38[2], S2);
-  normalise38(S0, S1, S2);
+#pragma unroll
+  for (int l = 0; l < NB; ++l) S[l] = fma(-q, c.M38[l], S[l]);
+  normalise38<NB>(S);
   return fabs(f - q) > 0.49999;
 }
 
@@ -338,78 +381,73 @@ __device__ __forceinline__ bool crt38_reduce(const Oz2Const& c, double& S0, doub
 // X >= ceil(M/2) (subtract M); N = X + floor(M/2) < 0 means X <
 // -floor(M/2) (add M); the sign of a normalised limb vector is that of its
 // top limb
-__device__ __forceinline__ void crt38_fix(const Oz2Const& c, double& S0, double& S1, double& S2) {
-  double P0 = S0 - c.M38[0] + c.Mhalf38[0], P1 = S1 - c.M38[1] + c.Mhalf38[1],
-         P2 = S2 - c.M38[2] + c.Mhalf38[2];
-  double N0 = S0 + c.Mhalf38[0], N1 = S1 + c.Mhalf38[1], N2 = S2 + c.Mhalf38[2];
-  normalise38(P0, P1, P2);
-  normalise38(N0, N1, N2);
-  const double adj = (P2 >= 0.0) ? -1.0 : ((N2 < 0.0) ? 1.0 : 0.0);
-  S0 = fma(adj, c.M38[0], S0);
-  S1 = fma(adj, c.M38[1], S1);
-  S2 = fma(adj, c.M38[2], S2);
-  normalise38(S0, S1, S2);
-}
-
-// C~ of output I of a thread (R <= 12 residues, |x_i| <= 577) rounded with the
-// exponent shift -e: the direct CRT sum in radix-2^38 limbs, the reduction by
-// the quotient estimate (with the exact range check where it is ambiguous),
-// then round38.
-// The exact integer C~ of output I of a thread (R <= 12 residues, |x_i| <= 577)
-// as normalised radix-2^38 limbs: the direct CRT sum, the reduction by the
-// quotient estimate, and the exact range check where the estimate is
-// ambiguous.  (The reconstruction rounds these limbs; the integer query of
-// the staged API exports them.)
-template <int R>
-__device__ __forceinline__ void crt38_acc(const Oz2Const& c, const double (&xi)[R], double& S0,
-                                          double& S1, double& S2) {
-  static_assert(R <= 12, "three radix-2^38 limbs hold [-M/2, M/2) only for r <= 12");
+template <int NB>
+__device__ __forceinline__ void crt38_fix(const Oz2Const& c, double (&S)[NB]) {
+  double P[NB], N[NB];
 #pragma unroll
-  for (int i = 0; i < R; ++i) {
-    S0 = fma(xi[i], c.W38[i][0], S0);
-    S1 = fma(xi[i], c.W38[i][1], S1);
-    S2 = fma(xi[i], c.W38[i][2], S2);
+  for (int l = 0; l < NB; ++l) {
+    P[l] = S[l] - c.M38[l] + c.Mhalf38[l];
+    N[l] = S[l] + c.Mhalf38[l];
   }
-}
-template <int R>
-__device__ __forceinline__ void crt38_sum(const Oz2Const& c, const double (&xi)[R], double& S0,
-                                          double& S1, double& S2) {
-  S0 = 0.0;
-  S1 = 0.0;
-  S2 = 0.0;
-  crt38_acc<R>(c, xi, S0, S1, S2);
-  if (crt38_reduce(c, S0, S1, S2)) crt38_fix(c, S0, S1, S2);
+  normalise38<NB>(P);
+  normalise38<NB>(N);
+  const double adj = (P[NB - 1] >= 0.0) ? -1.0 : ((N[NB - 1] < 0.0) ? 1.0 : 0.0);
+#pragma unroll
+  for (int l = 0; l < NB; ++l) S[l] = fma(adj, c.M38[l], S[l]);
+  normalise38<NB>(S);
 }
 
-template <int R, int I>
-__device__ __forceinline__ void crt38_limbs(const Oz2Const& c, const uint4 (&x)[R], double& S0,
-                                            double& S1, double& S2) {
+// The exact integer C~ of an output as normalised radix-2^38 limbs: the
+// direct CRT sum, the reduction by the quotient estimate, and the exact range
+// check where the estimate is ambiguous.  (The reconstruction rounds these
+// limbs; the integer query of the staged API exports them.)
+template <int R, int NB>
+__device__ __forceinline__ void crt38_acc(const Oz2Const& c, const double (&xi)[R],
+                                          double (&S)[NB]) {
+  static_assert(NB == Limbs38<R>::value, "limb count of r moduli");
+#pragma unroll
+  for (int i = 0; i < R; ++i)
+#pragma unroll
+    for (int l = 0; l < NB; ++l) S[l] = fma(xi[i], c.W38[i][l], S[l]);
+}
+template <int R, int NB>
+__device__ __forceinline__ void crt38_sum(const Oz2Const& c, const double (&xi)[R],
+                                          double (&S)[NB]) {
+#pragma unroll
+  for (int l = 0; l < NB; ++l) S[l] = 0.0;
+  crt38_acc<R, NB>(c, xi, S);
+  if (crt38_reduce<NB>(c, S)) crt38_fix<NB>(c, S);
+}
+
+// from int16 representatives (output I of the thread's eight)
+template <int R, int I, int NB>
+__device__ __forceinline__ void crt38_limbs(const Oz2Const& c, const uint4 (&x)[R],
+                                            double (&S)[NB]) {
   double xi[R];
 #pragma unroll
   for (int i = 0; i < R; ++i) xi[i] = res_at<I>(x[i]);
-  crt38_sum<R>(c, xi, S0, S1, S2);
+  crt38_sum<R, NB>(c, xi, S);
 }
 // from stored records: the limb sums start at -K38 (the offsets' share) and
 // add u_i W38[i]: the same exact integers as from the representatives
-// (partial sums below 2^52)
-template <int R, int I>
-__device__ __forceinline__ void crt38_limbs(const Oz2Const& c, const uint3 (&x)[R], double& S0,
-                                            double& S1, double& S2) {
+template <int R, int I, int NB>
+__device__ __forceinline__ void crt38_limbs(const Oz2Const& c, const uint3 (&x)[R],
+                                            double (&S)[NB]) {
   double ui[R];
 #pragma unroll
   for (int i = 0; i < R; ++i) ui[i] = slot_at<I>(x[i]);
-  S0 = -c.K38[0];
-  S1 = -c.K38[1];
-  S2 = -c.K38[2];
-  crt38_acc<R>(c, ui, S0, S1, S2);
-  if (crt38_reduce(c, S0, S1, S2)) crt38_fix(c, S0, S1, S2);
+#pragma unroll
+  for (int l = 0; l < NB; ++l) S[l] = -c.K38[l];
+  crt38_acc<R, NB>(c, ui, S);
+  if (crt38_reduce<NB>(c, S)) crt38_fix<NB>(c, S);
 }
 
 template <int R, int I, class X>
 __device__ __forceinline__ double crt38_rounded(const Oz2Const& c, const X (&x)[R], int e) {
-  double S0, S1, S2;
-  crt38_limbs<R, I>(c, x, S0, S1, S2);
-  return round38(S0, S1, S2, e);
+  constexpr int NB = Limbs38<R>::value;
+  double S[NB];
+  crt38_limbs<R, I, NB>(c, x, S);
+  return round38<NB>(S, e);
 }
 
 }  // namespace

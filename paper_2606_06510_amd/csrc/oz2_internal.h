@@ -39,13 +39,14 @@ struct Oz2Const {
   double Mhalf[OZ2_NLIMB];        // 32-bit words of floor(M/2)
   int nw;                         // words of the two's complement integer in [-M/2, M/2)
   double mtop;                    // 2^(32 (nw - 1)) / M, rounded
-  // the same in three radix-2^38 limbs (used for r <= 12, 114 bits)
-  double W38[OZ2_MAXR][3];
-  double M38[3], Mhalf38[3];
-  double mtop38;                  // 2^76 / M, rounded
+  // the same in radix-2^38 limbs: three for r <= 12 (114 bits), four above
+  // (152 bits); the reconstruction's exact integer
+  double W38[OZ2_MAXR][4];
+  double M38[4], Mhalf38[4];
+  double mtop38;                  // 2^(38 (limbs - 1)) / M, rounded
   // the staged residues are stored as u_i = x_i + floor(m_i/2) + 32 >= 0:
   // sum_i u_i W_i limb by limb minus these gives sum_i x_i W_i exactly
-  double K38[3];                  // sum_i (floor(m_i/2) + 32) W38[i][l] (exact: < 2^51)
+  double K38[4];                  // sum_i (floor(m_i/2) + 32) W38[i][l] (exact: < 2^52)
   double Kw[OZ2_NLIMB];           // sum_i (floor(m_i/2) + 32) W[i][j] (exact: < 2^46)
   int cA, cB;                     // width budgets of the scaling rule
   // residue -> plane-bytes tables: entry toff[i] + d for the centred residue d

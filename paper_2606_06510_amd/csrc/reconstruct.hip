@@ -74,17 +74,10 @@ struct Outputs {
   __device__ __forceinline__ static void run(const Oz2Const& c, const Oz2Dims& d,
                                              const uint3 (&x)[R], const BlockMap& b, int tj,
                                              const int32_t* __restrict__ sA, double (*tr)[33]) {
-    constexpr int NW = NWords<R>::value;
     const int rr = b.rb + 8 * (I >> 2) + (I & 3);
     const int row = b.row0 + rr;
     const int si = row < d.m ? sA[row] : 0;
-    if constexpr (R <= 12) {
-      tr[b.cl][rr] = crt38_rounded<R, I>(c, x, si + tj);
-    } else {
-      uint32_t w[NW];
-      crt_words<R, NW, I>(c, x, w);
-      tr[b.cl][rr] = round_scaled<NW>(w, si + tj);
-    }
+    tr[b.cl][rr] = crt38_rounded<R, I>(c, x, si + tj);
     Outputs<R, I + 1>::run(c, d, x, b, tj, sA, tr);
   }
 };
@@ -157,18 +150,15 @@ k_reconstruct(Oz2Const c, Oz2Dims d, const uint32_t* __restrict__ res,
 
 // The exact integer of output I of a thread as NL 32-bit words (two's
 // complement, little endian), formed by the routine the reconstruction
-// itself uses: radix-2^38 limbs for R <= 12, 32-bit words above.
+// itself uses: radix-2^38 limbs (three for R <= 12, four above).
 template <int R, int I, class X>
 __device__ __forceinline__ void store_integer(const Oz2Const& c, const X (&x)[R], uint32_t* o) {
-  constexpr int NW = R <= 12 ? 4 : NWords<R>::value;
+  constexpr int NB = Limbs38<R>::value, NW = NB + 1;
+  static_assert(NW <= NL, "the exported words hold the limbs");
   uint32_t w[NW];
-  if constexpr (R <= 12) {
-    double S0, S1, S2;
-    crt38_limbs<R, I>(c, x, S0, S1, S2);
-    limbs38_words(S0, S1, S2, w);
-  } else {
-    crt_words<R, NW, I>(c, x, w);
-  }
+  double S[NB];
+  crt38_limbs<R, I, NB>(c, x, S);
+  limbs38_words<NB>(S, w);
   const uint32_t ext = (uint32_t)((int32_t)w[NW - 1] >> 31);
 #pragma unroll
   for (int q = 0; q < NL; ++q) o[q] = q < NW ? w[q < NW ? q : 0] : ext;
@@ -177,14 +167,7 @@ __device__ __forceinline__ void store_integer(const Oz2Const& c, const X (&x)[R]
 // The rounded value of output I exactly as the reconstruction forms it.
 template <int R, int I, class X>
 __device__ __forceinline__ double rounded_value(const Oz2Const& c, const X (&x)[R], int e) {
-  if constexpr (R <= 12) {
-    return crt38_rounded<R, I>(c, x, e);
-  } else {
-    constexpr int NW = NWords<R>::value;
-    uint32_t w[NW];
-    crt_words<R, NW, I>(c, x, w);
-    return round_scaled<NW>(w, e);
-  }
+  return crt38_rounded<R, I>(c, x, e);
 }
 
 template <int R, int I>
@@ -192,7 +175,6 @@ struct IntOut {
   __device__ __forceinline__ static void run(const Oz2Const& c, const Oz2Dims& d,
                                              const uint3 (&x)[R], const BlockMap& b,
                                              uint32_t* out) {
-    constexpr int NW = NWords<R>::value;
     const int row = b.row0 + b.rb + 8 * (I >> 2) + (I & 3);
     const int col = b.col0 + b.cl;
     if (row < d.m && col < d.n) {
