@@ -9,18 +9,18 @@
 // as Garner's Eq. (garner).  On this VALU the direct CRT sum is cheaper than
 // Garner's r(r-1)/2 dependent modular steps:
 //     X = sum_i x_i W_i - q M,  W_i = (M/m_i) ((M/m_i)^-1 mod m_i),
-// evaluated exactly in fp64 on 32-bit words, with q = rint(sum_i x_i W_i/M)
-// (error < 2^-35; an exact range check fixes the rare ambiguous case).  The
-// x_i are any representatives of the residues with |x_i| <= m_i/2 + 32 <= 577
-// (what the residue GEMM stores): every partial word sum is then an integer
-// below 2^46 (32-bit words) or 2^51 (radix-2^38 limbs), and the quotient
-// estimate is as good for them as for centred residues.  The residue GEMMs
-// store them offset (u = x + floor(m/2) + 32, 12 bits per output): the sums
-// start at minus the offsets' share and add the u_i, which gives the same
-// integers.
-// The limbs are normalised to five 32-bit words (two's complement), and
-// rounded once to binary64 with the exponent shift -(s_i + t_j), including
-// gradual underflow and overflow.
+// evaluated exactly in radix-2^38 fp64 limbs (three for r <= 12, four
+// above), with q = rint(sum_i x_i W_i/M) estimated from the top limbs (error
+// < 2^-24; an exact range check fixes the rare ambiguous case).  The x_i are
+// any representatives of the residues with |x_i| <= m_i/2 + 32 <= 577 (what
+// the residue GEMM stores): every partial limb sum is then an integer below
+// 2^52, and the quotient estimate is as good for them as for centred
+// residues.  The residue GEMMs store them offset (u = x + floor(m/2) + 32,
+// 12 bits per output): the sums start at minus the offsets' share and add the
+// u_i, which gives the same integers.
+// The normalised limbs are rounded once to binary64 with the exponent shift
+// -(s_i + t_j), including gradual underflow (through 32-bit words) and
+// overflow.
 #include "oz2_device.h"
 
 namespace {

@@ -5,7 +5,7 @@
         [STEPS]
     python -m paper_2606_06510_amd.rocprof_summary traffic FETCH_CSV WRITE_CSV OUT_TXT \\
         KERNEL COPY_BYTES SOURCE CMD_FETCH CMD_WRITE [STEPS]
-    python -m paper_2606_06510_amd.rocprof_summary mfma COUNTER_CSV OUT_TXT SOURCE CMD [SKIP]
+    python -m paper_2606_06510_amd.rocprof_summary mfma COUNTER_CSV OUT_TXT SOURCE CMD [SKIP [STEPS]]
     python -m paper_2606_06510_amd.rocprof_summary hbm STATS_CSV FETCH_CSV WRITE_CSV OUT_MD \
         COPY_BYTES M N K R PSTORE CMD_TRACE CMD_FETCH CMD_WRITE [SKIP COUNT [ACC]]
     python -m paper_2606_06510_amd.rocprof_summary counters OUT_TXT KERNEL SOURCE SKIP UNITS \
@@ -163,7 +163,7 @@ def traffic(fetch_csv, write_csv, dst, kernel, copy_bytes, source, cmd_fetch, cm
             f.write(f"#   {k}: {fetch[k]:.1f} / {write.get(k, float('nan')):.1f}\n")
 
 
-def mfma(src, dst, source, cmd, skip=0, xcds=8, simds=1024):
+def mfma(src, dst, source, cmd, skip=0, steps=None, xcds=8, simds=1024):
     per = collections.defaultdict(lambda: collections.defaultdict(float))
     names, dur, start = {}, {}, {}
     for r in csv.DictReader(open(src)):
@@ -177,7 +177,9 @@ def mfma(src, dst, source, cmd, skip=0, xcds=8, simds=1024):
         order[names[key]].append((start[key], key))
     keep = set()
     for name, ks in order.items():
-        keep.update(key for _, key in sorted(ks)[skip:])
+        # SKIP counts steps when STEPS is given: L launches per step each
+        L = (_per_step(len(ks), steps) or 1) if steps else 1
+        keep.update(key for _, key in sorted(ks)[L * skip:])
     by = collections.defaultdict(list)
     for key, v in per.items():
         if key not in keep:
@@ -186,7 +188,7 @@ def mfma(src, dst, source, cmd, skip=0, xcds=8, simds=1024):
             continue
         cycles = v["GRBM_GUI_ACTIVE"] / xcds
         by[names[key]].append((dur[key], v["SQ_INSTS_VALU_MFMA_MOPS_F8"] * 512.0,
-                               v["SQ_VALU_MFMA_BUSY_CYCLES"] / (cycles * simds), cycles / dur[key]))
+                               v["SQ_VALU_MFMA_BUSY_CYCLES"], cycles))
     sha = hashlib.sha256(open(source, "rb").read()).hexdigest()
     with open(dst, "w") as f:
         f.write("# FP8 MFMA activity per launch: rocprofv3 SQ_INSTS_VALU_MFMA_MOPS_F8 (x 512 = FP8\n"
@@ -194,7 +196,9 @@ def mfma(src, dst, source, cmd, skip=0, xcds=8, simds=1024):
                 f"# the {xcds} XCDs for the clock.\n")
         f.write(f"command: {cmd}\nkernel_source: {source}\nkernel_source_sha256: {sha}\n")
         if skip:
-            f.write(f"# the first {skip} launches of each kernel (warm-up) are left out\n")
+            f.write(f"# the first {skip} {'steps' if steps else 'launches'} of each kernel "
+                    "(warm-up) are left out\n")
+        f.write("# busy share and clock are summed over the launches (weighted by their cycles)\n")
         f.write("| kernel | launches | avg (us) | FP8 ops per launch | TFLOP/s | MFMA busy | clock (GHz) |\n")
         f.write("|---|---|---|---|---|---|---|\n")
         for k in sorted(by):
@@ -202,8 +206,10 @@ def mfma(src, dst, source, cmd, skip=0, xcds=8, simds=1024):
             n = len(xs)
             d = sum(x[0] for x in xs) / n
             fl = sum(x[1] for x in xs) / n
+            cyc = sum(x[3] for x in xs)
             f.write(f"| {k} | {n} | {d * 1e6:.1f} | {fl:.4g} | {fl / d / 1e12:.0f} | "
-                    f"{100 * sum(x[2] for x in xs) / n:.1f}% | {sum(x[3] for x in xs) / n / 1e9:.2f} |\n")
+                    f"{100 * sum(x[2] for x in xs) / (cyc * simds):.1f}% | "
+                    f"{cyc / sum(x[0] for x in xs) / 1e9:.2f} |\n")
 
 
 def _algorithmic(m, n, k, r, pstore, acc=False):
@@ -331,7 +337,7 @@ def main(argv):
         traffic(argv[1], argv[2], argv[3], argv[4], int(argv[5]), argv[6], argv[7], argv[8],
                 *(int(x) for x in argv[9:10]))
     elif argv[0] == "mfma":
-        mfma(*argv[1:5], *(int(x) for x in argv[5:6]))
+        mfma(*argv[1:5], *(int(x) for x in argv[5:7]))
     elif argv[0] == "hbm":
         hbm(argv[1], argv[2], argv[3], argv[4], int(argv[5]), *map(int, argv[6:11]),
             argv[11], argv[12], argv[13], *(int(x) for x in argv[14:16]),
