@@ -369,6 +369,122 @@ __device__ __forceinline__ void chain_scale(v16f (&acc)[4][2], float f) {
     for (int j = 0; j < 2; ++j) acc[i][j] *= f;
 }
 
+// Residue-GEMM epilogue: a representative of fin * acc (+ the previous
+// slab's) mod m, in fp32 throughout.  acc is an integer with |acc| <= 2^24
+// and fin is 1 or 16, so v = fin * acc is exact.  v * RN(1/m) is within
+// 2 * 2^-24 |v| / m <= 32 / m of v / m (the relative errors of RN(1/m) and of
+// the product), so x = v - m rint(.) is an exact integer of magnitude
+// <= m/2 + 32.  The reconstruction's exact CRT sum takes any representative
+// of that size (the canonical centring is left to the diagnostic residue
+// query).  With a previous slab, the sum (|.| <= m + 64) is reduced once
+// more: its quotient estimate is then within 2^-22 of the exact one, so the
+// result lies in [-m/2, m/2].
+// Stored: u = x + floor(m/2) + 32 (0 <= u <= m + 64 < 2^12) in 12-bit slots,
+// the lane's 16 outputs of a 32x32 block as two 96-bit records (outputs
+// 8h .. 8h+7 in record h, output 8h + e at bits 12 e).  fin is a power of
+// two, so the reduction runs on acc itself: RN(acc * (fin RN(1/m))) =
+// RN(v * RN(1/m)), the same quotient q; acc - q (m/fin) = x/fin is exact, and
+// the fma that adds the offset restores x.  Two neighbouring slots are formed
+// as one integer u0 + 4096 u1 < 2^24 by two more fmas (exact) and one
+// conversion.  dst: the lane's records of the wave's 128 x 64 outputs.
+__device__ __forceinline__ void pack_residues(const Oz2Const& c, int mi, const v16f (&acc)[4][2],
+                                              int accumulate, const uint32_t* dst,
+                                              uint32_t (&pk)[4][2][6]) {
+  const int m = c.m[mi];
+  const float fm = (float)m, inv = c.finv[mi];
+  const float ffin = (float)c.fin[mi];
+  const int offi = m / 2 + 32;
+  const float finv = inv * ffin, fmf = fm / ffin;
+  // the scale of r16 at packing time: x/fin, or x after the slab sum
+  const float pf = accumulate ? 1.0f : ffin;
+  const float off1 = (float)offi, off2 = (float)(offi * 4097);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      float r16[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float a = acc[i][j][e];
+        r16[e] = __builtin_fmaf(-rintf(a * finv), fmf, a);
+      }
+      if (accumulate) {
+        const uint2* p = reinterpret_cast<const uint2*>(dst + (i * 2 + j) * 384);
+        const uint2 o0 = p[0], o1 = p[1], o2 = p[2];
+        const uint32_t ow[7] = {o0.x, o0.y, o1.x, o1.y, o2.x, o2.y, 0u};
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          // slot e % 8 of record e / 8 (words 3 (e / 8) ..)
+          const int bit = 96 * (e >> 3) + 12 * (e & 7), wi = bit >> 5, sh = bit & 31;
+          const uint32_t u = (sh + 12 <= 32 ? (ow[wi] >> sh)
+                                            : __builtin_amdgcn_alignbit(ow[wi + 1], ow[wi], sh)) &
+                             0xFFFu;
+          const float t = r16[e] * ffin + (float)((int)u - offi);
+          r16[e] = __builtin_fmaf(-rintf(t * inv), fm, t);
+        }
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float* x8 = r16 + 8 * h;
+        // u_e = x_e + offi; p_ab = u_a + 4096 u_b
+        const uint32_t p01 = (uint32_t)__builtin_fmaf(x8[1], pf * 4096.0f,
+                                                      __builtin_fmaf(x8[0], pf, off2));
+        const uint32_t p34 = (uint32_t)__builtin_fmaf(x8[4], pf * 4096.0f,
+                                                      __builtin_fmaf(x8[3], pf, off2));
+        const uint32_t p67 = (uint32_t)__builtin_fmaf(x8[7], pf * 4096.0f,
+                                                      __builtin_fmaf(x8[6], pf, off2));
+        const uint32_t u2 = (uint32_t)__builtin_fmaf(x8[2], pf, off1);
+        const uint32_t u5 = (uint32_t)__builtin_fmaf(x8[5], pf, off1);
+        pk[i][j][3 * h] = p01 | (u2 << 24);
+        pk[i][j][3 * h + 1] = (u2 >> 8) | (p34 << 4) | (u5 << 28);
+        pk[i][j][3 * h + 2] = (u5 >> 4) | (p67 << 8);
+      }
+    }
+}
+
+// The non-temporal stores of pack_residues' records: nothing in the launch
+// reads them, and with a short k (a few stages per modulus) they drain
+// measurably faster.
+__device__ __forceinline__ void store_residues(uint32_t* dst, const uint32_t (&pk)[4][2][6]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      u32x2* p = reinterpret_cast<u32x2*>(dst + (i * 2 + j) * 384);
+#pragma unroll
+      for (int q = 0; q < 3; ++q)
+        __builtin_nontemporal_store(u32x2{pk[i][j][2 * q], pk[i][j][2 * q + 1]}, p + q);
+    }
+}
+
+// The same records stored as whole 16-byte pieces: each 32 x 32 block's
+// 1536 bytes pass through the wave's 1.5 KiB of LDS (written at their
+// offsets in the block, read back 16 contiguous bytes per lane), so that a
+// store instruction covers 1 KiB of consecutive addresses instead of 64
+// pieces of 8 bytes at a 24-byte stride (the rank-256 update's residue
+// GEMMs: about 4% faster).  The wave alone uses its buffer: no barrier.
+__device__ __forceinline__ void store_residues_lds(uint32_t* dst, const uint32_t (&pk)[4][2][6],
+                                                   uint8_t* buf) {
+  const int lane = threadIdx.x & 63;
+  uint32_t* wb = dst - lane * 6;   // the block's first record
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      u32x2* b2 = reinterpret_cast<u32x2*>(buf + lane * 24);
+#pragma unroll
+      for (int q = 0; q < 3; ++q) b2[q] = u32x2{pk[i][j][2 * q], pk[i][j][2 * q + 1]};
+      wait_lgkm0();
+      const u32x4 v0 = reinterpret_cast<const u32x4*>(buf)[lane];
+      u32x4 v1 = u32x4{0u, 0u, 0u, 0u};
+      if (lane < 32) v1 = reinterpret_cast<const u32x4*>(buf + 1024)[lane];
+      wait_lgkm0();
+      u32x4* g = reinterpret_cast<u32x4*>(wb + (i * 2 + j) * 384);
+      __builtin_nontemporal_store(v0, g + lane);
+      if (lane < 32) __builtin_nontemporal_store(v1, g + 64 + lane);
+    }
+}
+
 // ------------------------------------------------------------- residue GEMM
 // grid: (tiles tbase .. tbase + gridDim.x - 1, 1).  Workgroup t computes
 // moduli mgroup*mpw .. min(r, (mgroup+1)*mpw) - 1 of tile tbase + t over k in
@@ -439,93 +555,187 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
     }
     it += 3 * nk;
 
-    // epilogue: a representative of fin * acc (+ the previous slab's) mod m,
-    // in fp32 throughout.  acc is an integer with |acc| <= 2^24 and fin is 1
-    // or 16, so v = fin * acc is exact.  v * RN(1/m) is within
-    // 2 * 2^-24 |v| / m <= 32 / m of v / m (the relative errors of RN(1/m)
-    // and of the product), so x = v - m rint(.) is an exact integer of
-    // magnitude <= m/2 + 32.  The reconstruction's exact CRT sum takes any
-    // representative of that size (the canonical centring is left to the
-    // diagnostic residue query).  With a previous slab, the sum (|.| <= m +
-    // 64) is reduced once more: its quotient estimate is then within 2^-22
-    // of the exact one, so the result lies in [-m/2, m/2].
-    // Stored: u = x + floor(m/2) + 32 (0 <= u <= m + 64 < 2^12) in 12-bit
-    // slots, the lane's 16 outputs of a 32x32 block as two 96-bit records
-    // (outputs 8h .. 8h+7 in record h, output 8h + e at bits 12 e).
-    // fin is a power of two, so the reduction runs on acc itself:
-    // RN(acc * (fin RN(1/m))) = RN(v * RN(1/m)), the same quotient q;
-    // acc - q (m/fin) = x/fin is exact, and the fma that adds the offset
-    // restores x.  Two neighbouring slots are formed as one integer
-    // u0 + 4096 u1 < 2^24 by two more fmas (exact) and one conversion.
-    const float ffin = (float)c.fin[mi];
-    const int offi = m / 2 + 32;
-    const float finv = inv * ffin, fmf = fm / ffin;
-    // the scale of r16 at packing time: x/fin, or x after the slab sum
-    const float pf = accumulate ? 1.0f : ffin;
-    const float off1 = (float)offi, off2 = (float)(offi * 4097);
     uint32_t* dst = res + ((size_t)mi * mp * np + (size_t)tile * (TILE * TILE) +
                            (size_t)w * 8192) / 8 * 3 + lane * 6;
     uint32_t pk[4][2][6];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        float r16[16];
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float a = acc[i][j][e];
-          r16[e] = __builtin_fmaf(-rintf(a * finv), fmf, a);
-        }
-        if (accumulate) {
-          const uint2* p = reinterpret_cast<const uint2*>(dst + (i * 2 + j) * 384);
-          const uint2 o0 = p[0], o1 = p[1], o2 = p[2];
-          const uint32_t ow[7] = {o0.x, o0.y, o1.x, o1.y, o2.x, o2.y, 0u};
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            // slot e % 8 of record e / 8 (words 3 (e / 8) ..)
-            const int bit = 96 * (e >> 3) + 12 * (e & 7), wi = bit >> 5, sh = bit & 31;
-            const uint32_t u = (sh + 12 <= 32 ? (ow[wi] >> sh)
-                                              : __builtin_amdgcn_alignbit(ow[wi + 1], ow[wi], sh)) &
-                               0xFFFu;
-            const float t = r16[e] * ffin + (float)((int)u - offi);
-            r16[e] = __builtin_fmaf(-rintf(t * inv), fm, t);
-          }
-        }
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const float* x8 = r16 + 8 * h;
-          // u_e = x_e + offi; p_ab = u_a + 4096 u_b
-          const uint32_t p01 = (uint32_t)__builtin_fmaf(x8[1], pf * 4096.0f,
-                                                        __builtin_fmaf(x8[0], pf, off2));
-          const uint32_t p34 = (uint32_t)__builtin_fmaf(x8[4], pf * 4096.0f,
-                                                        __builtin_fmaf(x8[3], pf, off2));
-          const uint32_t p67 = (uint32_t)__builtin_fmaf(x8[7], pf * 4096.0f,
-                                                        __builtin_fmaf(x8[6], pf, off2));
-          const uint32_t u2 = (uint32_t)__builtin_fmaf(x8[2], pf, off1);
-          const uint32_t u5 = (uint32_t)__builtin_fmaf(x8[5], pf, off1);
-          pk[i][j][3 * h] = p01 | (u2 << 24);
-          pk[i][j][3 * h + 1] = (u2 >> 8) | (p34 << 4) | (u5 << 28);
-          pk[i][j][3 * h + 2] = (u5 >> 4) | (p67 << 8);
-        }
-      }
+    pack_residues(c, mi, acc, accumulate, dst, pk);
     // Every DMA issued so far (the next modulus's first stages, up to three)
     // has landed before the stores go out; those stages then skip their wait,
-    // and the wait of the stage after them also covers the stores.  The
-    // stores are non-temporal: nothing in this launch reads them, and with a
-    // short k (a few stages per modulus) they drain measurably faster.
+    // and the wait of the stage after them also covers the stores.
     wait_vm<0>();
     landed = it + 3;
+    store_residues(dst, pk);
+  }
+  if (!g) bar();
+  wait_vm<0>();
+}
+
+
+// ------------------------------------------- residue GEMM, two workgroups per CU
+// For short k (a workgroup walks many moduli of its tile, each a handful of
+// K-stages) the per-modulus work outside the MFMAs -- chain transitions, the
+// epilogue and its stores -- is as long as the modulus's MFMAs, and the
+// lockstep ping-pong of k_resgemm cannot overlap it.  This variant gives each
+// CU two independent workgroups instead: 256 threads (4 waves, 1 per SIMD),
+// one 256 x 128 half of a 256 x 256 tile, a 3-deep ring of 24 KiB stages
+// (72 KiB of LDS), one barrier per stage.  While one workgroup's waves run a
+// transition, an epilogue or wait for LDS, the other's keep the SIMDs'
+// matrix units busy.  Wave v computes the same 128 x 64 outputs (and stores
+// them in the same records) as wave w = 4 (v / 2) + 2 h + v % 2 of k_resgemm
+// for half h.  The DMA stream: stage = A tile (16 blocks of 16 rows x 64 B)
+// + the half's B tile (8 blocks); wave v moves A blocks v + 4j (j < 4) and B
+// blocks v + 4j (j < 2).
+constexpr int DSTB = OPB + OPB / 2;   // 24 KiB per stage
+constexpr int DNB = 3;                // ring depth
+constexpr int DNT = 256;
+constexpr int DLDS = DNB * DSTB + 4 * 1536;   // + the waves' store staging (78 KiB)
+
+struct DuoDma {
+  const uint8_t* pa;
+  const uint8_t* pb;
+  int left, q, mi;
+  uint32_t vo;   // lane offset of block v in a stage (VGPR)
+  uint32_t mv;   // v * 1 KiB (uniform)
+};
+
+__device__ __forceinline__ void duo_issue(const Oz2Const* c, const Ctx& x, DuoDma& d,
+                                          uint32_t lbase) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) dma16(d.pa + 4096 * j, d.vo, lbase + d.mv + 4096u * j);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) dma16(d.pb + 4096 * j, d.vo, lbase + OPB + d.mv + 4096u * j);
+  d.pa += x.kbA;
+  d.pb += x.kbB;
+  if (--d.left == 0) {
+    d.left = x.nk;
+    if (++d.q == 3) {
+      d.q = 0;
+      ++d.mi;
+    }
+    if (d.mi < x.mi1) {
+      const int s = c->sq[d.mi], p0 = c->pbase[d.mi];
+      d.pa = x.a0 + (size_t)(p0 + planeA(s, d.q)) * x.psA;
+      d.pb = x.b0 + (size_t)(p0 + planeB(s, d.q)) * x.psB;
+    }
+  }
+}
+
+// Stages [it0, it0 + n): wait for this wave's share of stage t (issued two
+// stages ahead: six DMA instructions per stage, returning in order; stages
+// below `landed` are known to be in LDS), barrier (every share of stage t
+// landed, every wave done reading stage t - 1), refill the slot of stage
+// t - 1 with stage t + 2, then the fragments and the 8 MFMAs of stage t.
+__device__ __forceinline__ void duo_run(const Oz2Const* c, const Ctx& x, DuoDma& dm,
+                                        const uint8_t* LB, uint32_t lds0, int it0, int n,
+                                        int landed, int wr, int wc, v16f (&acc)[4][2]) {
+  const int T = x.T;
+  const int lane = threadIdx.x & 63;
+  const int h = lane >> 5, sw = swz(lane & 31);
+  const int o0 = 16 * ((2 * h) ^ sw), o1 = 16 * ((2 * h + 1) ^ sw);
+  for (int it = it0; it < it0 + n; ++it) {
+    if (it >= landed) {
+      if (it + 1 < T) wait_vm<6>();
+      else wait_vm<0>();
+    }
+    bar();
+    if (it + 2 < T) duo_issue(c, x, dm, lds0 + ((it + 2) % DNB) * DSTB);
+    const uint8_t* st = LB + (it % DNB) * DSTB;
+    const uint8_t* sa = st + (wr * 128 + (lane & 31)) * KS;
+    const uint8_t* sb = st + OPB + (wc * 64 + (lane & 31)) * KS;
+    v8i fa[4], fb[2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) fa[i] = ldfrag(sa + i * 32 * KS, o0, o1);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) fb[j] = ldfrag(sb + j * 32 * KS, o0, o1);
+    wait_lgkm0();
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        u32x2* p = reinterpret_cast<u32x2*>(dst + (i * 2 + j) * 384);
-#pragma unroll
-        for (int q = 0; q < 3; ++q)
-          __builtin_nontemporal_store(u32x2{pk[i][j][2 * q], pk[i][j][2 * q + 1]}, p + q);
-      }
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[i], fb[j], acc[i][j], 0, 0,
+                                                                   0, 0, 0, 0);
   }
-  if (!g) bar();
+}
+
+// grid: 2 x (tiles tbase .. tbase + gridDim.x / 2 - 1), the two halves of a
+// tile on the same XCD (blocks b and b + 8); the tile count of a launch is a
+// multiple of 8.
+template <int CH>
+__global__ void __launch_bounds__(DNT, 2)
+k_resgemm_duo(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict__ PB, int mp,
+              int np, int kp, int kbeg, int kend, int accumulate, int mpw, int mgroup, int tbase,
+              uint32_t* __restrict__ res) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t LB[];
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)LB;
+  const int ntm = mp / TILE, ntn = np / TILE;
+  const int b = blockIdx.x, slot = b >> 3, half = slot & 1;
+  const int tile = tile_of(tbase + (slot >> 1) * 8 + (b & 7), ntm, ntn);
+  const int mi0 = mgroup * mpw, mi1 = min(c.r, mi0 + mpw);
+  const int tm = tile % ntm, tn = tile / ntm;
+  Ctx x;
+  x.psA = (size_t)mp * kp;
+  x.psB = (size_t)np * kp;
+  x.kbA = (size_t)mp * KS;
+  x.kbB = (size_t)np * KS;
+  x.a0 = PA + (size_t)tm * TILE * KS + (size_t)(kbeg / KS) * x.kbA;
+  x.b0 = PB + (size_t)(tn * TILE + half * (TILE / 2)) * KS + (size_t)(kbeg / KS) * x.kbB;
+  x.nk = (kend - kbeg) / KS;
+  x.T = 3 * x.nk * (mi1 - mi0);
+  x.mi1 = mi1;
+  const int nk = x.nk;
+  const int lane = threadIdx.x & 63;
+  const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wr = v >> 1, wc = v & 1, w = 4 * wr + 2 * half + wc;
+  DuoDma dm;
+  {
+    const int rb = lane >> 2;
+    dm.vo = (uint32_t)(rb * KS + 16 * ((lane & 3) ^ swz(rb))) + (uint32_t)v * 1024u;
+    dm.mv = (uint32_t)v * 1024u;
+    dm.left = nk;
+    dm.q = 0;
+    dm.mi = mi0;
+    const int s = c.sq[mi0], p0 = c.pbase[mi0];
+    dm.pa = x.a0 + (size_t)(p0 + planeA(s, 0)) * x.psA;
+    dm.pb = x.b0 + (size_t)(p0 + planeB(s, 0)) * x.psB;
+  }
+  for (int t = 0; t < DNB - 1; ++t)
+    if (t < x.T) duo_issue(&c, x, dm, lds0 + t * DSTB);
+
+  int it = 0, landed = 0;
+  for (int mi = mi0; mi < mi1; ++mi) {
+    const int m = c.m[mi], s = c.sq[mi];
+    const float fm = (float)m, inv = c.finv[mi];
+    v16f acc[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = v16f{0.f};
+    // the chains of k_resgemm
+    if (s) {
+      duo_run(&c, x, dm, LB, lds0, it, 2 * nk, landed, wr, wc, acc);
+      if (CH & 1) chain_scale(acc, (float)s);
+      else chain_reduce(acc, inv, fm, (float)s);
+      duo_run(&c, x, dm, LB, lds0, it + 2 * nk, nk, landed, wr, wc, acc);
+    } else {
+      duo_run(&c, x, dm, LB, lds0, it, nk, landed, wr, wc, acc);
+      if (CH & 2) chain_scale(acc, -16.0f);
+      else chain_reduce(acc, inv, fm, (float)c.rho0[mi]);
+      duo_run(&c, x, dm, LB, lds0, it + nk, nk, landed, wr, wc, acc);
+      chain_reduce(acc, inv, fm, (float)c.rho1[mi]);
+      duo_run(&c, x, dm, LB, lds0, it + 2 * nk, nk, landed, wr, wc, acc);
+    }
+    it += 3 * nk;
+    uint32_t* dst = res + ((size_t)mi * mp * np + (size_t)tile * (TILE * TILE) +
+                           (size_t)w * 8192) / 8 * 3 + lane * 6;
+    uint32_t pk[4][2][6];
+    pack_residues(c, mi, acc, accumulate, dst, pk);
+    // the DMAs issued so far (the next modulus's first two stages) land
+    // before the stores go out; those stages skip their wait, and the wait
+    // of the stage after them also covers the stores
+    wait_vm<0>();
+    landed = it + 2;
+    store_residues_lds(dst, pk, LB + DNB * DSTB + v * 1536);
+  }
   wait_vm<0>();
 }
 
@@ -543,6 +753,10 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
 // long (+0.5% at 16384^3) and four when it is short (one round per launch
 // lost 4.6% on 32768^2 x 256).  Chunks are whole multiples of 256 tiles, so
 // that tbase keeps the XCD of every workgroup and the 4 x 8 groups whole.
+// the two-workgroups-per-CU residue GEMM runs products of at most this many
+// K-stages (k <= 64 DUO_MAX_KSTEPS per slab)
+constexpr int DUO_MAX_KSTEPS = 8;
+
 static int launch_tiles(int rounds) {
   return std::max(256, (rounds * oz2_device_cus() + 255) / 256 * 256);
 }
@@ -588,12 +802,20 @@ hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Con
       else ns_cheap = ns_cheap && ok;
     }
     const int ch = (sq_cheap ? 1 : 0) | (ns_cheap ? 2 : 0);
-    void (*kern)(Oz2Const, const uint8_t*, const uint8_t*, int, int, int, int, int, int, int, int,
-                 int, uint32_t*) = ch == 3 ? k_resgemm<3> : ch == 2 ? k_resgemm<2>
-                                           : ch == 1 ? k_resgemm<1> : k_resgemm<0>;
+    typedef void (*Kern)(Oz2Const, const uint8_t*, const uint8_t*, int, int, int, int, int, int,
+                         int, int, int, uint32_t*);
+    const bool duo = tiles % 8 == 0 && (ke - kb) / KS <= DUO_MAX_KSTEPS;
+    Kern kern = duo ? (ch == 3 ? k_resgemm_duo<3> : ch == 2 ? k_resgemm_duo<2>
+                       : ch == 1 ? k_resgemm_duo<1> : k_resgemm_duo<0>)
+                    : (ch == 3 ? k_resgemm<3> : ch == 2 ? k_resgemm<2>
+                       : ch == 1 ? k_resgemm<1> : k_resgemm<0>);
+    const int lds = duo ? DLDS : 0;
+    if (duo) (void)hipFuncSetAttribute((const void*)kern,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     for (int g = 0; g < groups; ++g)
       for (int tb = 0; tb < tiles; tb += chunk) {
-        hipLaunchKernelGGL(kern, dim3(std::min(chunk, tiles - tb)), dim3(NT), 0, s, c,
+        const int nt = std::min(chunk, tiles - tb);
+        hipLaunchKernelGGL(kern, dim3(duo ? 2 * nt : nt), dim3(duo ? DNT : NT), lds, s, c,
                            ws + L.planesA, ws + L.planesB, d.mp, d.np, d.kp, kb, ke,
                            sl > 0 ? 1 : 0, mpw, g, tb, (uint32_t*)(ws + L.res));
         const hipError_t e = hipGetLastError();

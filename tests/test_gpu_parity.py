@@ -439,6 +439,27 @@ def test_moduli_per_workgroup_grids(shape, r):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("shape,r,acc", [((1024, 512, 200), 12, False), ((1000, 500, 448), 15, False),
+                                         ((1024, 512, 256), 12, True), ((2048, 1024, 512), 9, False)])
+def test_short_k_two_workgroups_per_cu(shape, r, acc):
+    """Short k (at most 8 K-stages per product) on a tile count divisible by
+    8: the residue GEMMs run as two workgroups per CU, each on one 256 x 128
+    half of a tile.  Every stage is compared with the oracle (codes, scales,
+    planes, residue representatives, C), including the accumulate route and
+    ragged m, n and k."""
+    m, n, k = shape
+    if acc:
+        A, B, Cin = synth.rankk(m, n, k, seed=m + n + k)
+        res = oracle.dgemm(A, B, r, C_in=Cin)
+        plan, C = run_staged(A, B, r, flags=1, C_in=Cin)
+        compare_C(C, A, B, res, C_in=Cin)
+        return
+    A, B = synth.lognormal(m, n, k, seed=m + n + k + r)
+    res = oracle.dgemm(A, B, r)
+    plan, C = run_staged(A, B, r)
+    compare_all(plan, C, A, B, r, res, check_integers=m * n <= 600000)
+
+
 def test_subnormal_and_overflowing_results():
     """Rows and columns scaled so that one block of C lies in the subnormal
     range and another overflows: the GPU's gradual-underflow rounding path and
