@@ -179,7 +179,7 @@ def main():
     log(f"{warmup} warm-up steps done")
 
     # timed steps: HIP events around the residue GEMMs (the dominant kernel:
-    # one launch per modulus group, 1024-tile chunk and k-slab) on the stream
+    # one launch per modulus group, chunk of tiles and k-slab) on the stream
     # they are launched on
     gev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -297,7 +297,7 @@ def main():
                      "traffic": None if traffic is None else round(traffic),
                      "per_step": f"{fp8_flop:.4g} FP8 FLOP (3r plane products x 2mnk)"
                                  + ("" if fused else ", over all residue-GEMM launches of the "
-                                    "step (one per modulus group, 1024-tile chunk and "
+                                    "step (one per modulus group, chunk of 256 or 1024 tiles and "
                                     f"k-slab; {slabs} k-slab{'s' if slabs > 1 else ''})"),
                      "timing": f"HIP events around the {'fused kernel' if fused else 'residue GEMMs'}"
                                f" in each of the {args.steps} timed steps (first launch start "
