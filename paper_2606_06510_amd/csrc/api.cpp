@@ -976,14 +976,17 @@ int ozaki2_plan_query(ozaki2_plan_t p, int what, void* host_out, size_t bytes) {
       return OZ2_OK;
     }
     case OZ2_Q_RESIDUES: {
-      // [tile][wave 8][x 4][y 2][lane 64][2 records of 3 words] per modulus,
-      // output 8h + e of a lane in slot e of record h, as x + floor(m/2) + 32
-      // -> the representative x itself, [r][n][m]
+      // [tile][wave 8][x 4][y 2] blocks of 384 words per modulus holding
+      // each lane's 2 records of 3 words (word w of lane L at 6 L + w, or
+      // pair-major at 128 (w / 2) + 2 L + w % 2: oz2_pair_records), output
+      // 8h + e of a lane in slot e of record h, as x + floor(m/2) + 32 -> the
+      // representative x itself, [r][n][m]
       const size_t plane = (size_t)d.mp * d.np / 8 * 3;
       std::vector<uint32_t> raw((size_t)p->c.r * plane);
       if (!cp(raw.data(), ws + L.res, raw.size() * 4)) return OZ2_E_DEVICE;
       int16_t* o = (int16_t*)out;
       const int ntm = d.mp / OZ2_TILE;
+      const bool pair = oz2_pair_records(d);
       for (int i = 0; i < p->c.r; ++i)
         for (size_t t = 0; t < (size_t)d.mp * d.np / 16; ++t) {
           const size_t tile = t >> 12;
@@ -993,7 +996,10 @@ int ozaki2_plan_query(ozaki2_plan_t p, int what, void* host_out, size_t bytes) {
           const int row = tm * OZ2_TILE + (w >> 2) * 128 + 32 * x + 4 * (lane >> 5);
           const int col = tn * OZ2_TILE + (w & 3) * 64 + 32 * y + (lane & 31);
           if (col >= d.n) continue;
-          const uint32_t* rec = raw.data() + (size_t)i * plane + t * 6;
+          const uint32_t* blkw = raw.data() + (size_t)i * plane + (t >> 6) * 384;
+          uint32_t rec[6];
+          for (int w = 0; w < 6; ++w)
+            rec[w] = blkw[pair ? 128 * (w / 2) + 2 * lane + w % 2 : 6 * lane + w];
           for (int e = 0; e < 16; ++e) {
             const int rr = row + 8 * (e >> 2) + (e & 3);
             if (rr >= d.m) continue;

@@ -381,7 +381,9 @@ __device__ __forceinline__ void chain_scale(v16f (&acc)[4][2], float f) {
 // result lies in [-m/2, m/2].
 // Stored: u = x + floor(m/2) + 32 (0 <= u <= m + 64 < 2^12) in 12-bit slots,
 // the lane's 16 outputs of a 32x32 block as two 96-bit records (outputs
-// 8h .. 8h+7 in record h, output 8h + e at bits 12 e).  fin is a power of
+// 8h .. 8h+7 in record h, output 8h + e at bits 12 e); lane-major here
+// (the lane's six words at 6 L: accumulate reads them so), pair-major in
+// the short-k kernel (store_residues_pair).  fin is a power of
 // two, so the reduction runs on acc itself: RN(acc * (fin RN(1/m))) =
 // RN(v * RN(1/m)), the same quotient q; acc - q (m/fin) = x/fin is exact, and
 // the fma that adds the offset restores x.  Two neighbouring slots are formed
@@ -457,31 +459,20 @@ __device__ __forceinline__ void store_residues(uint32_t* dst, const uint32_t (&p
     }
 }
 
-// The same records stored as whole 16-byte pieces: each 32 x 32 block's
-// 1536 bytes pass through the wave's 1.5 KiB of LDS (written at their
-// offsets in the block, read back 16 contiguous bytes per lane), so that a
-// store instruction covers 1 KiB of consecutive addresses instead of 64
-// pieces of 8 bytes at a 24-byte stride (the rank-256 update's residue
-// GEMMs: about 4% faster).  The wave alone uses its buffer: no barrier.
-__device__ __forceinline__ void store_residues_lds(uint32_t* dst, const uint32_t (&pk)[4][2][6],
-                                                   uint8_t* buf) {
+// The short-k kernel's records, pair-major (oz2_pair_records): word pair q
+// of lane L at 8-byte slot 64 q + L of the block, so that each of the three
+// non-temporal stores writes 512 consecutive bytes.  wb: the wave's records
+// (8 blocks of 384 words).
+__device__ __forceinline__ void store_residues_pair(uint32_t* wb, const uint32_t (&pk)[4][2][6]) {
   const int lane = threadIdx.x & 63;
-  uint32_t* wb = dst - lane * 6;   // the block's first record
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      u32x2* b2 = reinterpret_cast<u32x2*>(buf + lane * 24);
+      u32x2* p = reinterpret_cast<u32x2*>(wb + (i * 2 + j) * 384) + lane;
 #pragma unroll
-      for (int q = 0; q < 3; ++q) b2[q] = u32x2{pk[i][j][2 * q], pk[i][j][2 * q + 1]};
-      wait_lgkm0();
-      const u32x4 v0 = reinterpret_cast<const u32x4*>(buf)[lane];
-      u32x4 v1 = u32x4{0u, 0u, 0u, 0u};
-      if (lane < 32) v1 = reinterpret_cast<const u32x4*>(buf + 1024)[lane];
-      wait_lgkm0();
-      u32x4* g = reinterpret_cast<u32x4*>(wb + (i * 2 + j) * 384);
-      __builtin_nontemporal_store(v0, g + lane);
-      if (lane < 32) __builtin_nontemporal_store(v1, g + 64 + lane);
+      for (int q = 0; q < 3; ++q)
+        __builtin_nontemporal_store(u32x2{pk[i][j][2 * q], pk[i][j][2 * q + 1]}, p + 64 * q);
     }
 }
 
@@ -581,14 +572,13 @@ k_resgemm(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restrict_
 // (72 KiB of LDS), one barrier per stage.  While one workgroup's waves run a
 // transition, an epilogue or wait for LDS, the other's keep the SIMDs'
 // matrix units busy.  Wave v computes the same 128 x 64 outputs (and stores
-// them in the same records) as wave w = 4 (v / 2) + 2 h + v % 2 of k_resgemm
-// for half h.  The DMA stream: stage = A tile (16 blocks of 16 rows x 64 B)
+// them in the same blocks, pair-major) as wave w = 4 (v / 2) + 2 h + v % 2 of
+// k_resgemm for half h.  The DMA stream: stage = A tile (16 blocks of 16 rows x 64 B)
 // + the half's B tile (8 blocks); wave v moves A blocks v + 4j (j < 4) and B
 // blocks v + 4j (j < 2).
 constexpr int DSTB = OPB + OPB / 2;   // 24 KiB per stage
 constexpr int DNB = 3;                // ring depth
 constexpr int DNT = 256;
-constexpr int DLDS = DNB * DSTB + 4 * 1536;   // + the waves' store staging (78 KiB)
 
 struct DuoDma {
   const uint8_t* pa;
@@ -725,16 +715,16 @@ k_resgemm_duo(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restr
       duo_run(&c, x, dm, LB, lds0, it + 2 * nk, nk, landed, wr, wc, acc);
     }
     it += 3 * nk;
-    uint32_t* dst = res + ((size_t)mi * mp * np + (size_t)tile * (TILE * TILE) +
-                           (size_t)w * 8192) / 8 * 3 + lane * 6;
+    uint32_t* wb = res + ((size_t)mi * mp * np + (size_t)tile * (TILE * TILE) +
+                          (size_t)w * 8192) / 8 * 3;
     uint32_t pk[4][2][6];
-    pack_residues(c, mi, acc, accumulate, dst, pk);
+    pack_residues(c, mi, acc, 0, wb, pk);   // a single slab: nothing to add
     // the DMAs issued so far (the next modulus's first two stages) land
     // before the stores go out; those stages skip their wait, and the wait
     // of the stage after them also covers the stores
     wait_vm<0>();
     landed = it + 2;
-    store_residues_lds(dst, pk, LB + DNB * DSTB + v * 1536);
+    store_residues_pair(wb, pk);
   }
   wait_vm<0>();
 }
@@ -753,10 +743,6 @@ k_resgemm_duo(Oz2Const c, const uint8_t* __restrict__ PA, const uint8_t* __restr
 // long (+0.5% at 16384^3) and four when it is short (one round per launch
 // lost 4.6% on 32768^2 x 256).  Chunks are whole multiples of 256 tiles, so
 // that tbase keeps the XCD of every workgroup and the 4 x 8 groups whole.
-// the two-workgroups-per-CU residue GEMM runs products of at most this many
-// K-stages (k <= 64 DUO_MAX_KSTEPS per slab)
-constexpr int DUO_MAX_KSTEPS = 8;
-
 static int launch_tiles(int rounds) {
   return std::max(256, (rounds * oz2_device_cus() + 255) / 256 * 256);
 }
@@ -804,12 +790,12 @@ hipError_t oz2_launch_resgemm(const Oz2Dims& d, const Oz2Layout& L, const Oz2Con
     const int ch = (sq_cheap ? 1 : 0) | (ns_cheap ? 2 : 0);
     typedef void (*Kern)(Oz2Const, const uint8_t*, const uint8_t*, int, int, int, int, int, int,
                          int, int, int, uint32_t*);
-    const bool duo = tiles % 8 == 0 && (ke - kb) / KS <= DUO_MAX_KSTEPS;
+    const bool duo = oz2_pair_records(d);
     Kern kern = duo ? (ch == 3 ? k_resgemm_duo<3> : ch == 2 ? k_resgemm_duo<2>
                        : ch == 1 ? k_resgemm_duo<1> : k_resgemm_duo<0>)
                     : (ch == 3 ? k_resgemm<3> : ch == 2 ? k_resgemm<2>
                        : ch == 1 ? k_resgemm<1> : k_resgemm<0>);
-    const int lds = duo ? DLDS : 0;
+    const int lds = duo ? DNB * DSTB : 0;
     if (duo) (void)hipFuncSetAttribute((const void*)kern,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     for (int g = 0; g < groups; ++g)

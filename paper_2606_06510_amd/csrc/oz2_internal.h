@@ -65,6 +65,16 @@ struct Oz2Dims {
   unsigned flags;
 };
 
+// Short k (one slab of at most 8 K-stages) on a tile count divisible by 8:
+// the residue GEMMs run as two workgroups per CU and store each 32x32
+// block's records pair-major (word w of lane L at 128 (w / 2) + 2 L + w % 2;
+// otherwise lane-major, at 6 L + w).  Pair-major stores and loads took the
+// rank-256 update's residue GEMMs and reconstruction from 11.2 / 7.8 to
+// 10.9 / 7.5 ms; the long-k kernel keeps its lane-major stores.
+__host__ __device__ inline bool oz2_pair_records(const Oz2Dims& d) {
+  return ((d.mp / OZ2_TILE) * (d.np / OZ2_TILE)) % 8 == 0 && d.kp <= 8 * OZ2_KBLK;
+}
+
 // Workspace carve-up (byte offsets from the workspace base).
 struct Oz2Layout {
   size_t rowbits, colbits;    // uint64 [mp] / [np]: max |x| bit patterns

@@ -29,11 +29,14 @@ namespace {
 // leaves, per modulus, each 32x32 output block (wave w of a 256x256 tile,
 // sub-block x, y) as 1024 12-bit slots in its accumulator order: lane L holds
 // 16 outputs of column L%32, rows 4(L/32) + 8(e/4) + e%4, e = 0..15, as two
-// 96-bit records (e = 0..7, e = 8..15).  Here two threads share a lane's 16
-// (t = 2L + h takes record h), so the 128 threads of a block read 1.5 KiB
-// contiguous per modulus; a workgroup of 256 takes two blocks.
+// 96-bit records (e = 0..7, e = 8..15), six words w = 0..5 per lane, stored
+// lane-major or pair-major (oz2_pair_records).  Here two threads share a
+// lane's 16 (t = 2L + h takes record h: words 3h .. 3h + 2), so the 128
+// threads of a block read its 1.5 KiB per modulus; a workgroup of 256 takes
+// two blocks.
 struct BlockMap {
-  size_t roff;      // word offset of the thread's record in a modulus plane
+  size_t roff;      // word offset of the block in a modulus plane
+  int lane, h;      // the record: lane L's record h
   int row0, col0;   // block origin in C
   int cl;           // column within the block
   int rb;           // row within the block of output i: rb + 8(i/4) + i%4
@@ -56,21 +59,39 @@ __device__ __forceinline__ BlockMap block_map(int mp) {
   const int lane = b.tt >> 1, h = b.tt & 1;
   b.cl = lane & 31;
   b.rb = 4 * (lane >> 5) + 16 * h;
-  b.roff = tile * (OZ2_TILE * OZ2_TILE / 8 * 3) + (size_t)blk * 384 + (size_t)b.tt * 3;
+  b.roff = tile * (OZ2_TILE * OZ2_TILE / 8 * 3) + (size_t)blk * 384;
+  b.lane = lane;
+  b.h = h;
   return b;
 }
 
-// the thread's record of each modulus (plane: words per modulus).  The
-// residues, C_in and C are each touched once: non-temporal loads and stores
-// (3-4% faster reconstruction on the 16384^3 and rank-256 workloads).
-template <int R>
+// the thread's record of each modulus (plane: words per modulus).
+// Lane-major: words 6 L + 3 h .. + 2, one 12-byte load.  Pair-major: record
+// 0 is words 0, 1 (8 bytes at 2 L) and 2 (at 128 + 2 L), record 1 words 3
+// (at 129 + 2 L) and 4, 5 (8 bytes at 256 + 2 L).  The residues, C_in and C
+// are each touched once: non-temporal loads and stores (3-4% faster
+// reconstruction on the 16384^3 and rank-256 workloads).
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+template <int R, bool PAIR>
 __device__ __forceinline__ void load_residues(const uint32_t* __restrict__ res, size_t plane,
-                                              size_t roff, uint3 (&x)[R]) {
+                                              const BlockMap& b, uint3 (&x)[R]) {
+  if constexpr (PAIR) {
+    const int o2 = b.h ? 256 + 2 * b.lane : 2 * b.lane, o1 = 128 + 2 * b.lane + b.h;
 #pragma unroll
-  for (int i = 0; i < R; ++i) {
-    const uint32_t* q = res + (size_t)i * plane + roff;
-    x[i] = make_uint3(__builtin_nontemporal_load(q), __builtin_nontemporal_load(q + 1),
-                      __builtin_nontemporal_load(q + 2));
+    for (int i = 0; i < R; ++i) {
+      const uint32_t* q = res + (size_t)i * plane + b.roff;
+      const u32x2 p = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(q + o2));
+      const uint32_t w = __builtin_nontemporal_load(q + o1);
+      x[i] = b.h ? make_uint3(w, p.x, p.y) : make_uint3(p.x, p.y, w);
+    }
+  } else {
+    const int o = 6 * b.lane + 3 * b.h;
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      const uint32_t* q = res + (size_t)i * plane + b.roff + o;
+      x[i] = make_uint3(__builtin_nontemporal_load(q), __builtin_nontemporal_load(q + 1),
+                        __builtin_nontemporal_load(q + 2));
+    }
   }
 }
 
@@ -100,8 +121,10 @@ struct Outputs<R, 8> {
 // flagged rows of A into a contiguous panel (row r at panel[r + l cap]), read
 // once here instead of once per column tile there (nothing to do on inputs
 // without flagged rows).  ACC (OZ2_ACCUMULATE): C_in is loaded before the
-// CRT work, so that its latency hides behind it.
-template <int R, bool ACC>
+// CRT work, so that its latency hides behind it.  PAIR: the records are
+// pair-major (oz2_pair_records; a separate instantiation, which measured
+// 0.4 ms faster on the rank-256 update than one kernel reading both).
+template <int R, bool ACC, bool PAIR>
 __global__ void __launch_bounds__(256)
 k_reconstruct(Oz2Const c, Oz2Dims d, const uint32_t* __restrict__ res,
               const int32_t* __restrict__ sA, const int32_t* __restrict__ tB,
@@ -124,7 +147,7 @@ k_reconstruct(Oz2Const c, Oz2Dims d, const uint32_t* __restrict__ res,
   }
   {
     uint3 x[R];
-    load_residues<R>(res, (size_t)d.mp * d.np / 8 * 3, b.roff, x);
+    load_residues<R, PAIR>(res, (size_t)d.mp * d.np / 8 * 3, b, x);
     const int col = b.col0 + b.cl;
     const int tj = col < d.n ? tB[col] : 0;
     Outputs<R, 0>::run(c, d, x, b, tj, sA, tr[b.hb]);
@@ -201,7 +224,8 @@ __global__ void __launch_bounds__(256)
 k_integers(Oz2Const c, Oz2Dims d, const uint32_t* __restrict__ res, uint32_t* out) {
   const BlockMap b = block_map(d.mp);
   uint3 x[R];
-  load_residues<R>(res, (size_t)d.mp * d.np / 8 * 3, b.roff, x);
+  if (oz2_pair_records(d)) load_residues<R, true>(res, (size_t)d.mp * d.np / 8 * 3, b, x);
+  else load_residues<R, false>(res, (size_t)d.mp * d.np / 8 * 3, b, x);
   IntOut<R, 0>::run(c, d, x, b, out);
 }
 
@@ -358,7 +382,9 @@ void launch_reconstruct_r(const Oz2Dims& d, const Oz2Layout& L, const Oz2Const& 
                           const double* A, int lda, double* C, int ldc, hipStream_t s) {
   const size_t blocks = (size_t)d.mp * d.np / 2048;
   const bool gather = !(d.flags & 8u);   // OZ2_NO_FALLBACK: no fallback, no panel
-  auto kern = (d.flags & 1u) ? k_reconstruct<R, true> : k_reconstruct<R, false>;
+  const bool pair = oz2_pair_records(d);
+  auto kern = (d.flags & 1u) ? (pair ? k_reconstruct<R, true, true> : k_reconstruct<R, true, false>)
+                             : (pair ? k_reconstruct<R, false, true> : k_reconstruct<R, false, false>);
   hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), 0, s, c, d,
                      (const uint32_t*)(ws + L.res), (const int32_t*)(ws + L.sA),
                      (const int32_t*)(ws + L.tB), (const uint32_t*)(ws + L.flagsA),
