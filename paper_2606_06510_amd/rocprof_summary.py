@@ -222,8 +222,10 @@ def _algorithmic(m, n, k, r, pstore, acc=False):
         "k_scan_codes_cols": 9 * eb,
         "k_rebase": 2 * (ea + eb),                # code bytes read and rewritten in place
         "k_split": (8 + pstore) * (ea + eb),      # operand read, plane bytes written
-        # 12-bit residues read, FP64 written (and read when accumulating)
-        f"void k_reconstruct<{r}, {'true' if acc else 'false'}>": 3 * r * m * n // 2 + (16 if acc else 8) * m * n,
+        # 12-bit residues read, FP64 written (and read when accumulating);
+        # one instantiation per residue layout (lane-major, pair-major)
+        **{f"void k_reconstruct<{r}, {'true' if acc else 'false'}, {pair}>":
+           3 * r * m * n // 2 + (16 if acc else 8) * m * n for pair in ("false", "true")},
     }
 
 
