@@ -395,8 +395,7 @@ def stationary_line(args, cfg, r, dev, A, B):
                                f"r={r} moduli (alpha={3 * r}), new B each step",
                    "m": m, "n": n, "k": k, "num_moduli": r},
         "roofline": {"bound": "mfma",
-                     "kernel": ("k_resgemm_crt (residue GEMMs fused with the reconstruction)"
-                                if fused else "k_resgemm (residue GEMMs, 3r FP8 products)"),
+                     "kernel": "k_resgemm (residue GEMMs, 3r FP8 products)",
                      "achieved": round(achieved, 2), "peak": FP8_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
                      "traffic": None},
