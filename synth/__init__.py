@@ -36,7 +36,8 @@ def _exp(x):
     """Elementwise exp of a float64 array.  Evaluated with torch's vectorised,
     multi-threaded CPU kernel when torch is importable (numpy's takes over a
     minute for the 2^28 entries of a 16384^2 matrix on some hosts; the two
-    agree to the bit on the values checked), else with numpy."""
+    can differ by an ulp on some entries, so every consumer of these inputs
+    draws them through this function), else with numpy."""
     try:
         import torch
     except ImportError:  # pragma: no cover
