@@ -414,6 +414,21 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
     }
     quantise8(xa, S.sS[row], t2a, S.qa);
     quantise8(xb, S.sT[row], t2b, S.qb);
+    // The workgroup's next problem: one 8-byte load per thread touches each
+    // of its 128-byte lines of A (threads 0..255: column t/4, rows 16 (t%4)
+    // ..) and B (threads 256..511), so that they sit in L2 when that problem
+    // starts (its loads are otherwise the only memory latency a problem
+    // exposes).  The value is consumed by an empty asm after this problem's
+    // outputs are written: no effect on the results.
+    double touch = 0.0;
+    {
+      const size_t bn = (size_t)b + gridDim.x;
+      const int tl = t & 255, col = tl >> 2, seg = 16 * (tl & 3);
+      if (bn < (size_t)batch) {
+        if (t < 256 && col < k && seg < m) touch = A[bn * strideA + (size_t)col * lda + seg];
+        if (t >= 256 && col < n && seg < k) touch = B[bn * strideB + (size_t)col * ldb + seg];
+      }
+    }
     if constexpr (R <= 12) {
       // each modulus's residues go straight into the CRT sums (three
       // radix-2^38 limbs per output)
@@ -434,6 +449,7 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
       if (t2b && row < n) atomicOr(&S.fB[row], OZ2_T2);
       __syncthreads();
       emit38(c, S0, S1, S2, S, rb0, cb0, m, n, k, Ab, lda, Bb, ldb, Cb, ldc, Ib);
+      asm volatile("" ::"v"(touch));
     } else {
       // residues of every modulus: one uint4 (8 int16 outputs) per modulus
       uint4 res[R];
@@ -449,6 +465,7 @@ k_batched(Oz2Const c, int m, int n, int k, int batch, const double* __restrict__
       if (t2b && row < n) atomicOr(&S.fB[row], OZ2_T2);
       __syncthreads();
       Emit<R, 0>::run(c, res, S, rb0, cb0, m, n, k, Ab, lda, Bb, ldb, Cb, ldc, Ib);
+      asm volatile("" ::"v"(touch));
     }
   }
 }
