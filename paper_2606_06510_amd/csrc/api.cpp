@@ -123,6 +123,9 @@ bool build_const(int r, Oz2Const& c) {
     Wi.mul_small((uint32_t)inv);
     for (int j = 0; j < OZ2_NLIMB; ++j) c.W[i][j] = (double)Wi.word(j);
     for (int j = 0; j < 4; ++j) c.W38[i][j] = (double)Wi.bits(38 * j, 38);
+    Big Wf = Mi;
+    Wf.mul_small((uint32_t)((inv * c.fin[i]) % m));
+    for (int j = 0; j < 4; ++j) c.W38f[i][j] = (double)Wf.bits(38 * j, 38);
     c.wfrac[i] = (double)inv / (double)m;   // W_i / M exactly = inv_i / m_i
   }
   c.P = pb;

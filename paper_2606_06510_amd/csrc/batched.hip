@@ -189,20 +189,20 @@ __device__ __forceinline__ uint4 modulus_products(const Oz2Const& c, int i, cons
 }
 
 // r <= 12: output 4q + e's residue of modulus i, reduced once, added into its
-// CRT sums.  The chain value v (|v| < 2^16, exact) times fin, reduced with
-// the fp32 quotient estimate, lies within m/2 + 1 of zero: any representative
-// of magnitude <= 577 serves the sums, whose limbs stay below 2^52.
+// CRT sums.  The chain value v (|v| < 2^16, exact) is congruent to C~/fin mod
+// m; reduced with the fp32 quotient estimate it lies within m/2 + 1 of zero,
+// and the sums take it times the weights of fin W_i (W38f), which gives the
+// same integers mod M as fin v times W_i.  Any representative of magnitude
+// <= 577 serves the sums, whose limbs stay below 2^52.
 __device__ __forceinline__ void crt_add(const Oz2Const& c, int i, const v4f (&acc)[2],
                                         double (&S0)[8], double (&S1)[8], double (&S2)[8]) {
-  const float fm = (float)c.m[i], inv = c.finv[i], fin = (float)c.fin[i];
-  const bool scaled = c.fin[i] != 1;
-  const double w0 = c.W38[i][0], w1 = c.W38[i][1], w2 = c.W38[i][2];
+  const float fm = (float)c.m[i], inv = c.finv[i];
+  const double w0 = c.W38f[i][0], w1 = c.W38f[i][1], w2 = c.W38f[i][2];
 #pragma unroll
   for (int q = 0; q < 2; ++q)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      float v = acc[q][e];
-      if (scaled) v = __builtin_fmaf(-rintf(v * inv), fm, v) * fin;
+      const float v = acc[q][e];
       const double x = (double)__builtin_fmaf(-rintf(v * inv), fm, v);
       const int I = 4 * q + e;
       S0[I] = fma(x, w0, S0[I]);

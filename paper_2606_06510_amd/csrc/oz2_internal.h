@@ -42,6 +42,9 @@ struct Oz2Const {
   // the same in radix-2^38 limbs: three for r <= 12 (114 bits), four above
   // (152 bits); the reconstruction's exact integer
   double W38[OZ2_MAXR][4];
+  // the same for fin_i W_i mod M = (M/m_i) ((fin_i (M/m_i)^-1) mod m_i): a
+  // representative of C~/fin_i mod m_i times these gives the same sum mod M
+  double W38f[OZ2_MAXR][4];
   double M38[4], Mhalf38[4];
   double mtop38;                  // 2^(38 (limbs - 1)) / M, rounded
   // the staged residues are stored as u_i = x_i + floor(m_i/2) + 32 >= 0:
