@@ -38,6 +38,7 @@ constexpr int FTR = 8 * 32 * TRP * 8;    // the epilogue's transposition (66 KiB
 // the fourth word of every output's packed residues lives in LDS (64 KiB:
 // [wave][output][lane]); the other three stay in registers
 constexpr int FPK3 = FTR;
+static_assert(FNB * FSTB <= FTR, "the ring lies inside the transposition's space");
 constexpr int FLDS = FPK3 + 8 * 32 * 64 * 4;
 
 __device__ __forceinline__ void bar() {
@@ -311,16 +312,38 @@ k_resgemm_crt(Oz2Const c, Oz2Dims d, const uint8_t* __restrict__ PA, const uint8
   const bool accum = (d.flags & 1u) != 0;   // OZ2_ACCUMULATE
   const bool nofb = (d.flags & 8u) != 0;    // OZ2_NO_FALLBACK
   const bool force = (d.flags & 16u) != 0;  // OZ2_FORCE_FALLBACK
+  // every per-row and per-column value the half needs is loaded before its
+  // CRT work, with no divergent branch around a load, so that the loads'
+  // latency is paid once and hidden behind the CRT (the scale and flag
+  // arrays hold mp and np entries: the tile's padded rows and columns are in
+  // bounds; C_in's address is clamped to the matrix, and what is read for a
+  // padded or flagged output is never stored)
+  const int srow = row0 + (lane & 31);     // the store layout's row of this lane
+  const int crow = srow < d.m ? srow : d.m - 1;
+  const uint32_t fa = fA[srow];
+  const bool rok = srow < d.m && (nofb || !(force || (fa & (OZ2_T1 | OZ2_T2))));
 #pragma unroll
   for (int y = 0; y < 2; ++y) {
     const int col0 = tn * FT + wc * 64 + 32 * y;
-    const int col = col0 + cl;
-    const int tj = col < d.n ? tB[col] : 0;
+    const int tj = tB[col0 + cl];
+    int si[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) si[e] = sA[row0 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3)];
+    // the store layout: column col0 + 2 j + lane / 32 of row srow
+    uint32_t okm = 0;
+    double cin[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int cj = col0 + 2 * j + (lane >> 5);
+      const uint32_t fb = fB[cj];
+      okm |= (rok && cj < d.n && (nofb || !(fb & (OZ2_T1 | OZ2_T2)))) ? 1u << j : 0u;
+      cin[j] = 0.0;
+      if (accum)
+        cin[j] = __builtin_nontemporal_load(C + (size_t)(cj < d.n ? cj : d.n - 1) * ldc + crow);
+    }
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
       const int rr = 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-      const int row = row0 + rr;
-      const int si = row < d.m ? sA[row] : 0;
       double x[R];
       constexpr Pack P = Packing<R>::p;
       const uint32_t w3 = pk3[(16 * y + e) * 64];
@@ -332,21 +355,19 @@ k_resgemm_crt(Oz2Const c, Oz2Dims d, const uint8_t* __restrict__ PA, const uint8
       }
       double S[3];
       crt38_sum<R, 3>(c, x, S);
-      T[cl * TRP + rr] = round38<3>(S, si + tj);
+      T[cl * TRP + rr] = round38<3>(S, si[e] + tj);
       // one output at a time: interleaving several CRTs would need more
       // registers than the packed residues leave
       __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
-    const int rr = lane & 31, row = row0 + rr;
-    const bool rok = row < d.m && (nofb || !(force || (fA[row] & (OZ2_T1 | OZ2_T2))));
+    const int rr = lane & 31;
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int cc = 2 * j + (lane >> 5), cj = col0 + cc;
-      if (rok && cj < d.n && (nofb || !(fB[cj] & (OZ2_T1 | OZ2_T2)))) {
-        double* o = C + (size_t)cj * ldc + row;
+      if ((okm >> j) & 1u) {
         const double v = T[cc * TRP + rr];
-        *o = accum ? *o + v : v;
+        __builtin_nontemporal_store(accum ? cin[j] + v : v, C + (size_t)cj * ldc + srow);
       }
     }
     __syncthreads();
