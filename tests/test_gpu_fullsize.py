@@ -139,6 +139,24 @@ def test_rankk32768x256_accumulate_sampled():
     _free()
 
 
+def test_rankk32768x256_fused_accumulate_sampled():
+    """The fused reconstruction epilogue (OZ2_FUSED) on the full rank-256
+    update: 65536 tiles of 128 x 128 in one launch, C_in read and C written by
+    the epilogue; sampled entries (the first and last rows and columns among
+    them) bit-exact against the oracle."""
+    import paper_2606_06510_amd as oz
+    A, B, C0 = synth.make("rankk32768x256")
+    rng = np.random.default_rng(11)
+    rows = np.unique(np.concatenate([rng.choice(32768, 200, replace=False), [0, 32767]]))
+    cols = np.unique(np.concatenate([rng.choice(32768, 200, replace=False), [0, 32767]]))
+    plan, Cd = _run(A, B, 12, flags=oz.OZ2_ACCUMULATE | oz.OZ2_FUSED, C_in=C0)
+    C = _sample_C(Cd, rows, cols)
+    res = oracle.dgemm(A, B, 12, rows=rows, cols=cols, C_in=C0)
+    assert np.array_equal(bits(C), bits(res.C))
+    del plan, Cd
+    _free()
+
+
 def test_outputs_beyond_2_pow_31():
     """65536 x 40000 outputs (2.6e9, above 2^31) at k = 64: C, the staged
     residues (12 x 2.6e9 12-bit slots, 47 GB) and the launch grids all need 64-bit
