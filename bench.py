@@ -536,13 +536,9 @@ def gemv_line(args, cfg, r, dev):
         res = oracle.dgemm(A, X, r, rows=rows, mode="fixed")
         dt = time.perf_counter() - tc
         Y = Yd.index_select(0, torch.as_tensor(rows, device=dev)).cpu().numpy()
-        try:
-            from threadpoolctl import threadpool_info
-            cores = max([tp.get("num_threads", 1) for tp in threadpool_info()] + [1])
-        except Exception:  # pragma: no cover
-            cores = os.cpu_count()
+        hi = host_info()
         cpu = {"value": round(2.0 * k * nrhs * len(rows) / dt / 1e12, 9), "unit": "TFLOPS",
-               "cores": cores,
+               "cores": hi["cores"], "blas": hi["blas"], "cpu_model": hi["cpu_model"],
                "kind": "oracle", "sample": f"{len(rows)} sampled rows x {nrhs} columns, full k; "
                                            f"{dt:.2f} s",
                "sample_bitexact": f"{int(np.sum(Y.view(np.uint64) == res.C.view(np.uint64)))}/{Y.size}"}
@@ -573,6 +569,30 @@ def plan_pstore(r):
     return sum(2 if int(round(x ** 0.5)) ** 2 == x else 3 for x in ms)
 
 
+def host_info():
+    """Threads of the host BLAS, its name and version, and the CPU model: the
+    oracle's products run on them."""
+    cores, blas = os.cpu_count(), None
+    try:
+        from threadpoolctl import threadpool_info
+        pools = [t for t in threadpool_info() if t.get("user_api") == "blas"] or threadpool_info()
+        cores = max([t.get("num_threads", 1) for t in pools] + [1])
+        if pools:
+            blas = f"{pools[0].get('internal_api', '?')} {pools[0].get('version', '')}".strip()
+    except Exception:  # pragma: no cover
+        pass
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
+    return {"cores": cores, "blas": blas, "cpu_model": model}
+
+
 def cpu_baseline(A, B, r, Cd, nsamp, mode="bound", C_in=None):
     """The oracle, as it stands, on a bounded sample: nsamp sampled rows x nsamp
     sampled columns of the same workload (the scales of a sampled row need its
@@ -582,11 +602,7 @@ def cpu_baseline(A, B, r, Cd, nsamp, mode="bound", C_in=None):
     import oracle
     from oracle import refgemm
     import paper_2606_06510_amd as oz
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([t.get("num_threads", 1) for t in threadpool_info()] + [1])
-    except Exception:  # pragma: no cover
-        cores = os.cpu_count()
+    hi = host_info()
     m, k = A.shape
     n = B.shape[1]
     rng = np.random.default_rng(1234)
@@ -604,7 +620,7 @@ def cpu_baseline(A, B, r, Cd, nsamp, mode="bound", C_in=None):
     ratio = None if C_in is not None else refgemm.componentwise_ratio(
         C.ravel()[:1024], A, B, rr.ravel()[:1024], cc.ravel()[:1024])
     return {"value": round(2.0 * k * len(rows) * len(cols) / dt / 1e12, 9), "unit": "TFLOPS",
-            "cores": cores, "kind": "oracle",
+            "cores": hi["cores"], "kind": "oracle", "blas": hi["blas"], "cpu_model": hi["cpu_model"],
             "sample": f"{len(rows)}x{len(cols)} output entries (sampled rows x cols) of the same "
                       f"workload, full k={k}; {dt:.2f} s",
             "sample_bitexact": f"{same}/{C.size}",
